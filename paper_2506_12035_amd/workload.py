@@ -1,0 +1,240 @@
+"""Seeded synthetic MAR-shaped workloads.
+
+This module only draws random numbers and lays them out; it holds none of the
+method's arithmetic (no layer norm, projection, attention, selection or mask
+schedule).  Both the HIP path and the fp64 oracle take their inputs from here,
+so the two sides see identical values.
+
+The paper measures class-conditional ImageNet 256x256 generation with trained
+MAR-B/L/H weights (Section 5.1).  Neither the dataset nor the weights exist
+here, so seeded tensors with the same shapes stand in for them:
+
+* token layout: ``n_buf`` buffer tokens at indices ``[0, n_buf)`` followed by
+  the image tokens ``[n_buf, N)`` (16x16 = 256 image tokens, or 32x32 = 1024
+  for the high-resolution stress shape);
+* linear weights and biases ~ N(0, 0.02^2); LayerNorm gamma = 1 + N(0, 0.02^2),
+  beta ~ N(0, 0.02^2); all rounded once to the storage dtype;
+* embeddings (class embedding per image, one "generated value" embedding per
+  image token, the mask embedding and the positional embedding) ~ N(0, 1);
+* a random generation order per image (Section 3, the permutation pi).
+
+Random streams: ``SeedSequence(seed)`` is spawned into four children
+(weights, state, orders, planted); the weights child is spawned again, once per
+layer, so any single layer can be regenerated without the others.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field, replace
+from typing import Dict, List, Optional
+
+import numpy as np
+
+SEED_BASE = 2506120350
+
+STREAM_WEIGHTS, STREAM_STATE, STREAM_ORDERS, STREAM_PLANTED = range(4)
+
+LAYER_PARAM_NAMES = (
+    "ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
+    "ln2_g", "ln2_b", "w_1", "b_1", "w_2", "b_2",
+)
+
+
+@dataclass(frozen=True)
+class Config:
+    """Shape and policy of one synthetic workload."""
+
+    cid: int
+    name: str
+    n_layers: int
+    d_model: int
+    n_heads: int
+    head_dim: int
+    d_mlp: int
+    n_tokens: int
+    n_buf: int
+    batch: int
+    dtype: str                 # storage / compute dtype of the path: "f32" or "bf16"
+    n_steps: int = 64          # decoding steps of the mask schedule
+    ratio_bp: int = 1000       # refresh budget: basis points of the candidate tokens
+    sel_layer: int = 2         # 1-based layer whose attention feeds the refresh selection
+    full_every: int = 3        # periodic full refresh period (0 = only the first step)
+    ln_eps: float = 1e-6
+    weight_std: float = 0.02
+    seed: Optional[int] = None
+
+    @property
+    def n_img(self) -> int:
+        return self.n_tokens - self.n_buf
+
+    @property
+    def seed_value(self) -> int:
+        return SEED_BASE + self.cid if self.seed is None else self.seed
+
+    def with_(self, **kw) -> "Config":
+        return replace(self, **kw)
+
+
+# The five workload shapes.  Id 1 is the single-block fp32 case, ids 2-4 are
+# MAR-B/L/H-shaped decoder stacks (the model scales of Table 1), id 5 is a
+# 32x32-token high-resolution stress shape with long KV.
+CONFIGS: Dict[int, Config] = {
+    1: Config(1, "single-block-d768-fp32", 1, 768, 12, 64, 3072, 320, 64, 1, "f32",
+              n_steps=1, ratio_bp=0, sel_layer=1, full_every=0),
+    2: Config(2, "mar-b-d768-L24-B64", 24, 768, 12, 64, 3072, 320, 64, 64, "bf16"),
+    3: Config(3, "mar-l-d1024-L32-B128", 32, 1024, 16, 64, 4096, 320, 64, 128, "bf16"),
+    4: Config(4, "mar-h-d1280-L40-B256", 40, 1280, 16, 80, 5120, 320, 64, 256, "bf16"),
+    5: Config(5, "hires-d1024-L32-N1088-B32", 32, 1024, 16, 64, 4096, 1088, 64, 32, "bf16"),
+}
+
+# Refresh ratios swept on the MAR-H shape (basis points; 10000 = full recompute).
+MAR_H_RATIO_SWEEP_BP = (0, 500, 1000, 2500, 10000)
+
+
+def streams(seed: int) -> List[np.random.Generator]:
+    """The four child generators (weights, state, orders, planted)."""
+    ss = np.random.SeedSequence(seed)
+    return [np.random.Generator(np.random.PCG64(c)) for c in ss.spawn(4)]
+
+
+def round_to(a: np.ndarray, dtype: str) -> np.ndarray:
+    """Round float32 values once to the storage dtype (RNE), returned as float32.
+
+    For "bf16" every returned value is exactly representable in bfloat16, so
+    the GPU side converts it to bf16 exactly and the oracle to float64 exactly.
+    """
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    if dtype == "f32":
+        return a
+    if dtype != "bf16":
+        raise ValueError(f"unknown dtype {dtype!r}")
+    u = a.view(np.uint32).astype(np.uint64)
+    nan = np.isnan(a)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    out = r.astype(np.uint32).view(np.float32).copy()
+    out[nan] = np.nan
+    return out
+
+
+def _normal(rng: np.random.Generator, shape, std: float) -> np.ndarray:
+    return rng.standard_normal(size=shape, dtype=np.float32) * np.float32(std)
+
+
+def layer_weights(cfg: Config, layer: int) -> Dict[str, np.ndarray]:
+    """Parameters of one block, in torch ``nn.Linear`` layout ``[out][in]``.
+
+    ``w_qkv`` is ``[3D][D]``: rows ``[0, D)`` project queries, ``[D, 2D)`` keys
+    and ``[2D, 3D)`` values; inside each third, head ``h`` owns rows
+    ``[h*d_h, (h+1)*d_h)``.
+    """
+    if not 0 <= layer < cfg.n_layers:
+        raise IndexError(layer)
+    root = np.random.SeedSequence(cfg.seed_value).spawn(4)[STREAM_WEIGHTS]
+    ss = root.spawn(cfg.n_layers)[layer]
+    rng = np.random.Generator(np.random.PCG64(ss))
+    D, F, s = cfg.d_model, cfg.d_mlp, cfg.weight_std
+    p = {
+        "ln1_g": 1.0 + _normal(rng, (D,), s),
+        "ln1_b": _normal(rng, (D,), s),
+        "w_qkv": _normal(rng, (3 * D, D), s),
+        "b_qkv": _normal(rng, (3 * D,), s),
+        "w_o": _normal(rng, (D, D), s),
+        "b_o": _normal(rng, (D,), s),
+        "ln2_g": 1.0 + _normal(rng, (D,), s),
+        "ln2_b": _normal(rng, (D,), s),
+        "w_1": _normal(rng, (F, D), s),
+        "b_1": _normal(rng, (F,), s),
+        "w_2": _normal(rng, (D, F), s),
+        "b_2": _normal(rng, (D,), s),
+    }
+    return {k: round_to(v, cfg.dtype) for k, v in p.items()}
+
+
+def all_weights(cfg: Config) -> List[Dict[str, np.ndarray]]:
+    return [layer_weights(cfg, l) for l in range(cfg.n_layers)]
+
+
+@dataclass
+class Embeddings:
+    """Synthetic decoder-input embeddings (stand-in for Eq. 1-2's encoder output).
+
+    ``cls``   [B][D]      class embedding per image, used at the buffer tokens;
+    ``value`` [B][N_img][D] embedding of an image token once it is generated;
+    ``mask``  [D]         the mask embedding;
+    ``pos``   [N][D]      positional embedding.
+    """
+
+    cls: np.ndarray
+    value: np.ndarray
+    mask: np.ndarray
+    pos: np.ndarray
+
+
+def embeddings(cfg: Config, batch: Optional[int] = None) -> Embeddings:
+    B = cfg.batch if batch is None else batch
+    rng = streams(cfg.seed_value)[STREAM_STATE]
+    D = cfg.d_model
+    cls = rng.standard_normal((cfg.batch, D), dtype=np.float32)[:B]
+    value = rng.standard_normal((cfg.batch, cfg.n_img, D), dtype=np.float32)[:B]
+    mask = rng.standard_normal((D,), dtype=np.float32)
+    pos = rng.standard_normal((cfg.n_tokens, D), dtype=np.float32)
+    return Embeddings(np.ascontiguousarray(cls), np.ascontiguousarray(value), mask, pos)
+
+
+def orders(cfg: Config, batch: Optional[int] = None) -> np.ndarray:
+    """Generation order per image: ``[B][N_img]``, a permutation of ``0..N_img-1``
+    (image-local positions; token index = ``n_buf + position``)."""
+    B = cfg.batch if batch is None else batch
+    rng = streams(cfg.seed_value)[STREAM_ORDERS]
+    out = np.empty((cfg.batch, cfg.n_img), dtype=np.int32)
+    for b in range(cfg.batch):
+        out[b] = rng.permutation(cfg.n_img)
+    return out[:B].copy()
+
+
+@dataclass
+class SingleBlockCase:
+    """Inputs of the single-block case: one cache-aware layer plus top-k.
+
+    ``x`` [B][N][D], ``k_cache``/``v_cache`` [B][H][N][d_h] (all float32 values
+    rounded to ``cfg.dtype``), ``active`` [B][n_a] int32 with the ``n_gen``
+    generating tokens first, ``k_top`` the refresh-set size.
+    """
+
+    x: np.ndarray
+    k_cache: np.ndarray
+    v_cache: np.ndarray
+    active: np.ndarray
+    n_gen: int
+    k_top: int
+
+
+def single_block_case(cfg: Config, n_gen: int = 16, n_ref: int = 16, k_top: int = 16,
+                      batch: Optional[int] = None) -> SingleBlockCase:
+    """x and cached K/V ~ N(0, 1); generating tokens drawn without replacement
+    from the image tokens, refresh tokens from the remaining tokens."""
+    B = cfg.batch if batch is None else batch
+    rng = streams(cfg.seed_value)[STREAM_STATE]
+    N, D, H, dh = cfg.n_tokens, cfg.d_model, cfg.n_heads, cfg.head_dim
+    x = rng.standard_normal((B, N, D), dtype=np.float32)
+    kc = round_to(rng.standard_normal((B, H, N, dh), dtype=np.float32), cfg.dtype)
+    vc = round_to(rng.standard_normal((B, H, N, dh), dtype=np.float32), cfg.dtype)
+    act = np.empty((B, n_gen + n_ref), dtype=np.int32)
+    for b in range(B):
+        g = rng.choice(np.arange(cfg.n_buf, N), size=n_gen, replace=False)
+        rest = np.setdiff1d(np.arange(N), g)
+        r = rng.choice(rest, size=n_ref, replace=False)
+        act[b, :n_gen] = g
+        act[b, n_gen:] = r
+    return SingleBlockCase(x, kc, vc, act, n_gen, k_top)
+
+
+def planted_rows(cfg: Config, candidates: np.ndarray, k: int, batch: Optional[int] = None) -> np.ndarray:
+    """Seeded choice of ``k`` candidate tokens per image for planted-structure
+    variants (the caller decides how to make them stand out)."""
+    B = cfg.batch if batch is None else batch
+    rng = streams(cfg.seed_value)[STREAM_PLANTED]
+    out = np.empty((B, k), dtype=np.int32)
+    for b in range(B):
+        c = candidates[b] if candidates.ndim == 2 else candidates
+        out[b] = np.sort(rng.choice(c, size=k, replace=False))
+    return out

@@ -1,0 +1,102 @@
+"""Pins of the oracle's decoding step over a stack (CPU only).
+
+* at a 100% refresh ratio the MARche schedule equals full recomputation bit
+  for bit at every step (the active set is then every token, and the
+  cache-aware layer canonicalises its rows);
+* at 0% the active set is exactly G u N (the "no refreshing tokens" setting of
+  Section 5.3);
+* a full step is the plain stack of full layers, and the selection layer's
+  scores come from the generating rows only.
+"""
+import numpy as np
+import pytest
+
+from oracle import block, schedule, select, step
+from paper_2506_12035_amd import workload
+
+TINY = workload.Config(90, "tiny", n_layers=3, d_model=32, n_heads=4, head_dim=8, d_mlp=128,
+                       n_tokens=20, n_buf=4, batch=2, dtype="f32", n_steps=6,
+                       ratio_bp=1000, sel_layer=2, full_every=3, weight_std=0.2)
+
+
+def _inputs(cfg):
+    p = [{k: v.astype(np.float64) for k, v in w.items()} for w in workload.all_weights(cfg)]
+    e = workload.embeddings(cfg)
+    o = workload.orders(cfg)
+    return p, e, o
+
+
+def _run(cfg, b, **kw):
+    p, e, o = _inputs(cfg)
+    args = dict(n_buf=cfg.n_buf, n_steps=cfg.n_steps, n_heads=cfg.n_heads, eps=cfg.ln_eps,
+                sel_layer=cfg.sel_layer, full_every=cfg.full_every)
+    args.update(kw)
+    return step.run_generation(p, e.cls[b], e.value[b], e.mask, e.pos, o[b], **args)
+
+
+@pytest.mark.parametrize("full_every", [3, 0])
+def test_ratio_100_is_bitwise_full_recompute(full_every):
+    marche = _run(TINY, 1, full_every=full_every, policy="ratio", budget=10000)
+    full = _run(TINY, 1, full_every=1, policy="ratio", budget=10000)
+    for a, f in zip(marche, full):
+        np.testing.assert_array_equal(a.x_out, f.x_out)
+        for l in range(TINY.n_layers):
+            np.testing.assert_array_equal(a.k_caches[l], f.k_caches[l])
+            np.testing.assert_array_equal(a.v_caches[l], f.v_caches[l])
+        if a.active is not None:
+            assert sorted(a.active) == list(range(TINY.n_tokens))
+
+
+def test_ratio_0_active_is_gen_and_caching():
+    res = _run(TINY, 0, policy="ratio", budget=0)
+    for t, r in enumerate(res):
+        if schedule.is_full_step(t, TINY.full_every):
+            assert r.refresh is None
+        else:
+            assert r.refresh == [] and r.active == r.gen + r.cache_tokens
+
+
+def test_fixed_budget_fills_active_set():
+    res = _run(TINY, 0, policy="fixed", budget=12)
+    for r in res:
+        if r.refresh is not None:
+            assert len(r.active) == max(12, len(r.gen) + len(r.cache_tokens))
+            assert len(set(r.active)) == len(r.active)
+
+
+def test_full_step_is_stack_of_full_layers_and_scores_from_gen():
+    cfg = TINY
+    p, e, o = _inputs(cfg)
+    H, N, dh = cfg.n_heads, cfg.n_tokens, cfg.head_dim
+    rng = np.random.default_rng(5)
+    kcs = [rng.normal(size=(H, N, dh)) for _ in p]
+    vcs = [rng.normal(size=(H, N, dh)) for _ in p]
+    t = 4
+    gen = schedule.generating_tokens(o[0], cfg.n_buf, cfg.n_steps, t)
+    cache = schedule.caching_tokens(o[0], cfg.n_buf, cfg.n_steps, t)
+    known = schedule.known_before(o[0], cfg.n_buf, cfg.n_steps, t)
+    x = step.decoder_input(e.cls[0], e.value[0], e.mask, e.pos, known, cfg.n_buf)
+    # decoder input: buffer rows carry the class embedding, known image rows their
+    # value embedding, masked rows the mask embedding; all add the position
+    for j in range(N):
+        base = e.cls[0] if j < cfg.n_buf else (e.value[0][j - cfg.n_buf] if j in known else e.mask)
+        np.testing.assert_array_equal(x[j], base.astype(np.float64) + e.pos[j])
+    full = step.marche_step(p, x, kcs, vcs, gen, cache, n_heads=H, eps=cfg.ln_eps,
+                            sel_layer=2, full=True, k_refresh=3)
+    xx = x
+    for l in range(cfg.n_layers):
+        xx = block.full_layer(p[l], xx, kcs[l], vcs[l], n_heads=H, eps=cfg.ln_eps).x_out
+    np.testing.assert_array_equal(full.x_out, xx)
+    assert full.refresh is None
+
+    k = 3
+    ca = step.marche_step(p, x, kcs, vcs, gen, cache, n_heads=H, eps=cfg.ln_eps,
+                          sel_layer=2, full=False, k_refresh=k, keep_layers=True)
+    # the selection layer (layer 2) is full; its scores are the attention mass
+    # of the generating rows, which sums to |G| per head
+    np.testing.assert_allclose(ca.scores.sum(axis=1), len(gen), rtol=1e-12)
+    assert ca.refresh == select.select_topk(ca.scores.sum(axis=0), gen + cache, k)
+    assert list(ca.layers[2].rows) == sorted(gen + cache + ca.refresh)
+    # the first two layers are identical to the full step's
+    np.testing.assert_array_equal(ca.layers[1].x_out, block.full_layer(
+        p[1], ca.layers[0].x_out, kcs[1], vcs[1], n_heads=H, eps=cfg.ln_eps).x_out)

@@ -1,0 +1,46 @@
+"""Seeded synthetic inputs: determinism, per-layer independence and exact
+storage-dtype rounding (CPU only)."""
+import numpy as np
+import torch
+
+from paper_2506_12035_amd import workload
+
+
+def test_bf16_rounding_matches_torch_rne():
+    rng = np.random.default_rng(0)
+    a = np.concatenate([rng.normal(size=10000).astype(np.float32),
+                        np.array([0.0, -0.0, 1e-40, 3.4e38, -3.4e38, np.inf, -np.inf], np.float32)])
+    ref = torch.from_numpy(a).to(torch.bfloat16).to(torch.float32).numpy()
+    np.testing.assert_array_equal(workload.round_to(a, "bf16"), ref)
+    assert np.isnan(workload.round_to(np.array([np.nan], np.float32), "bf16")[0])
+
+
+def test_weights_deterministic_and_layer_independent():
+    cfg = workload.CONFIGS[2].with_(n_layers=3, d_model=64, n_heads=4, head_dim=16, d_mlp=256)
+    w1 = workload.layer_weights(cfg, 1)
+    w1b = workload.layer_weights(cfg, 1)
+    w0 = workload.layer_weights(cfg, 0)
+    for k in workload.LAYER_PARAM_NAMES:
+        np.testing.assert_array_equal(w1[k], w1b[k])
+        assert not np.array_equal(w1[k], w0[k])
+        np.testing.assert_array_equal(workload.round_to(w1[k], "bf16"), w1[k])
+    assert w1["w_qkv"].shape == (192, 64) and w1["w_2"].shape == (64, 256)
+    assert abs(float(w1["w_qkv"].std()) - 0.02) < 0.002
+
+
+def test_orders_and_single_block_case():
+    cfg = workload.CONFIGS[1]
+    o = workload.orders(cfg.with_(batch=3))
+    assert all(sorted(r) == list(range(cfg.n_img)) for r in o)
+    c = workload.single_block_case(cfg)
+    assert c.x.shape == (1, 320, 768) and c.k_cache.shape == (1, 12, 320, 64)
+    a = c.active[0]
+    assert len(set(a.tolist())) == 32
+    assert all(j >= cfg.n_buf for j in a[:16])
+
+
+def test_config_shapes():
+    for cid, c in workload.CONFIGS.items():
+        assert c.d_model == c.n_heads * c.head_dim
+        assert c.d_mlp == 4 * c.d_model
+    assert workload.CONFIGS[5].n_tokens == 1088 and workload.CONFIGS[4].head_dim == 80
