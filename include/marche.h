@@ -1,0 +1,194 @@
+/*
+ * marche.h -- C ABI of libmarche.so: MARche's cache-aware decode step on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * MARche (cache-aware attention with selective KV refresh) speeds up the
+ * decoder of masked autoregressive image generation.  At each decoding step
+ * only the *active* tokens A = G u N u R (generating tokens G, caching tokens
+ * N generated one step earlier, refreshing tokens R) are projected; their
+ * fresh keys/values overwrite a per-layer, per-image KV cache; every active
+ * query attends over all N tokens (fresh K/V at A, cached K/V elsewhere); the
+ * output projection and the MLP run on the active rows only (Algorithm 1,
+ * Section 4.1).  R is chosen by the attention mass the generating tokens put
+ * on each token at a selection layer, summed over heads, top-k (Section 4.2).
+ *
+ * Conventions for every entry point:
+ *  - All tensors are caller-owned device memory (hipMalloc / torch).  The
+ *    library keeps no pointer after a call returns and allocates no device
+ *    memory; scratch space is the caller's `workspace`.
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t passed as a
+ *    void*; NULL = the default stream).  No entry point synchronises the
+ *    host, except where stated.
+ *  - Host-side validation runs before any HIP call.  Errors are returned as a
+ *    marche_status_t, never thrown and never an abort; marche_last_error()
+ *    then returns a thread-local message naming the offending argument.
+ *  - Device-side index lists (a_idx, excl_idx, ...) are preconditions: their
+ *    values are not read on the host.
+ *  - Block parameters: matrices are in nn.Linear layout [out][in] and in the
+ *    model dtype; LayerNorm gains/shifts and biases are float32 vectors.
+ *  - The residual stream x is always float32; the KV cache uses the model
+ *    dtype.  bf16 values are IEEE bfloat16; fp32->bf16 rounds to nearest even.
+ */
+#ifndef MARCHE_H
+#define MARCHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MARCHE_OK = 0,
+  MARCHE_ERR_INVALID_ARG = 1, /* null pointer, inconsistent shape, bad range */
+  MARCHE_ERR_UNSUPPORTED = 2, /* valid but not implemented (dtype, head_dim, width) */
+  MARCHE_ERR_HIP = 3,         /* a HIP launch or runtime call failed */
+  MARCHE_ERR_WORKSPACE = 4    /* workspace missing or smaller than required */
+} marche_status_t;
+
+typedef enum { MARCHE_F32 = 0, MARCHE_BF16 = 1 } marche_dtype_t;
+
+/* Opaque HIP stream (hipStream_t). */
+typedef void *marche_stream_t;
+
+/* Shape of the decoder stack.  Pre-LN bidirectional blocks:
+ *   x += W_o . Attn(LN1(x)) + b_o;   x += W_2 . GELU(W_1 . LN2(x) + b_1) + b_2,
+ * LayerNorm with population variance and eps inside the square root,
+ * exact-erf GELU, attention scale 1/sqrt(head_dim).
+ * Supported: d_model == n_heads * head_dim, d_model % 256 == 0,
+ * d_model <= 2048, head_dim in {64, 80}, d_mlp % 256 == 0,
+ * 1 <= n_tokens <= 4096. */
+typedef struct {
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t n_heads;
+  int32_t head_dim;
+  int32_t d_mlp;
+  int32_t n_tokens;
+  int32_t dtype; /* marche_dtype_t */
+  float ln_eps;
+} marche_model_t;
+
+/* Parameters of one block (device pointers).
+ * w_qkv [3D][D]: rows [0,D) queries, [D,2D) keys, [2D,3D) values; inside each
+ * third head h owns rows [h*head_dim, (h+1)*head_dim).  b_qkv [3D] f32.
+ * w_o [D][D], b_o [D] f32; w_1 [F][D], b_1 [F] f32; w_2 [D][F], b_2 [D] f32;
+ * ln1_g/ln1_b/ln2_g/ln2_b [D] f32. */
+typedef struct {
+  const void *ln1_g, *ln1_b;
+  const void *w_qkv, *b_qkv;
+  const void *w_o, *b_o;
+  const void *ln2_g, *ln2_b;
+  const void *w_1, *b_1;
+  const void *w_2, *b_2;
+} marche_layer_t;
+
+/* Per-layer, per-image KV cache C (Algorithm 1's cache).  k and v each hold
+ * [n_layers][batch][n_heads][n_tokens][head_dim] elements of `dtype`. */
+typedef struct {
+  void *k;
+  void *v;
+  int32_t n_layers, batch, n_heads, n_tokens, head_dim;
+  int32_t dtype; /* marche_dtype_t */
+} marche_kv_cache_t;
+
+/* Bind caller buffers k_buf / v_buf (bytes_each bytes each, at least
+ * n_layers*batch*n_heads*n_tokens*head_dim elements) as the cache of `m` for
+ * `batch` images and fill it: copied from k_init / v_init (device, same layout)
+ * when given, else zero.  The first decoding step runs every layer with all
+ * tokens active, which writes every cache row before any is read (Section
+ * 4.3's initial full step).  Returns INVALID_ARG on null or short buffers. */
+marche_status_t kv_cache_init(marche_kv_cache_t *cache, const marche_model_t *m, int32_t batch,
+                              void *k_buf, void *v_buf, size_t bytes_each, const void *k_init,
+                              const void *v_init, marche_stream_t stream);
+
+/* Bytes of workspace marche_step needs for `a_total` active rows in total. */
+size_t marche_step_workspace_bytes(const marche_model_t *m, int32_t batch, int32_t a_total);
+
+/* Run layers [layer_begin, layer_end) of the stack the cache-aware way
+ * (Algorithm 1) for `batch` images.
+ *
+ * Active set (device, CSR over images): image b's active tokens are
+ * a_idx[a_off[b] .. a_off[b+1]), distinct values in [0, n_tokens); the first
+ * n_gen[b] of them are the generating tokens.  a_total = a_off[batch],
+ * a_max = max_b |A_b| and gen_max = max_b n_gen[b] are host copies used for
+ * launch geometry (they must match the device arrays).  A full-attention
+ * layer is the same call with every token active.
+ *
+ * Per layer l and image b:
+ *   u      = LN1(x[b][i]) for i in A_b
+ *   q|k|v  = u W_qkv^T + b_qkv
+ *   cache.k[l][b][h][i] = k_h, cache.v[l][b][h][i] = v_h   (i in A_b; other rows untouched)
+ *   o_i    = sum_j softmax_j(q_i . K[j] / sqrt(d_h)) V[j] over all n_tokens keys
+ *   x[b][i] += o_i W_o^T + b_o;   x[b][i] += W_2 GELU(W_1 LN2(x[b][i]) + b_1) + b_2
+ * Rows of x and of the cache outside A_b are neither read by the MLP nor
+ * written.  x is [batch][n_tokens][d_model] float32, updated in place.
+ *
+ * Scores (Section 4.2): when `scores` is non-NULL and score_layer lies in
+ * [layer_begin, layer_end), that layer also writes
+ *   scores[b][h][j] = sum over the generating rows i of P_h[i][j]
+ * (post-softmax attention probabilities) for every key j, float32
+ * [batch][n_heads][n_tokens], overwriting the buffer.
+ *
+ * `layers` is a host array of n_layers entries; `workspace` holds at least
+ * marche_step_workspace_bytes(m, batch, a_total) bytes of device memory and
+ * must not be used by another call in flight. */
+marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layers,
+                            const marche_kv_cache_t *cache, int32_t layer_begin,
+                            int32_t layer_end, int32_t batch, float *x, const int32_t *a_idx,
+                            const int32_t *a_off, const int32_t *n_gen, int32_t a_total,
+                            int32_t a_max, int32_t gen_max, float *scores, int32_t score_layer,
+                            void *workspace, size_t workspace_bytes, marche_stream_t stream);
+
+/* Refresh selection (Section 4.2, top-k of the head-aggregated scores).
+ * For each image b: s_j = sum_{p < n_parts} scores[b][p][j] (summed in p
+ * order, float32); candidates are the tokens not in
+ * excl_idx[excl_off[b] .. excl_off[b+1]); the k candidates with the highest
+ * s_j are chosen, equal scores going to the lower token index and NaN ranking
+ * below every number; they are written in ascending token order to
+ * out_idx[out_off[b] .. out_off[b]+k).  If an image has fewer than k
+ * candidates the missing slots are written as -1.
+ * Requires 0 <= k <= n_tokens <= 4096, n_parts >= 1. */
+marche_status_t select_refresh(const float *scores, int32_t n_parts, const int32_t *excl_idx,
+                               const int32_t *excl_off, int32_t batch, int32_t n_tokens,
+                               int32_t k, int32_t *out_idx, const int32_t *out_off,
+                               marche_stream_t stream);
+
+/* Decoder input of one step (stand-in for Eq. 2's concatenation of encoder
+ * features and mask embeddings with positional encodings):
+ *   x[b][j] = pos[j] + cls[b]                      for j <  n_buf,
+ *   x[b][j] = pos[j] + value[b][j-n_buf]           for j >= n_buf, rank[b][j-n_buf] <  n_known,
+ *   x[b][j] = pos[j] + mask                        otherwise,
+ * where rank[b][p] is the position of image token p in image b's generation
+ * order, so the tokens generated before the step are those with rank below
+ * n_known.  All float32 except rank (int32 [batch][n_tokens-n_buf]);
+ * cls [batch][D], value [batch][n_tokens-n_buf][D], mask [D], pos [n_tokens][D]. */
+marche_status_t marche_decoder_input(float *x, const float *cls, const float *value,
+                                     const float *mask, const float *pos, const int32_t *rank,
+                                     int32_t batch, int32_t n_tokens, int32_t n_buf,
+                                     int32_t d_model, int32_t n_known, marche_stream_t stream);
+
+/* Name of a status code (static string). */
+const char *marche_status_string(marche_status_t s);
+
+/* Message of the calling thread's last non-OK return ("" if none). */
+const char *marche_last_error(void);
+
+/* ---- kernel timing (instrumentation; not needed to run the method) ----
+ * While enabled, every kernel launched by this library on any stream is
+ * bracketed by HIP events on its own stream, and its algorithmic work
+ * (flops and bytes, from the launch shape) is recorded.
+ * marche_profile_collect() synchronises those events (host sync), folds them
+ * into per-kernel totals and returns the number of kernel classes;
+ * marche_profile_entry() reads one.  marche_profile_reset() clears them. */
+marche_status_t marche_profile_enable(int32_t on);
+int32_t marche_profile_collect(void);
+marche_status_t marche_profile_entry(int32_t i, const char **name, int64_t *launches,
+                                     double *total_ms, double *flops, double *bytes);
+void marche_profile_reset(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MARCHE_H */

@@ -1,0 +1,404 @@
+// Cache-aware bidirectional attention (Algorithm 1 / Section 4.1) and the
+// attention-mass score pass of the selection layer (Section 4.2).
+//
+// Because the fresh K/V of the active tokens were already written into the
+// layer's cache by the QKV epilogue, the active segment K_A and the cached
+// segment K_C are one resident buffer [b][h][N][d_h]: the online-softmax
+// merge of the two segments (Appendix A) becomes the kernel's own loop over
+// key tiles, with a running maximum and a rescaled running sum, and no K/V is
+// ever concatenated or copied.
+//
+// bf16 kernel (gfx950 MFMA, v_mfma_f32_32x32x16_bf16), one workgroup per
+// (image, head, chunk of NW*32 active queries), one wavefront per 32 queries:
+//   - K and V tiles of 64 keys stream global -> registers -> LDS, double
+//     buffered (the next tile's loads are in flight during this tile's math);
+//   - S^T = K Q^T is formed so that lane l owns query (l & 31): the row
+//     maximum and sum need one cross-half exchange, and the accumulator
+//     rescale is a per-lane scalar;
+//   - O^T = V^T P^T: P stays in registers (converted to bf16), V is stored
+//     transposed in LDS with the keys of every 16-key group permuted to match
+//     the accumulator layout of S^T, so each MFMA operand is one 16-byte read.
+// Softmax runs in the log2 domain with fp32 statistics.
+#include "device_common.h"
+
+namespace marche {
+
+constexpr int TK = 64;  // keys per tile
+
+// Position of key k (0..15) inside its 16-key group in the transposed V tile.
+// S^T's accumulator gives lane half hf the keys {4hf..4hf+3, 8+4hf..8+4hf+3}
+// of each 16-key group; this places exactly those at positions 8hf..8hf+7.
+__device__ __forceinline__ int vperm16(int k) {
+  return (k & 3) | (((k >> 3) & 1) << 2) | (((k >> 2) & 1) << 3);
+}
+
+template <int DH, int NW>
+__global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chunks) {
+  constexpr int NT = NW * 64;
+  constexpr int KS = DH + 8;        // K tile row stride (elements)
+  constexpr int ODB = (DH + 31) / 32;
+  constexpr int DHV = ODB * 32;     // rows of the transposed V tile
+  constexpr int VS = TK + 8;        // V^T tile row stride (elements)
+  constexpr int CPR = DH / 8;       // 16-byte chunks per K/V row
+  constexpr int TCH = TK * CPR;     // chunks per tile per matrix
+  constexpr int LPT = (TCH + NT - 1) / NT;
+  constexpr int QS = DH / 16;       // k-steps of the QK^T contraction
+  __shared__ __attribute__((aligned(16))) bf16 Ks[2][TK * KS];
+  __shared__ __attribute__((aligned(16))) bf16 Vt[2][DHV * VS];
+
+  const int id = xcd_remap(blockIdx.x, gridDim.x);
+  const int bh = id / chunks, chunk = id - bh * chunks;
+  const int b = bh / a.n_heads, h = bh - b * a.n_heads;
+  const int r0 = a.a_off[b];
+  const int na = a.a_off[b + 1] - r0;
+  const int q0 = chunk * NW * 32;
+  if (q0 >= na) return;  // uniform over the workgroup
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int N = a.n_tokens, D = a.d_model;
+  const size_t head_base = (size_t)(b * a.n_heads + h) * N * DH;
+  const bf16 *kg = static_cast<const bf16 *>(a.k_cache) + head_base;
+  const bf16 *vg = static_cast<const bf16 *>(a.v_cache) + head_base;
+
+  // V^T rows beyond DH (padding up to a multiple of 32) hold zeros.
+  if constexpr (DHV > DH) {
+    for (int i = tid; i < 2 * (DHV - DH) * VS; i += NT) {
+      const int buf = i / ((DHV - DH) * VS), rem = i % ((DHV - DH) * VS);
+      Vt[buf][DH * VS + rem] = (bf16)0.0f;
+    }
+  }
+
+  // This wavefront's queries as the B operand of S^T = K Q^T.
+  const int wq0 = q0 + wave * 32;
+  const int qi = wq0 + (lane & 31);
+  const bf16 *qrow = static_cast<const bf16 *>(a.q) + (size_t)(r0 + min(qi, na - 1)) * D + h * DH;
+  bf16x8 qf[QS];
+#pragma unroll
+  for (int s = 0; s < QS; ++s)
+    qf[s] = *reinterpret_cast<const bf16x8 *>(qrow + s * 16 + (lane >> 5) * 8);
+
+  uint4 rk[LPT], rv[LPT];
+  auto gload = [&](int t0) {
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+      const int c = i * NT + tid;
+      if (c < TCH) {
+        const int key = min(t0 + c / CPR, N - 1), d = (c % CPR) * 8;
+        rk[i] = *reinterpret_cast<const uint4 *>(kg + (size_t)key * DH + d);
+        rv[i] = *reinterpret_cast<const uint4 *>(vg + (size_t)key * DH + d);
+      }
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+      const int c = i * NT + tid;
+      if (c < TCH) {
+        const int key = c / CPR, d = (c % CPR) * 8;
+        *reinterpret_cast<uint4 *>(&Ks[buf][key * KS + d]) = rk[i];
+        const bf16x8 v = __builtin_bit_cast(bf16x8, rv[i]);
+        const int pos = (key & ~15) | vperm16(key & 15);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) Vt[buf][(d + e) * VS + pos] = v[e];
+      }
+    }
+  };
+
+  const float sl2 = 1.4426950408889634f / sqrtf((float)DH);  // log2(e) / sqrt(d_h)
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x16 acc[ODB];
+#pragma unroll
+  for (int d = 0; d < ODB; ++d) acc[d] = f32x16{};
+
+  const int ntiles = (N + TK - 1) / TK;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int t = 0; t < ntiles; ++t) {
+    const int cur = t & 1, t0 = t * TK;
+    if (t + 1 < ntiles) gload(t0 + TK);
+
+    // S^T for two 32-key blocks: lane -> query (lane & 31),
+    // register r -> key (r / 4) * 8 + (lane / 32) * 4 + r % 4 of the block.
+    f32x16 s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      s[kb] = f32x16{};
+#pragma unroll
+      for (int st = 0; st < QS; ++st) {
+        const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(
+            &Ks[cur][(kb * 32 + (lane & 31)) * KS + st * 16 + (lane >> 5) * 8]);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[st], s[kb], 0, 0, 0);
+      }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = t0 + kb * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        const float v = key < N ? s[kb][r] * sl2 : -INFINITY;
+        s[kb][r] = v;
+        mx = fmaxf(mx, v);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    float psum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = __builtin_amdgcn_exp2f(s[kb][r] - m_new);
+        s[kb][r] = p;
+        psum += p;
+      }
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+#pragma unroll
+    for (int d = 0; d < ODB; ++d) acc[d] *= alpha;
+
+    // O^T += V^T P^T over the 64 keys of the tile, 16 keys per MFMA.
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        bf16x8 pb;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pb[e] = (bf16)s[kb][8 * u + e];
+#pragma unroll
+        for (int d = 0; d < ODB; ++d) {
+          const bf16x8 va = *reinterpret_cast<const bf16x8 *>(
+              &Vt[cur][(d * 32 + (lane & 31)) * VS + kb * 32 + 16 * u + (lane >> 5) * 8]);
+          acc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, acc[d], 0, 0, 0);
+        }
+      }
+
+    if (t + 1 < ntiles) sstore(cur ^ 1);
+    __syncthreads();
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float inv = 1.0f / l_tot;
+  if (qi < na) {
+    bf16 *orow = static_cast<bf16 *>(a.o) + (size_t)(r0 + qi) * D + h * DH;
+#pragma unroll
+    for (int d = 0; d < ODB; ++d)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int dh0 = d * 32 + g * 8 + (lane >> 5) * 4;
+        if (dh0 < DH) {
+          bf16x4 pk = {(bf16)(acc[d][4 * g + 0] * inv), (bf16)(acc[d][4 * g + 1] * inv),
+                       (bf16)(acc[d][4 * g + 2] * inv), (bf16)(acc[d][4 * g + 3] * inv)};
+          *reinterpret_cast<bf16x4 *>(orow + dh0) = pk;
+        }
+      }
+  }
+}
+
+template <int DH, int NW>
+static hipError_t run_attn_mfma(const AttnArgs &a, hipStream_t s) {
+  const int chunks = (a.a_max + NW * 32 - 1) / (NW * 32);
+  const int grid = a.batch * a.n_heads * chunks;
+  attn_mfma_kernel<DH, NW><<<grid, NW * 64, 0, s>>>(a, chunks);
+  return hipGetLastError();
+}
+
+template <int DH>
+static hipError_t attn_bf16_dispatch(const AttnArgs &a, hipStream_t s) {
+  if (a.a_max <= 32) return run_attn_mfma<DH, 1>(a, s);
+  if (a.a_max <= 64) return run_attn_mfma<DH, 2>(a, s);
+  return run_attn_mfma<DH, 4>(a, s);
+}
+
+// fp32 attention: one wavefront per (active row, head).  Logits are formed
+// lane-per-key, then the output lane-per-dimension; exact expf.
+template <int DH>
+__global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
+  extern __shared__ float smem[];
+  float *qs = smem;          // [DH]
+  float *ps = smem + DH;     // [N]
+  const int gw = blockIdx.x;
+  const int row = gw / a.n_heads, h = gw - row * a.n_heads;
+  const int lane = threadIdx.x;
+  const int N = a.n_tokens, D = a.d_model;
+  const RowMap m = a.map[row];
+  const size_t head_base = (size_t)(m.b * a.n_heads + h) * N * DH;
+  const float *kg = static_cast<const float *>(a.k_cache) + head_base;
+  const float *vg = static_cast<const float *>(a.v_cache) + head_base;
+  const float *qg = static_cast<const float *>(a.q) + (size_t)row * D + h * DH;
+  for (int d = lane; d < DH; d += 64) qs[d] = qg[d];
+  __syncthreads();
+  const float scale = 1.0f / sqrtf((float)DH);
+  float mx = -INFINITY;
+  for (int j = lane; j < N; j += 64) {
+    const float *kr = kg + (size_t)j * DH;
+    float acc = 0.f;
+#pragma unroll 8
+    for (int d = 0; d < DH; ++d) acc = fmaf(qs[d], kr[d], acc);
+    acc *= scale;
+    ps[j] = acc;
+    mx = fmaxf(mx, acc);
+  }
+  mx = wave_max(mx);
+  float sum = 0.f;
+  for (int j = lane; j < N; j += 64) {
+    const float e = expf(ps[j] - mx);
+    ps[j] = e;
+    sum += e;
+  }
+  sum = wave_sum(sum);
+  __syncthreads();
+  const float inv = 1.0f / sum;
+  float *og = static_cast<float *>(a.o) + (size_t)row * D + h * DH;
+  for (int d = lane; d < DH; d += 64) {
+    float acc = 0.f;
+    for (int j = 0; j < N; ++j) acc = fmaf(ps[j], vg[(size_t)j * DH + d], acc);
+    og[d] = acc * inv;
+  }
+}
+
+template <int DH>
+static hipError_t attn_f32_dispatch(const AttnArgs &a, hipStream_t s) {
+  const size_t lds = (size_t)(DH + a.n_tokens) * sizeof(float);
+  attn_f32_kernel<DH><<<a.a_total * a.n_heads, 64, lds, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_attention(DType dt, const AttnArgs &a, hipStream_t s) {
+  if (a.a_total == 0) return hipSuccess;
+  if (dt == DType::BF16) {
+    if (a.head_dim == 64) return attn_bf16_dispatch<64>(a, s);
+    if (a.head_dim == 80) return attn_bf16_dispatch<80>(a, s);
+  } else {
+    if (a.head_dim == 64) return attn_f32_dispatch<64>(a, s);
+    if (a.head_dim == 80) return attn_f32_dispatch<80>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+// ---------------------------------------------------------------- score pass
+//
+// scores[b][h][j] = sum over the generating rows i (the first n_gen[b] active
+// rows of image b) of softmax_j(q_i . k_j / sqrt(d_h)) -- the post-softmax
+// attention mass each key receives, one head at a time, with each row's
+// maximum and normaliser taken over all N keys.  One workgroup per
+// (image, head); thread t owns keys t, t+256, ...; generating rows are taken
+// GQ at a time and their logits staged in LDS.  All sums run in a fixed
+// order, so the result is deterministic.
+
+constexpr int SC_THREADS = 256;
+constexpr int SC_MAX_KPT = 16;  // keys per thread: n_tokens <= 4096
+
+__device__ __forceinline__ float block_reduce(float v, bool is_max, float *red) {
+  v = is_max ? wave_max(v) : wave_sum(v);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int i = 1; i < SC_THREADS / 64; ++i) r = is_max ? fmaxf(r, red[i]) : r + red[i];
+  return r;
+}
+
+template <typename T, int DH>
+__global__ __launch_bounds__(SC_THREADS) void attn_scores_kernel(AttnArgs a,
+                                                                 const int32_t *__restrict__ n_gen,
+                                                                 float *__restrict__ scores,
+                                                                 int gq) {
+  extern __shared__ float smem[];
+  const int N = a.n_tokens, D = a.d_model;
+  float *qs = smem;                 // [gq][DH]
+  float *ss = smem + gq * DH;       // [gq][N]
+  float *red = ss + gq * N;         // [4]
+  const int b = blockIdx.x / a.n_heads, h = blockIdx.x - b * a.n_heads;
+  const int tid = threadIdx.x;
+  const int g = n_gen[b], r0 = a.a_off[b];
+  const size_t head_base = (size_t)(b * a.n_heads + h) * N * DH;
+  const T *kg = static_cast<const T *>(a.k_cache) + head_base;
+  const T *qg = static_cast<const T *>(a.q);
+  const float scale = 1.0f / sqrtf((float)DH);
+
+  float acc[SC_MAX_KPT];
+#pragma unroll
+  for (int i = 0; i < SC_MAX_KPT; ++i) acc[i] = 0.f;
+
+  for (int g0 = 0; g0 < g; g0 += gq) {
+    const int nq = min(gq, g - g0);
+    for (int i = tid; i < nq * DH; i += SC_THREADS) {
+      const int qq = i / DH, d = i - qq * DH;
+      qs[i] = to_f32(qg[(size_t)(r0 + g0 + qq) * D + h * DH + d]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < SC_MAX_KPT; ++i) {
+      const int j = tid + SC_THREADS * i;
+      if (j >= N) break;
+      float dot[8];
+#pragma unroll
+      for (int qq = 0; qq < 8; ++qq) dot[qq] = 0.f;
+      const T *kr = kg + (size_t)j * DH;
+#pragma unroll 4
+      for (int d = 0; d < DH; ++d) {
+        const float kv = to_f32(kr[d]);
+#pragma unroll
+        for (int qq = 0; qq < 8; ++qq)
+          if (qq < nq) dot[qq] = fmaf(qs[qq * DH + d], kv, dot[qq]);
+      }
+#pragma unroll
+      for (int qq = 0; qq < 8; ++qq)
+        if (qq < nq) ss[qq * N + j] = dot[qq] * scale;
+    }
+    __syncthreads();
+    for (int qq = 0; qq < nq; ++qq) {
+      float mx = -INFINITY;
+      for (int j = tid; j < N; j += SC_THREADS) mx = fmaxf(mx, ss[qq * N + j]);
+      mx = block_reduce(mx, true, red);
+      float sm = 0.f;
+      for (int j = tid; j < N; j += SC_THREADS) sm += expf(ss[qq * N + j] - mx);
+      sm = block_reduce(sm, false, red);
+      const float inv = 1.0f / sm;
+#pragma unroll
+      for (int i = 0; i < SC_MAX_KPT; ++i) {
+        const int j = tid + SC_THREADS * i;
+        if (j >= N) break;
+        acc[i] += expf(ss[qq * N + j] - mx) * inv;
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < SC_MAX_KPT; ++i) {
+    const int j = tid + SC_THREADS * i;
+    if (j >= N) break;
+    scores[(size_t)(b * a.n_heads + h) * N + j] = acc[i];
+  }
+}
+
+template <typename T, int DH>
+static hipError_t scores_dispatch(const AttnArgs &a, const int32_t *n_gen, float *scores,
+                                  hipStream_t s) {
+  int gq = 12288 / a.n_tokens;
+  gq = gq < 1 ? 1 : (gq > 8 ? 8 : gq);
+  const size_t lds = (size_t)(gq * DH + gq * a.n_tokens + 4) * sizeof(float);
+  attn_scores_kernel<T, DH><<<a.batch * a.n_heads, SC_THREADS, lds, s>>>(a, n_gen, scores, gq);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_scores(DType dt, const AttnArgs &a, const int32_t *n_gen, int32_t gen_max,
+                              float *scores, hipStream_t s) {
+  (void)gen_max;
+  if (a.batch == 0) return hipSuccess;
+  if (a.n_tokens > SC_THREADS * SC_MAX_KPT) return hipErrorInvalidValue;
+  if (dt == DType::BF16) {
+    if (a.head_dim == 64) return scores_dispatch<bf16, 64>(a, n_gen, scores, s);
+    if (a.head_dim == 80) return scores_dispatch<bf16, 80>(a, n_gen, scores, s);
+  } else {
+    if (a.head_dim == 64) return scores_dispatch<float, 64>(a, n_gen, scores, s);
+    if (a.head_dim == 80) return scores_dispatch<float, 80>(a, n_gen, scores, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace marche

@@ -1,0 +1,391 @@
+// Host side of libmarche.so: argument validation, workspace layout, the
+// per-layer launch sequence of a cache-aware decoder step, error reporting
+// and optional per-kernel timing.  Public contract: include/marche.h.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/marche.h"
+#include "marche_internal.h"
+
+using namespace marche;
+
+namespace {
+
+thread_local std::string t_err;
+
+marche_status_t fail(marche_status_t s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  t_err = buf;
+  return s;
+}
+
+marche_status_t fail_hip(hipError_t e, const char *what) {
+  return fail(MARCHE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+size_t elem_size(int32_t dt) { return dt == MARCHE_BF16 ? 2 : 4; }
+
+marche_status_t check_model(const marche_model_t *m) {
+  if (!m) return fail(MARCHE_ERR_INVALID_ARG, "model is NULL");
+  if (m->n_layers < 1) return fail(MARCHE_ERR_INVALID_ARG, "model.n_layers=%d < 1", m->n_layers);
+  if (m->n_heads < 1 || m->head_dim < 1 || m->d_model != m->n_heads * m->head_dim)
+    return fail(MARCHE_ERR_INVALID_ARG, "model.d_model=%d != n_heads*head_dim (%d*%d)", m->d_model,
+                m->n_heads, m->head_dim);
+  if (m->dtype != MARCHE_F32 && m->dtype != MARCHE_BF16)
+    return fail(MARCHE_ERR_UNSUPPORTED, "model.dtype=%d is not F32 or BF16", m->dtype);
+  if (m->head_dim != 64 && m->head_dim != 80)
+    return fail(MARCHE_ERR_UNSUPPORTED, "model.head_dim=%d (supported: 64, 80)", m->head_dim);
+  if (m->d_model % 256 != 0 || m->d_model > 2048)
+    return fail(MARCHE_ERR_UNSUPPORTED, "model.d_model=%d (must be a multiple of 256, <= 2048)",
+                m->d_model);
+  if (m->d_mlp < 256 || m->d_mlp % 256 != 0)
+    return fail(MARCHE_ERR_UNSUPPORTED, "model.d_mlp=%d (must be a positive multiple of 256)",
+                m->d_mlp);
+  if (m->n_tokens < 1 || m->n_tokens > 4096)
+    return fail(MARCHE_ERR_INVALID_ARG, "model.n_tokens=%d (must be in [1, 4096])", m->n_tokens);
+  if (!(m->ln_eps > 0.0f)) return fail(MARCHE_ERR_INVALID_ARG, "model.ln_eps must be > 0");
+  return MARCHE_OK;
+}
+
+// ------------------------------------------------------------------ profiling
+
+enum KClass {
+  K_ROW_MAP, K_GATHER_LN, K_GEMM_QKV, K_ATTN, K_ATTN_SCORES, K_GEMM_O, K_GEMM_FC1, K_GEMM_FC2,
+  K_SELECT, K_DECODER_INPUT, K_FILL, K_NCLASS
+};
+const char *const kClassNames[K_NCLASS] = {
+    "row_map", "gather_ln",  "gemm_qkv", "attention", "attn_scores", "gemm_o",
+    "gemm_fc1", "gemm_fc2", "select_topk", "decoder_input", "fill_zero"};
+
+struct Pending {
+  int cls;
+  hipEvent_t e0, e1;
+  double flops, bytes;
+};
+struct Totals {
+  int64_t launches = 0;
+  double ms = 0, flops = 0, bytes = 0;
+};
+
+std::mutex g_mu;
+bool g_prof = false;
+std::vector<Pending> g_pending;
+std::vector<hipEvent_t> g_pool;
+Totals g_tot[K_NCLASS];
+
+hipEvent_t pool_get() {
+  if (!g_pool.empty()) {
+    hipEvent_t e = g_pool.back();
+    g_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Brackets one kernel launch with events when profiling is on.
+struct ProfScope {
+  int cls;
+  hipStream_t s;
+  double flops, bytes;
+  hipEvent_t e0 = nullptr;
+  bool on = false;
+  ProfScope(int c, hipStream_t st, double f, double b) : cls(c), s(st), flops(f), bytes(b) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (!g_prof) return;
+    e0 = pool_get();
+    if (e0 && hipEventRecord(e0, s) == hipSuccess) on = true;
+  }
+  void done() {
+    if (!on) return;
+    std::lock_guard<std::mutex> lk(g_mu);
+    hipEvent_t e1 = pool_get();
+    if (e1 && hipEventRecord(e1, s) == hipSuccess) g_pending.push_back({cls, e0, e1, flops, bytes});
+    on = false;
+  }
+};
+
+#define LAUNCH(cls, flops, bytes, call)                        \
+  do {                                                         \
+    ProfScope ps_(cls, stream, (double)(flops), (double)(bytes)); \
+    hipError_t e_ = (call);                                    \
+    ps_.done();                                                \
+    if (e_ != hipSuccess) return fail_hip(e_, #call);          \
+  } while (0)
+
+}  // namespace
+
+// ------------------------------------------------------------------ ABI
+
+extern "C" {
+
+const char *marche_status_string(marche_status_t s) {
+  switch (s) {
+    case MARCHE_OK: return "MARCHE_OK";
+    case MARCHE_ERR_INVALID_ARG: return "MARCHE_ERR_INVALID_ARG";
+    case MARCHE_ERR_UNSUPPORTED: return "MARCHE_ERR_UNSUPPORTED";
+    case MARCHE_ERR_HIP: return "MARCHE_ERR_HIP";
+    case MARCHE_ERR_WORKSPACE: return "MARCHE_ERR_WORKSPACE";
+  }
+  return "MARCHE_STATUS_UNKNOWN";
+}
+
+const char *marche_last_error(void) { return t_err.c_str(); }
+
+marche_status_t kv_cache_init(marche_kv_cache_t *cache, const marche_model_t *m, int32_t batch,
+                              void *k_buf, void *v_buf, size_t bytes_each, const void *k_init,
+                              const void *v_init, marche_stream_t stream_) {
+  if (!cache) return fail(MARCHE_ERR_INVALID_ARG, "cache is NULL");
+  marche_status_t st = check_model(m);
+  if (st != MARCHE_OK) return st;
+  if (batch < 0) return fail(MARCHE_ERR_INVALID_ARG, "batch=%d < 0", batch);
+  if (!k_buf || !v_buf) return fail(MARCHE_ERR_INVALID_ARG, "k_buf / v_buf is NULL");
+  if ((k_init == nullptr) != (v_init == nullptr))
+    return fail(MARCHE_ERR_INVALID_ARG, "k_init and v_init must both be given or both be NULL");
+  const size_t need = (size_t)m->n_layers * batch * m->n_heads * m->n_tokens * m->head_dim *
+                      elem_size(m->dtype);
+  if (bytes_each < need)
+    return fail(MARCHE_ERR_INVALID_ARG, "bytes_each=%zu < %zu needed", bytes_each, need);
+  if ((reinterpret_cast<uintptr_t>(k_buf) | reinterpret_cast<uintptr_t>(v_buf)) & 15)
+    return fail(MARCHE_ERR_INVALID_ARG, "k_buf / v_buf must be 16-byte aligned");
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  cache->k = k_buf;
+  cache->v = v_buf;
+  cache->n_layers = m->n_layers;
+  cache->batch = batch;
+  cache->n_heads = m->n_heads;
+  cache->n_tokens = m->n_tokens;
+  cache->head_dim = m->head_dim;
+  cache->dtype = m->dtype;
+  if (need == 0) return MARCHE_OK;
+  if (k_init) {
+    hipError_t e = hipMemcpyAsync(k_buf, k_init, need, hipMemcpyDeviceToDevice, stream);
+    if (e != hipSuccess) return fail_hip(e, "hipMemcpyAsync(k_init)");
+    e = hipMemcpyAsync(v_buf, v_init, need, hipMemcpyDeviceToDevice, stream);
+    if (e != hipSuccess) return fail_hip(e, "hipMemcpyAsync(v_init)");
+    return MARCHE_OK;
+  }
+  LAUNCH(K_FILL, 0, need, launch_fill_zero(k_buf, need, stream));
+  LAUNCH(K_FILL, 0, need, launch_fill_zero(v_buf, need, stream));
+  return MARCHE_OK;
+}
+
+size_t marche_step_workspace_bytes(const marche_model_t *m, int32_t batch, int32_t a_total) {
+  (void)batch;
+  if (!m || a_total < 0) return 0;
+  const size_t es = elem_size(m->dtype);
+  const size_t M = (size_t)a_total;
+  return align256(M * sizeof(RowMap)) + 2 * align256(M * m->d_model * es) +
+         align256(M * m->d_mlp * es);
+}
+
+marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layers,
+                            const marche_kv_cache_t *cache, int32_t layer_begin,
+                            int32_t layer_end, int32_t batch, float *x, const int32_t *a_idx,
+                            const int32_t *a_off, const int32_t *n_gen, int32_t a_total,
+                            int32_t a_max, int32_t gen_max, float *scores, int32_t score_layer,
+                            void *workspace, size_t workspace_bytes, marche_stream_t stream_) {
+  marche_status_t st = check_model(m);
+  if (st != MARCHE_OK) return st;
+  if (!layers) return fail(MARCHE_ERR_INVALID_ARG, "layers is NULL");
+  if (!cache || !cache->k || !cache->v) return fail(MARCHE_ERR_INVALID_ARG, "cache is NULL or unbound");
+  if (cache->n_layers != m->n_layers || cache->n_heads != m->n_heads ||
+      cache->n_tokens != m->n_tokens || cache->head_dim != m->head_dim ||
+      cache->dtype != m->dtype)
+    return fail(MARCHE_ERR_INVALID_ARG, "cache shape/dtype does not match the model");
+  if (batch < 0 || batch > cache->batch)
+    return fail(MARCHE_ERR_INVALID_ARG, "batch=%d outside [0, cache.batch=%d]", batch, cache->batch);
+  if (layer_begin < 0 || layer_end < layer_begin || layer_end > m->n_layers)
+    return fail(MARCHE_ERR_INVALID_ARG, "layer range [%d, %d) outside [0, %d]", layer_begin,
+                layer_end, m->n_layers);
+  if (a_total < 0 || a_total > batch * m->n_tokens)
+    return fail(MARCHE_ERR_INVALID_ARG, "a_total=%d outside [0, batch*n_tokens=%d]", a_total,
+                batch * m->n_tokens);
+  if (a_max < 0 || a_max > m->n_tokens || a_max > a_total || (a_total > 0 && a_max == 0))
+    return fail(MARCHE_ERR_INVALID_ARG, "a_max=%d inconsistent with a_total=%d, n_tokens=%d",
+                a_max, a_total, m->n_tokens);
+  if (gen_max < 0 || gen_max > a_max)
+    return fail(MARCHE_ERR_INVALID_ARG, "gen_max=%d outside [0, a_max=%d]", gen_max, a_max);
+  if (layer_begin == layer_end || batch == 0 || a_total == 0) return MARCHE_OK;
+  if (!x) return fail(MARCHE_ERR_INVALID_ARG, "x is NULL");
+  if (!a_idx || !a_off) return fail(MARCHE_ERR_INVALID_ARG, "a_idx / a_off is NULL");
+  const bool want_scores = scores && score_layer >= layer_begin && score_layer < layer_end;
+  if (want_scores && !n_gen) return fail(MARCHE_ERR_INVALID_ARG, "scores requested but n_gen is NULL");
+  for (int l = layer_begin; l < layer_end; ++l) {
+    const marche_layer_t &L = layers[l];
+    if (!L.ln1_g || !L.ln1_b || !L.w_qkv || !L.b_qkv || !L.w_o || !L.b_o || !L.ln2_g ||
+        !L.ln2_b || !L.w_1 || !L.b_1 || !L.w_2 || !L.b_2)
+      return fail(MARCHE_ERR_INVALID_ARG, "layers[%d] has a NULL parameter", l);
+  }
+  const size_t need = marche_step_workspace_bytes(m, batch, a_total);
+  if (!workspace || workspace_bytes < need)
+    return fail(MARCHE_ERR_WORKSPACE, "workspace %s: %zu bytes < %zu needed",
+                workspace ? "too small" : "is NULL", workspace_bytes, need);
+  if (reinterpret_cast<uintptr_t>(workspace) & 255)
+    return fail(MARCHE_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  const DType dt = m->dtype == MARCHE_BF16 ? DType::BF16 : DType::F32;
+  const size_t es = elem_size(m->dtype);
+  const int D = m->d_model, F = m->d_mlp, H = m->n_heads, dh = m->head_dim, N = m->n_tokens;
+  const int M = a_total;
+
+  char *ws = static_cast<char *>(workspace);
+  RowMap *map = reinterpret_cast<RowMap *>(ws);
+  ws += align256((size_t)M * sizeof(RowMap));
+  void *buf0 = ws;  // LN1 output, then attention output
+  ws += align256((size_t)M * D * es);
+  void *buf1 = ws;  // queries, then LN2 output
+  ws += align256((size_t)M * D * es);
+  void *hid = ws;   // MLP hidden activations
+
+  const size_t layer_elems = (size_t)cache->batch * H * N * dh;
+  const double gemm_bytes_act = (double)es;
+
+  LAUNCH(K_ROW_MAP, 0, (double)M * (4 + sizeof(RowMap)),
+         launch_row_map(map, a_idx, a_off, batch, N, stream));
+
+  for (int l = layer_begin; l < layer_end; ++l) {
+    const marche_layer_t &L = layers[l];
+    char *kc = static_cast<char *>(cache->k) + (size_t)l * layer_elems * es;
+    char *vc = static_cast<char *>(cache->v) + (size_t)l * layer_elems * es;
+
+    LAUNCH(K_GATHER_LN, 0, (double)M * D * (4 + es),
+           launch_gather_ln(dt, buf0, x, map, static_cast<const float *>(L.ln1_g),
+                            static_cast<const float *>(L.ln1_b), M, D, m->ln_eps, stream));
+    QkvOut qo{buf1, kc, vc, D, dh, H, N};
+    LAUNCH(K_GEMM_QKV, 2.0 * M * 3 * D * D,
+           gemm_bytes_act * ((double)M * D + 3.0 * D * D + 3.0 * M * D),
+           launch_gemm_qkv(dt, buf0, L.w_qkv, static_cast<const float *>(L.b_qkv), M, 3 * D, D,
+                           map, qo, stream));
+    AttnArgs aa{buf1, kc, vc, buf0, a_off, map, batch, H, N, dh, D, M, a_max};
+    // Algorithmic traffic: every cached K/V element of the batch read once,
+    // plus the queries read and the outputs written.
+    LAUNCH(K_ATTN, 4.0 * M * N * D, es * (2.0 * batch * N * D + 2.0 * M * D),
+           launch_attention(dt, aa, stream));
+    if (want_scores && l == score_layer) {
+      LAUNCH(K_ATTN_SCORES, 2.0 * batch * gen_max * N * D,
+             es * (double)batch * N * D + 4.0 * batch * H * N,
+             launch_attn_scores(dt, aa, n_gen, gen_max, scores, stream));
+    }
+    LAUNCH(K_GEMM_O, 2.0 * M * D * D, gemm_bytes_act * ((double)M * D + (double)D * D) + 8.0 * M * D,
+           launch_gemm_resid(dt, buf0, L.w_o, static_cast<const float *>(L.b_o), M, D, D, map, x,
+                             stream));
+    LAUNCH(K_GATHER_LN, 0, (double)M * D * (4 + es),
+           launch_gather_ln(dt, buf1, x, map, static_cast<const float *>(L.ln2_g),
+                            static_cast<const float *>(L.ln2_b), M, D, m->ln_eps, stream));
+    LAUNCH(K_GEMM_FC1, 2.0 * M * F * D,
+           gemm_bytes_act * ((double)M * D + (double)F * D + (double)M * F),
+           launch_gemm_gelu(dt, buf1, L.w_1, static_cast<const float *>(L.b_1), M, F, D, hid,
+                            stream));
+    LAUNCH(K_GEMM_FC2, 2.0 * M * D * F,
+           gemm_bytes_act * ((double)M * F + (double)D * F) + 8.0 * M * D,
+           launch_gemm_resid(dt, hid, L.w_2, static_cast<const float *>(L.b_2), M, D, F, map, x,
+                             stream));
+  }
+  return MARCHE_OK;
+}
+
+marche_status_t select_refresh(const float *scores, int32_t n_parts, const int32_t *excl_idx,
+                               const int32_t *excl_off, int32_t batch, int32_t n_tokens,
+                               int32_t k, int32_t *out_idx, const int32_t *out_off,
+                               marche_stream_t stream_) {
+  if (batch < 0) return fail(MARCHE_ERR_INVALID_ARG, "batch=%d < 0", batch);
+  if (n_tokens < 1 || n_tokens > 4096)
+    return fail(MARCHE_ERR_INVALID_ARG, "n_tokens=%d outside [1, 4096]", n_tokens);
+  if (k < 0 || k > n_tokens)
+    return fail(MARCHE_ERR_INVALID_ARG, "k=%d outside [0, n_tokens=%d]", k, n_tokens);
+  if (n_parts < 1) return fail(MARCHE_ERR_INVALID_ARG, "n_parts=%d < 1", n_parts);
+  if (batch == 0 || k == 0) return MARCHE_OK;
+  if (!scores || !out_idx || !out_off || !excl_off)
+    return fail(MARCHE_ERR_INVALID_ARG, "scores / out_idx / out_off / excl_off is NULL");
+  if (!excl_idx) return fail(MARCHE_ERR_INVALID_ARG, "excl_idx is NULL");
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  LAUNCH(K_SELECT, 0, 4.0 * batch * n_parts * n_tokens,
+         launch_select_topk(scores, n_parts, excl_idx, excl_off, batch, n_tokens, k, out_idx,
+                            out_off, stream));
+  return MARCHE_OK;
+}
+
+marche_status_t marche_decoder_input(float *x, const float *cls, const float *value,
+                                     const float *mask, const float *pos, const int32_t *rank,
+                                     int32_t batch, int32_t n_tokens, int32_t n_buf,
+                                     int32_t d_model, int32_t n_known, marche_stream_t stream_) {
+  if (batch < 0 || n_tokens < 1 || n_buf < 0 || n_buf > n_tokens)
+    return fail(MARCHE_ERR_INVALID_ARG, "batch=%d n_tokens=%d n_buf=%d inconsistent", batch,
+                n_tokens, n_buf);
+  if (d_model < 4 || d_model % 4 != 0)
+    return fail(MARCHE_ERR_INVALID_ARG, "d_model=%d must be a positive multiple of 4", d_model);
+  if (n_known < 0 || n_known > n_tokens - n_buf)
+    return fail(MARCHE_ERR_INVALID_ARG, "n_known=%d outside [0, %d]", n_known, n_tokens - n_buf);
+  if (batch == 0) return MARCHE_OK;
+  if (!x || !cls || !mask || !pos || (n_tokens > n_buf && (!value || !rank)))
+    return fail(MARCHE_ERR_INVALID_ARG, "NULL input to marche_decoder_input");
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  LAUNCH(K_DECODER_INPUT, 0, 12.0 * batch * n_tokens * d_model,
+         launch_decoder_input(x, cls, value, mask, pos, rank, batch, n_tokens, n_buf, d_model,
+                              n_known, stream));
+  return MARCHE_OK;
+}
+
+marche_status_t marche_profile_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  g_prof = on != 0;
+  return MARCHE_OK;
+}
+
+int32_t marche_profile_collect(void) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  for (Pending &p : g_pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(p.e1) == hipSuccess && hipEventElapsedTime(&ms, p.e0, p.e1) == hipSuccess) {
+      Totals &t = g_tot[p.cls];
+      t.launches += 1;
+      t.ms += ms;
+      t.flops += p.flops;
+      t.bytes += p.bytes;
+    }
+    g_pool.push_back(p.e0);
+    g_pool.push_back(p.e1);
+  }
+  g_pending.clear();
+  return K_NCLASS;
+}
+
+marche_status_t marche_profile_entry(int32_t i, const char **name, int64_t *launches,
+                                     double *total_ms, double *flops, double *bytes) {
+  if (i < 0 || i >= K_NCLASS) return fail(MARCHE_ERR_INVALID_ARG, "profile entry %d out of range", i);
+  std::lock_guard<std::mutex> lk(g_mu);
+  const Totals &t = g_tot[i];
+  if (name) *name = kClassNames[i];
+  if (launches) *launches = t.launches;
+  if (total_ms) *total_ms = t.ms;
+  if (flops) *flops = t.flops;
+  if (bytes) *bytes = t.bytes;
+  return MARCHE_OK;
+}
+
+void marche_profile_reset(void) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  for (Pending &p : g_pending) {
+    g_pool.push_back(p.e0);
+    g_pool.push_back(p.e1);
+  }
+  g_pending.clear();
+  for (Totals &t : g_tot) t = Totals();
+}
+
+}  // extern "C"

@@ -1,0 +1,79 @@
+// Internal declarations shared by the host API and the HIP kernels of
+// libmarche.so.  Not part of the public ABI (include/marche.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace marche {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Where active row r of the packed activations lives: image b, token tok,
+// and its row in the [batch][n_tokens][d_model] residual stream.
+struct RowMap {
+  int32_t x_row;  // b * n_tokens + tok
+  int32_t b;
+  int32_t tok;
+  int32_t pad;
+};
+
+// Element type of the packed activations, weights and KV cache.
+enum class DType { F32 = 0, BF16 = 1 };
+
+// ---- elementwise / indexing (k_elementwise.hip) ----
+hipError_t launch_row_map(RowMap *map, const int32_t *a_idx, const int32_t *a_off, int32_t batch,
+                          int32_t n_tokens, hipStream_t s);
+hipError_t launch_gather_ln(DType dt, void *out, const float *x, const RowMap *map, const float *g,
+                            const float *b, int32_t rows, int32_t d_model, float eps, hipStream_t s);
+hipError_t launch_decoder_input(float *x, const float *cls, const float *value, const float *mask,
+                                const float *pos, const int32_t *rank, int32_t batch,
+                                int32_t n_tokens, int32_t n_buf, int32_t d_model, int32_t n_known,
+                                hipStream_t s);
+hipError_t launch_fill_zero(void *dst, size_t bytes, hipStream_t s);
+
+// ---- GEMMs with fused epilogues (k_gemm.hip) ----
+// C[M][N] = A[M][K] . W[N][K]^T (+ bias) followed by one epilogue:
+//   qkv:   columns [0,D) -> q [M][D]; [D,2D) -> K cache, [2D,3D) -> V cache
+//          (scattered to [b][h][tok][d] of one layer's cache)
+//   resid: x[map[r].x_row][c] += C + bias        (float32 residual stream)
+//   gelu:  h[r][c] = GELU(C + bias)
+struct QkvOut {
+  void *q;
+  void *k_cache;  // layer base
+  void *v_cache;  // layer base
+  int32_t d_model, head_dim, n_heads, n_tokens;
+};
+hipError_t launch_gemm_qkv(DType dt, const void *a, const void *w, const float *bias, int32_t m,
+                           int32_t n, int32_t k, const RowMap *map, QkvOut out, hipStream_t s);
+hipError_t launch_gemm_resid(DType dt, const void *a, const void *w, const float *bias, int32_t m,
+                             int32_t n, int32_t k, const RowMap *map, float *x, hipStream_t s);
+hipError_t launch_gemm_gelu(DType dt, const void *a, const void *w, const float *bias, int32_t m,
+                            int32_t n, int32_t k, void *h, hipStream_t s);
+
+// ---- attention (k_attn.hip) ----
+struct AttnArgs {
+  const void *q;        // [a_total][D] packed queries
+  const void *k_cache;  // layer base [B][H][N][dh]
+  const void *v_cache;
+  void *o;              // [a_total][D]
+  const int32_t *a_off;
+  const RowMap *map;
+  int32_t batch, n_heads, n_tokens, head_dim, d_model, a_total, a_max;
+};
+hipError_t launch_attention(DType dt, const AttnArgs &a, hipStream_t s);
+// scores[b][h][j] = sum over the first n_gen[b] active rows i of P_h[i][j]
+hipError_t launch_attn_scores(DType dt, const AttnArgs &a, const int32_t *n_gen, int32_t gen_max,
+                              float *scores, hipStream_t s);
+
+// ---- selection (k_select.hip) ----
+hipError_t launch_select_topk(const float *scores, int32_t n_parts, const int32_t *excl_idx,
+                              const int32_t *excl_off, int32_t batch, int32_t n_tokens, int32_t k,
+                              int32_t *out_idx, const int32_t *out_off, hipStream_t s);
+
+}  // namespace marche

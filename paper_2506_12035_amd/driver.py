@@ -1,0 +1,200 @@
+"""Decoding-step driver: composes the C-ABI calls into MARche steps.
+
+One step t of a batch of images (Section 4.2-4.3, Algorithm 1):
+
+* build the decoder input x (marche_decoder_input);
+* full step (the first step and every periodic full refresh): one
+  marche_step over all layers with every token active;
+* otherwise: marche_step over layers [0, sel_layer) with every token active
+  and the generating tokens first, writing the selection layer's per-head
+  attention mass; select_refresh picks R per image into the tail of the
+  cache-aware active list [G | N | R]; marche_step over layers
+  [sel_layer, L) on that list.
+
+All index lists of every step are built on the host once, before decoding,
+and kept resident on the device; a step issues only kernel launches on one
+stream (no host synchronisation, no host-device copies).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import binding, schedule, workload
+
+
+def _dev_i32(a: np.ndarray, device) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(device)
+
+
+@dataclass
+class StepPlan:
+    t: int
+    full: bool
+    n_known: int
+    g: int
+    n: int
+    k: int
+    full_idx: torch.Tensor
+    full_off: torch.Tensor
+    n_gen: torch.Tensor
+    ca_idx: Optional[torch.Tensor] = None
+    ca_off: Optional[torch.Tensor] = None
+    excl_idx: Optional[torch.Tensor] = None
+    excl_off: Optional[torch.Tensor] = None
+    out_off: Optional[torch.Tensor] = None
+
+
+class Engine:
+    """Device state and step composition for one workload configuration."""
+
+    def __init__(self, cfg: workload.Config, device: str = "cuda", batch: Optional[int] = None,
+                 n_layers: Optional[int] = None, ratio_bp: Optional[int] = None,
+                 policy: str = "ratio", budget: Optional[int] = None,
+                 full_every: Optional[int] = None, sel_layer: Optional[int] = None,
+                 weights: Optional[Sequence[Dict[str, np.ndarray]]] = None):
+        if n_layers is not None:
+            cfg = cfg.with_(n_layers=n_layers)
+        self.cfg = cfg
+        self.device = torch.device(device)
+        self.B = cfg.batch if batch is None else batch
+        self.policy = policy
+        if budget is None:
+            if policy != "ratio":
+                raise ValueError("a fixed budget needs `budget` (the active-set size)")
+            budget = cfg.ratio_bp if ratio_bp is None else ratio_bp
+        self.budget = budget
+        self.full_every = cfg.full_every if full_every is None else full_every
+        self.sel = cfg.sel_layer if sel_layer is None else sel_layer
+        if not 1 <= self.sel <= cfg.n_layers:
+            raise ValueError("sel_layer must lie in [1, n_layers]")
+        self.dt = binding.MARCHE_BF16 if cfg.dtype == "bf16" else binding.MARCHE_F32
+        self.tdtype = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+        L, D, H, N, dh, F = (cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.n_tokens, cfg.head_dim,
+                             cfg.d_mlp)
+        self.model = binding.make_model(L, D, H, dh, F, N, self.dt, cfg.ln_eps)
+
+        ws = weights if weights is not None else [workload.layer_weights(cfg, l) for l in range(L)]
+        self.params = [self._upload_layer(w) for w in ws]
+        self.layers = binding.make_layers(self.params)
+
+        es = 2 if cfg.dtype == "bf16" else 4
+        n_el = L * self.B * H * N * dh
+        self.k_cache = torch.empty(n_el, dtype=self.tdtype, device=self.device)
+        self.v_cache = torch.empty(n_el, dtype=self.tdtype, device=self.device)
+        self.cache = binding.kv_cache_init(self.model, self.B, self.k_cache, self.v_cache, n_el * es,
+                                           stream=self.stream)
+        self.x = torch.empty(self.B, N, D, dtype=torch.float32, device=self.device)
+        self.scores = torch.empty(self.B, H, N, dtype=torch.float32, device=self.device)
+        self.ws_bytes = binding.workspace_bytes(self.model, self.B, self.B * N)
+        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+
+        emb = workload.embeddings(cfg, self.B)
+        self.orders = workload.orders(cfg, self.B)
+        rank = np.empty_like(self.orders)
+        for b in range(self.B):
+            rank[b, self.orders[b]] = np.arange(cfg.n_img, dtype=np.int32)
+        self.e_cls = torch.from_numpy(emb.cls).to(self.device)
+        self.e_value = torch.from_numpy(emb.value).to(self.device)
+        self.e_mask = torch.from_numpy(emb.mask).to(self.device)
+        self.e_pos = torch.from_numpy(emb.pos).to(self.device)
+        self.rank = _dev_i32(rank, self.device)
+        self.plans = [self._plan(t) for t in range(cfg.n_steps)]
+
+    @property
+    def stream(self):
+        return torch.cuda.current_stream(self.device)
+
+    # ------------------------------------------------------------------ setup
+
+    def _upload_layer(self, w: Dict[str, np.ndarray]) -> Dict[str, torch.Tensor]:
+        out = {}
+        for name, a in w.items():
+            t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+            if name.startswith("w_"):
+                t = t.to(self.tdtype)
+            out[name] = t.to(self.device).contiguous()
+        return out
+
+    def _plan(self, t: int) -> StepPlan:
+        c = self.cfg
+        si = schedule.step_indices(self.orders, c.n_buf, c.n_tokens, c.n_steps, t, self.full_every,
+                                   self.policy, self.budget)
+        B, N = self.B, c.n_tokens
+        g, n, k = si.gen.shape[1], si.cache.shape[1], si.k
+        plan = StepPlan(t, si.full, si.n_known, g, n, k,
+                        _dev_i32(si.full_order.reshape(-1), self.device),
+                        _dev_i32(np.arange(B + 1) * N, self.device),
+                        _dev_i32(np.full(B, g), self.device))
+        if not si.full:
+            a = g + n + k
+            ca = np.full((B, a), -1, np.int32)
+            ca[:, :g] = si.gen
+            ca[:, g:g + n] = si.cache
+            excl = np.concatenate([si.gen, si.cache], axis=1)
+            plan.ca_idx = _dev_i32(ca.reshape(-1), self.device)
+            plan.ca_off = _dev_i32(np.arange(B + 1) * a, self.device)
+            plan.excl_idx = _dev_i32(excl.reshape(-1), self.device)
+            plan.excl_off = _dev_i32(np.arange(B + 1) * (g + n), self.device)
+            plan.out_off = _dev_i32(np.arange(B) * a + g + n, self.device)
+        return plan
+
+    # ------------------------------------------------------------------ step
+
+    def decoder_input(self, t: int) -> None:
+        c = self.cfg
+        binding.decoder_input(self.x, self.e_cls, self.e_value, self.e_mask, self.e_pos, self.rank,
+                              self.B, c.n_tokens, c.n_buf, c.d_model, self.plans[t].n_known,
+                              stream=self.stream)
+
+    def run_layers(self, begin: int, end: int, idx, off, a_total: int, a_max: int, g: int,
+                   n_gen, score_layer: int = -1) -> None:
+        binding.marche_step(self.model, self.layers, self.cache, begin, end, self.B, self.x, idx,
+                            off, n_gen, a_total, a_max, g,
+                            self.scores if score_layer >= 0 else None, score_layer,
+                            self.workspace, self.ws_bytes, stream=self.stream)
+
+    def select(self, p: StepPlan) -> None:
+        binding.select_refresh(self.scores, self.cfg.n_heads, p.excl_idx, p.excl_off, self.B,
+                               self.cfg.n_tokens, p.k, p.ca_idx, p.out_off, stream=self.stream)
+
+    def step(self, t: int, build_input: bool = True) -> None:
+        """One decoding step (all layers) of the whole batch, enqueued on the
+        current stream."""
+        p = self.plans[t]
+        c = self.cfg
+        N, L, B = c.n_tokens, c.n_layers, self.B
+        if build_input:
+            self.decoder_input(t)
+        if p.full:
+            self.run_layers(0, L, p.full_idx, p.full_off, B * N, N, p.g, p.n_gen)
+            return
+        self.run_layers(0, self.sel, p.full_idx, p.full_off, B * N, N, p.g, p.n_gen,
+                        score_layer=self.sel - 1)
+        self.select(p)
+        a = p.g + p.n + p.k
+        self.run_layers(self.sel, L, p.ca_idx, p.ca_off, B * a, a, p.g, p.n_gen)
+
+    def generate(self, steps: Optional[Sequence[int]] = None) -> None:
+        for t in (range(self.cfg.n_steps) if steps is None else steps):
+            self.step(t)
+
+    # ------------------------------------------------------------------ readback (tests)
+
+    def k_layer(self, l: int) -> torch.Tensor:
+        c = self.cfg
+        return self.k_cache.view(c.n_layers, self.B, c.n_heads, c.n_tokens, c.head_dim)[l]
+
+    def v_layer(self, l: int) -> torch.Tensor:
+        c = self.cfg
+        return self.v_cache.view(c.n_layers, self.B, c.n_heads, c.n_tokens, c.head_dim)[l]
+
+    def active_lists(self, t: int) -> Optional[np.ndarray]:
+        """[B][|A|] cache-aware active list of step t as last computed (G | N | R)."""
+        p = self.plans[t]
+        if p.full:
+            return None
+        return p.ca_idx.view(self.B, -1).cpu().numpy()

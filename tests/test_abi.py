@@ -1,0 +1,147 @@
+"""The C-ABI library without a GPU: it loads, exports every entry point that
+include/marche.h declares, and rejects bad arguments on the host before any
+HIP call (CPU only; no kernel is launched)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2506_12035_amd import binding, build
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "marche.h")
+FAKE = 0x10000000  # never dereferenced: validation fails first
+
+
+@pytest.fixture(scope="module", autouse=True)
+def built_library():
+    if not os.path.exists(binding.LIB_PATH):
+        build.build()
+    return binding.lib()
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return set(re.findall(r"^\s*(?:const\s+)?(?:marche_status_t|size_t|int32_t|void|char)\s*\**\s*(\w+)\s*\(",
+                          text, flags=re.M))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert {"kv_cache_init", "marche_step", "select_refresh"} <= names
+    assert names == set(binding.EXPORTED)
+    lib = C.CDLL(binding.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def _model(**kw):
+    base = dict(n_layers=2, d_model=1024, n_heads=16, head_dim=64, d_mlp=4096, n_tokens=320,
+                dtype=binding.MARCHE_BF16, ln_eps=1e-6)
+    base.update(kw)
+    return binding.make_model(**base)
+
+
+def _cache(m, batch=2):
+    return binding.KVCache(FAKE, FAKE, m.n_layers, batch, m.n_heads, m.n_tokens, m.head_dim, m.dtype)
+
+
+def _layers(n):
+    return binding.make_layers([{k: FAKE for k, _ in binding.Layer._fields_} for _ in range(n)])
+
+
+def _step(m, cache=None, layers=None, **kw):
+    args = dict(layer_begin=0, layer_end=m.n_layers, batch=2, x=FAKE, a_idx=FAKE, a_off=FAKE,
+                n_gen=FAKE, a_total=10, a_max=5, gen_max=2, scores=None, score_layer=-1,
+                workspace=FAKE, workspace_bytes=0)
+    args.update(kw)
+    L = binding.lib()
+    return L.marche_step(C.byref(m), layers if layers is not None else _layers(m.n_layers),
+                         C.byref(cache if cache is not None else _cache(m)), args["layer_begin"],
+                         args["layer_end"], args["batch"], args["x"], args["a_idx"], args["a_off"],
+                         args["n_gen"], args["a_total"], args["a_max"], args["gen_max"],
+                         args["scores"], args["score_layer"], args["workspace"],
+                         args["workspace_bytes"], None)
+
+
+def test_status_strings():
+    assert binding.status_string(0) == "MARCHE_OK"
+    assert binding.status_string(4) == "MARCHE_ERR_WORKSPACE"
+    assert binding.status_string(99) == "MARCHE_STATUS_UNKNOWN"
+
+
+@pytest.mark.parametrize("kw,status,word", [
+    (dict(head_dim=96, d_model=1536, n_heads=16), binding.MARCHE_ERR_UNSUPPORTED, "head_dim"),
+    (dict(d_model=1000), binding.MARCHE_ERR_INVALID_ARG, "d_model"),
+    (dict(dtype=7), binding.MARCHE_ERR_UNSUPPORTED, "dtype"),
+    (dict(d_mlp=1000), binding.MARCHE_ERR_UNSUPPORTED, "d_mlp"),
+    (dict(n_tokens=0), binding.MARCHE_ERR_INVALID_ARG, "n_tokens"),
+    (dict(n_layers=0), binding.MARCHE_ERR_INVALID_ARG, "n_layers"),
+])
+def test_model_validation(kw, status, word):
+    m = _model(**kw)
+    assert _step(m) == status
+    assert word in binding.last_error()
+
+
+def test_step_argument_validation():
+    m = _model()
+    assert _step(m, layer_begin=1, layer_end=3) == binding.MARCHE_ERR_INVALID_ARG
+    assert "layer range" in binding.last_error()
+    assert _step(m, a_total=2 * 320 + 1) == binding.MARCHE_ERR_INVALID_ARG
+    assert _step(m, a_max=400) == binding.MARCHE_ERR_INVALID_ARG
+    assert _step(m, gen_max=6) == binding.MARCHE_ERR_INVALID_ARG
+    assert _step(m, batch=3) == binding.MARCHE_ERR_INVALID_ARG  # cache holds 2 images
+    assert _step(m, x=None) == binding.MARCHE_ERR_INVALID_ARG
+    assert _step(m, scores=FAKE, score_layer=0, n_gen=None) == binding.MARCHE_ERR_INVALID_ARG
+    bad = _layers(2)
+    bad[1].w_o = None
+    assert _step(m, layers=bad) == binding.MARCHE_ERR_INVALID_ARG
+    assert "layers[1]" in binding.last_error()
+    mism = _cache(m)
+    mism.head_dim = 80
+    assert _step(m, cache=mism) == binding.MARCHE_ERR_INVALID_ARG
+
+
+def test_workspace_validation_and_size():
+    m = _model()
+    need = binding.workspace_bytes(m, 2, 10)
+    # map + 2 * [M][D] bf16 + [M][F] bf16, each rounded up to 256 bytes
+    assert need == 256 + 2 * 20480 + 81920
+    assert _step(m, workspace_bytes=need - 1) == binding.MARCHE_ERR_WORKSPACE
+    assert _step(m, workspace=None, workspace_bytes=need) == binding.MARCHE_ERR_WORKSPACE
+    assert _step(m, workspace=FAKE + 8, workspace_bytes=need) == binding.MARCHE_ERR_INVALID_ARG
+    # nothing to do: returns OK without touching memory
+    assert _step(m, layer_begin=1, layer_end=1) == binding.MARCHE_OK
+    assert _step(m, a_total=0, a_max=0, gen_max=0) == binding.MARCHE_OK
+
+
+def test_select_refresh_validation():
+    L = binding.lib()
+    assert L.select_refresh(FAKE, 16, FAKE, FAKE, 2, 320, 321, FAKE, FAKE, None) == binding.MARCHE_ERR_INVALID_ARG
+    assert L.select_refresh(FAKE, 0, FAKE, FAKE, 2, 320, 3, FAKE, FAKE, None) == binding.MARCHE_ERR_INVALID_ARG
+    assert L.select_refresh(FAKE, 16, FAKE, FAKE, 2, 5000, 3, FAKE, FAKE, None) == binding.MARCHE_ERR_INVALID_ARG
+    assert L.select_refresh(None, 16, FAKE, FAKE, 2, 320, 3, FAKE, FAKE, None) == binding.MARCHE_ERR_INVALID_ARG
+    assert L.select_refresh(FAKE, 16, FAKE, FAKE, 2, 320, 0, FAKE, FAKE, None) == binding.MARCHE_OK
+
+
+def test_kv_cache_init_and_decoder_input_validation():
+    L = binding.lib()
+    m = _model()
+    c = binding.KVCache()
+    need = 2 * 3 * 16 * 320 * 64 * 2
+    assert L.kv_cache_init(C.byref(c), C.byref(m), 3, FAKE, FAKE, need - 1, None, None, None) == binding.MARCHE_ERR_INVALID_ARG
+    assert L.kv_cache_init(C.byref(c), C.byref(m), 3, FAKE, FAKE, need, FAKE, None, None) == binding.MARCHE_ERR_INVALID_ARG
+    assert L.kv_cache_init(C.byref(c), C.byref(m), 3, FAKE + 2, FAKE, need, None, None, None) == binding.MARCHE_ERR_INVALID_ARG
+    assert L.kv_cache_init(None, C.byref(m), 3, FAKE, FAKE, need, None, None, None) == binding.MARCHE_ERR_INVALID_ARG
+    assert L.marche_decoder_input(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 2, 320, 64, 1024, 257, None) == binding.MARCHE_ERR_INVALID_ARG
+    assert L.marche_decoder_input(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 2, 320, 400, 1024, 0, None) == binding.MARCHE_ERR_INVALID_ARG
+    assert L.marche_decoder_input(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, 320, 64, 1024, 0, None) == binding.MARCHE_OK
+
+
+def test_profile_entry_bounds():
+    binding.profile_reset()
+    assert binding.lib().marche_profile_entry(-1, None, None, None, None, None) == binding.MARCHE_ERR_INVALID_ARG
+    assert binding.profile_collect() == {}
