@@ -1,0 +1,288 @@
+#!/usr/bin/env python3
+"""Benchmark of MARche's cache-aware decode step on one MI355X.
+
+A bench step is one MAR decoding step of the whole batch (all layers: decoder
+input, full-attention layers up to the selection layer with the score pass,
+refresh top-k, cache-aware layers).  Steps cycle through the 64-step schedule;
+the default --warmup 64 --steps 64 times exactly one complete generation.
+
+Printed (one JSON line on stdout):
+  value         images/s of the timed steps = batch * steps / 64 / wall seconds
+                (inputs, weights and every step's index lists already resident
+                in HBM; the timed region is bracketed by device syncs);
+  step_us       median step latency by step type;
+  full_recompute  the same kernels with every token active in every step;
+  roofline      the kernel with the most time in the timed steps, timed live
+                with HIP events on the launch stream, against MI355X peak;
+  kernels       every kernel class with its achieved rate;
+  cpu_baseline  the fp64 oracle on a bounded sample (one image, the first
+                steps of its schedule) on this host's cores, extrapolated.
+
+Workload: seeded synthetic MAR-shaped tensors (no dataset or trained weights).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MAR-L-shape step latency (µs), images/s, MFMA/HBM % of peak vs full recompute"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+HBM_BOUND = {"gather_ln", "attention_q32", "attention_q64", "attn_scores", "select_topk",
+             "decoder_input", "row_map", "fill_zero"}
+KERNEL_SOURCES = {
+    "gemm": "paper_2506_12035_amd/csrc/k_gemm.hip",
+    "attention": "paper_2506_12035_amd/csrc/k_attn.hip",
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def source_hash(kernel: str) -> str:
+    fam = "attention" if kernel.startswith("attention") or kernel == "attn_scores" else "gemm"
+    with open(os.path.join(ROOT, KERNEL_SOURCES[fam]), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic_for(kernel: str, workload: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    e = rec.get(workload, {}).get(kernel)
+    if not e or e.get("source_sha") != source_hash(kernel):
+        return None
+    return e.get("bytes_per_launch")
+
+
+def kernel_rates(prof: dict, dtype: str) -> dict:
+    out = {}
+    peak_mfma = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_FP32_TFLOPS
+    for name, e in prof.items():
+        avg_s = e["ms"] * 1e-3 / e["launches"]
+        if name in HBM_BOUND or e["flops"] == 0:
+            ach = e["bytes"] / e["launches"] / avg_s / 1e9
+            out[name] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": ach / PEAK_HBM_GBS}
+        else:
+            ach = e["flops"] / e["launches"] / avg_s / 1e12
+            out[name] = {"bound": "mfma", "achieved": ach, "peak": peak_mfma, "unit": "TFLOP/s",
+                         "frac": ach / peak_mfma}
+        out[name].update({"launches": e["launches"], "avg_us": avg_s * 1e6,
+                          "total_ms": e["ms"]})
+    return out
+
+
+def cpu_baseline(cfg, weights, budget_s: float, n_full_sched: int, n_ca_sched: int):
+    """Time the fp64 oracle on image 0's first decoding steps until `budget_s`
+    seconds have passed (at least one full and one cache-aware step), and
+    extrapolate images/s over the whole schedule."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import schedule as osched
+    from oracle import step as ostep
+    from paper_2506_12035_amd import workload
+
+    p64 = [{k: np.asarray(v, np.float64) for k, v in w.items()} for w in weights]
+    emb = workload.embeddings(cfg, 1)
+    order = workload.orders(cfg, 1)[0]
+    H, N, dh = cfg.n_heads, cfg.n_tokens, cfg.head_dim
+    kcs = [np.zeros((H, N, dh)) for _ in p64]
+    vcs = [np.zeros((H, N, dh)) for _ in p64]
+    t_full, t_ca = [], []
+    start = time.perf_counter()
+    t = 0
+    while t < cfg.n_steps:
+        gen = osched.generating_tokens(order, cfg.n_buf, cfg.n_steps, t)
+        cache = osched.caching_tokens(order, cfg.n_buf, cfg.n_steps, t)
+        known = osched.known_before(order, cfg.n_buf, cfg.n_steps, t)
+        full = osched.is_full_step(t, cfg.full_every)
+        k = ostep.refresh_count("ratio", cfg.ratio_bp, N, len(gen), len(cache))
+        t0 = time.perf_counter()
+        x = ostep.decoder_input(emb.cls[0], emb.value[0], emb.mask, emb.pos, known, cfg.n_buf)
+        res = ostep.marche_step(p64, x, kcs, vcs, gen, cache, n_heads=H, eps=cfg.ln_eps,
+                                sel_layer=cfg.sel_layer, full=full, k_refresh=k)
+        (t_full if full else t_ca).append(time.perf_counter() - t0)
+        kcs, vcs = res.k_caches, res.v_caches
+        t += 1
+        log(f"  cpu oracle step {t - 1} ({'full' if full else 'cache-aware'}): "
+            f"{(t_full if full else t_ca)[-1]:.2f} s")
+        if t_full and t_ca and time.perf_counter() - start > budget_s:
+            break
+    tf, tc = statistics.mean(t_full), statistics.mean(t_ca)
+    per_image = n_full_sched * tf + n_ca_sched * tc
+    threads = sum(i.get("num_threads", 0) for i in threadpool_info() if i.get("user_api") == "blas")
+    return {
+        "value": 1.0 / per_image,
+        "unit": "images/s",
+        "cores": threads or len(os.sched_getaffinity(0)),
+        "kind": "oracle",
+        "sample": (f"fp64 numpy oracle, image 0, steps 0..{t - 1} of the 64-step schedule "
+                   f"({len(t_full)} full at {tf:.2f} s, {len(t_ca)} cache-aware at {tc:.2f} s); "
+                   f"images/s = 1 / ({n_full_sched} x full + {n_ca_sched} x cache-aware); "
+                   f"images are independent, so the batch adds no per-image work"),
+    }
+
+
+def timed(eng, steps, first, T):
+    import torch
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    evs[0].record()
+    for i in range(steps):
+        eng.step((first + i) % T)
+        evs[i + 1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = [evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(steps)]
+    kinds = [eng.plans[(first + i) % T].full for i in range(steps)]
+    return wall, per, kinds
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=64)
+    ap.add_argument("--config", type=int, default=3, help="workload id (2: MAR-B, 3: MAR-L, 4: MAR-H, 5: high-res)")
+    ap.add_argument("--batch", type=int, default=None)
+    ap.add_argument("--ratio-bp", type=int, default=None, help="refresh ratio in basis points")
+    ap.add_argument("--full-every", type=int, default=None)
+    ap.add_argument("--no-full-recompute", action="store_true")
+    ap.add_argument("--no-roofline", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=20.0)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
+              "the decode step shards over images without collectives and no multi-GPU run is "
+              "part of this build", file=sys.stderr)
+        return 2
+    if args.steps < 1 or args.warmup < 0:
+        print("--steps must be >= 1 and --warmup >= 0", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2506_12035_amd import binding, driver, schedule, workload
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    cfg = workload.CONFIGS[args.config]
+    if args.config == 1:
+        print("the single-block case is a parity case, not a bench workload", file=sys.stderr)
+        return 2
+    if args.ratio_bp is not None:
+        cfg = cfg.with_(ratio_bp=args.ratio_bp)
+    if args.full_every is not None:
+        cfg = cfg.with_(full_every=args.full_every)
+    B = cfg.batch if args.batch is None else args.batch
+    T = cfg.n_steps
+
+    log(f"[bench] workload {cfg.name}: generating weights")
+    weights = workload.all_weights(cfg)
+    log("[bench] uploading")
+    eng = driver.Engine(cfg, batch=B, weights=weights)
+    torch.cuda.synchronize()
+
+    log(f"[bench] warmup {args.warmup} steps")
+    for i in range(args.warmup):
+        eng.step(i % T)
+    torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} steps")
+    first = args.warmup % T
+    wall, per, kinds = timed(eng, args.steps, first, T)
+    value = B * args.steps / T / wall
+    step_us = {}
+    full_us = [p for p, f in zip(per, kinds) if f]
+    ca_us = [p for p, f in zip(per, kinds) if not f]
+    if full_us:
+        step_us["full"] = statistics.median(full_us)
+    if ca_us:
+        step_us["cache_aware"] = statistics.median(ca_us)
+    log(f"[bench] {value:.2f} images/s, {wall / args.steps * 1e3:.3f} ms/step, {step_us}")
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "images/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": cfg.dtype, "data": "synthetic",
+        "config": {"workload": cfg.name, "batch": B, "n_tokens": cfg.n_tokens,
+                   "n_image_tokens": cfg.n_img, "n_layers": cfg.n_layers,
+                   "d_model": cfg.d_model, "n_heads": cfg.n_heads, "head_dim": cfg.head_dim,
+                   "refresh_ratio": cfg.ratio_bp / 10000, "sel_layer": cfg.sel_layer,
+                   "full_every": cfg.full_every, "decode_steps": T,
+                   "full_steps_in_schedule": sum(p.full for p in eng.plans)},
+        "step_us": step_us,
+    }
+
+    if not args.no_full_recompute:
+        eng.set_schedule(1, "ratio", 10000)
+        n = min(args.steps, T)
+        for i in range(2):
+            eng.step(i)
+        log(f"[bench] full recompute: timing {n} steps")
+        fwall, fper, _ = timed(eng, n, 0, T)
+        fv = B * n / T / fwall
+        out["full_recompute"] = {"images_per_s": fv, "step_us": statistics.median(fper)}
+        out["speedup_vs_full_recompute"] = value / fv
+        log(f"[bench] full recompute {fv:.2f} images/s -> speedup {value / fv:.3f}")
+        eng.set_schedule(cfg.full_every, "ratio", cfg.ratio_bp)
+
+    if not args.no_roofline:
+        log(f"[bench] instrumented pass over the same {args.steps} steps")
+        for i in range(args.warmup):
+            eng.step(i % T)
+        torch.cuda.synchronize()
+        binding.profile_reset()
+        binding.profile_enable(True)
+        for i in range(args.steps):
+            eng.step((first + i) % T)
+        torch.cuda.synchronize()
+        binding.profile_enable(False)
+        prof = binding.profile_collect()
+        rates = kernel_rates(prof, cfg.dtype)
+        dom = max(rates, key=lambda k: rates[k]["total_ms"])
+        r = rates[dom]
+        tr = traffic_for(dom, cfg.name)
+        out["roofline"] = {"kernel": dom, "bound": r["bound"], "achieved": r["achieved"],
+                           "peak": r["peak"], "unit": r["unit"], "frac": r["frac"],
+                           "traffic": tr, "avg_us": r["avg_us"], "launches": r["launches"]}
+        out["kernels"] = {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv)
+                              for kk, vv in v.items()} for k, v in
+                          sorted(rates.items(), key=lambda kv: -kv[1]["total_ms"])}
+        log(f"[bench] dominant kernel {dom}: {r['achieved']:.1f} {r['unit']} ({r['frac']:.1%})")
+
+    del eng
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (fp64 oracle)")
+        n_full = sum(schedule.full_step(t, cfg.full_every) for t in range(T))
+        out["cpu_baseline"] = cpu_baseline(cfg, weights, args.cpu_budget_s, n_full, T - n_full)
+
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

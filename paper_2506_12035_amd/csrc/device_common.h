@@ -6,6 +6,10 @@
 
 namespace marche {
 
+// Native 16-byte vector (HIP's uint4 is a struct with a union, which keeps
+// arrays of it from being promoted to registers).
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

@@ -77,15 +77,15 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
   for (int s = 0; s < QS; ++s)
     qf[s] = *reinterpret_cast<const bf16x8 *>(qrow + s * 16 + (lane >> 5) * 8);
 
-  uint4 rk[LPT], rv[LPT];
+  u32x4 rk[LPT], rv[LPT];
   auto gload = [&](int t0) {
 #pragma unroll
     for (int i = 0; i < LPT; ++i) {
       const int c = i * NT + tid;
       if (c < TCH) {
         const int key = min(t0 + c / CPR, N - 1), d = (c % CPR) * 8;
-        rk[i] = *reinterpret_cast<const uint4 *>(kg + (size_t)key * DH + d);
-        rv[i] = *reinterpret_cast<const uint4 *>(vg + (size_t)key * DH + d);
+        rk[i] = *reinterpret_cast<const u32x4 *>(kg + (size_t)key * DH + d);
+        rv[i] = *reinterpret_cast<const u32x4 *>(vg + (size_t)key * DH + d);
       }
     }
   };
@@ -95,7 +95,7 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
       const int c = i * NT + tid;
       if (c < TCH) {
         const int key = c / CPR, d = (c % CPR) * 8;
-        *reinterpret_cast<uint4 *>(&Ks[buf][key * KS + d]) = rk[i];
+        *reinterpret_cast<u32x4 *>(&Ks[buf][key * KS + d]) = rk[i];
         const bf16x8 v = __builtin_bit_cast(bf16x8, rv[i]);
         const int pos = (key & ~15) | vperm16(key & 15);
 #pragma unroll
@@ -116,7 +116,8 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
   __syncthreads();
   for (int t = 0; t < ntiles; ++t) {
     const int cur = t & 1, t0 = t * TK;
-    if (t + 1 < ntiles) gload(t0 + TK);
+    const bool more = t + 1 < ntiles;
+    if (more) gload(t0 + TK);
 
     // S^T for two 32-key blocks: lane -> query (lane & 31),
     // register r -> key (r / 4) * 8 + (lane / 32) * 4 + r % 4 of the block.
@@ -174,7 +175,7 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
         }
       }
 
-    if (t + 1 < ntiles) sstore(cur ^ 1);
+    if (more) sstore(cur ^ 1);
     __syncthreads();
   }
 

@@ -49,6 +49,9 @@ struct EpiQkv {
   }
 };
 
+// TAG only distinguishes the output projection (0) from fc2 (1) as kernel
+// symbols, so per-kernel profiles can tell them apart.
+template <int TAG>
 struct EpiResid {
   float *x;
   const float *bias;
@@ -72,17 +75,20 @@ struct EpiGelu {
 
 // ------------------------------------------------------------------ bf16 MFMA
 
-template <int BM_, int BN_, int BK_>
+template <int BM_, int BN_, int BK_, int WGM_, int WGN_>
 struct TileCfg {
   static constexpr int BM = BM_, BN = BN_, BK = BK_;
-  static constexpr int NT = 256;               // 4 wavefronts, 2 x 2
-  static constexpr int WM = BM / 2, WN = BN / 2;
+  static constexpr int WGM = WGM_, WGN = WGN_;  // wavefront grid
+  static constexpr int NT = WGM * WGN * 64;
+  static constexpr int WM = BM / WGM, WN = BN / WGN;
   static constexpr int TM = WM / 32, TN = WN / 32;
   static constexpr int LDS_STRIDE = BK + 8;    // elements; +16 bytes per row
   static constexpr int CPR = BK / 8;           // 16-byte chunks per tile row
   static constexpr int A_CHUNKS = BM * CPR / NT;
   static constexpr int B_CHUNKS = BN * CPR / NT;
+  static constexpr int LDS_BYTES = 2 * (BM + BN) * LDS_STRIDE * 2;
   static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile not divisible");
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
 };
 
 // Grouped tile order: GROUP consecutive tile rows sweep all tile columns
@@ -98,12 +104,71 @@ __device__ __forceinline__ void tile_coords(int id, int tiles_m, int tiles_n, in
   tn = in / gm;
 }
 
+template <class Cfg>
+struct Stage {
+  u32x4 a[Cfg::A_CHUNKS];
+  u32x4 b[Cfg::B_CHUNKS];
+};
+
+template <class Cfg>
+__device__ __forceinline__ void stage_load(Stage<Cfg> &st, const bf16 *__restrict__ A,
+                                           const bf16 *__restrict__ W, int M, int K, int m0,
+                                           int n0, int k0, int tid) {
+#pragma unroll
+  for (int i = 0; i < Cfg::A_CHUNKS; ++i) {
+    const int c = i * Cfg::NT + tid, row = c / Cfg::CPR, col = (c % Cfg::CPR) * 8;
+    const int grow = min(m0 + row, M - 1);
+    st.a[i] = *reinterpret_cast<const u32x4 *>(A + (size_t)grow * K + k0 + col);
+  }
+#pragma unroll
+  for (int i = 0; i < Cfg::B_CHUNKS; ++i) {
+    const int c = i * Cfg::NT + tid, row = c / Cfg::CPR, col = (c % Cfg::CPR) * 8;
+    st.b[i] = *reinterpret_cast<const u32x4 *>(W + (size_t)(n0 + row) * K + k0 + col);
+  }
+}
+
+template <class Cfg>
+__device__ __forceinline__ void stage_store(const Stage<Cfg> &st, bf16 *As, bf16 *Bs, int tid) {
+#pragma unroll
+  for (int i = 0; i < Cfg::A_CHUNKS; ++i) {
+    const int c = i * Cfg::NT + tid, row = c / Cfg::CPR, col = (c % Cfg::CPR) * 8;
+    *reinterpret_cast<u32x4 *>(&As[row * Cfg::LDS_STRIDE + col]) = st.a[i];
+  }
+#pragma unroll
+  for (int i = 0; i < Cfg::B_CHUNKS; ++i) {
+    const int c = i * Cfg::NT + tid, row = c / Cfg::CPR, col = (c % Cfg::CPR) * 8;
+    *reinterpret_cast<u32x4 *>(&Bs[row * Cfg::LDS_STRIDE + col]) = st.b[i];
+  }
+}
+
+// One BK-deep slab of MFMAs for this wavefront's TM x TN block of 32x32 tiles.
+template <class Cfg>
+__device__ __forceinline__ void tile_mfma(f32x16 (&acc)[Cfg::TM][Cfg::TN], const bf16 *As,
+                                          const bf16 *Bs, int wm, int wn, int lane) {
+  constexpr int LS = Cfg::LDS_STRIDE;
+  const int lrow = lane & 31, lk = (lane >> 5) * 8;
+#pragma unroll
+  for (int kk = 0; kk < Cfg::BK; kk += 16) {
+    bf16x8 af[Cfg::TM], bw[Cfg::TN];
+#pragma unroll
+    for (int i = 0; i < Cfg::TM; ++i)
+      af[i] = *reinterpret_cast<const bf16x8 *>(&As[(wm * Cfg::WM + i * 32 + lrow) * LS + kk + lk]);
+#pragma unroll
+    for (int j = 0; j < Cfg::TN; ++j)
+      bw[j] = *reinterpret_cast<const bf16x8 *>(&Bs[(wn * Cfg::WN + j * 32 + lrow) * LS + kk + lk]);
+#pragma unroll
+    for (int i = 0; i < Cfg::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < Cfg::TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bw[j], acc[i][j], 0, 0, 0);
+  }
+}
+
 template <class Cfg, class Epi>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16 *__restrict__ A,
-                                                        const bf16 *__restrict__ W, int M, int N,
-                                                        int K, Epi epi) {
-  constexpr int BM = Cfg::BM, BN = Cfg::BN, BK = Cfg::BK, NT = Cfg::NT;
-  constexpr int LS = Cfg::LDS_STRIDE, CPR = Cfg::CPR;
+__global__ __launch_bounds__(Cfg::NT) void gemm_bf16_kernel(const bf16 *__restrict__ A,
+                                                            const bf16 *__restrict__ W, int M,
+                                                            int N, int K, Epi epi) {
+  constexpr int BM = Cfg::BM, BN = Cfg::BN, BK = Cfg::BK, LS = Cfg::LDS_STRIDE;
   __shared__ __attribute__((aligned(16))) bf16 As[2][BM * LS];
   __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * LS];
 
@@ -112,34 +177,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16 *__restrict__
   tile_coords(xcd_remap(blockIdx.x, gridDim.x), tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-
-  uint4 ra[Cfg::A_CHUNKS], rb[Cfg::B_CHUNKS];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < Cfg::A_CHUNKS; ++i) {
-      const int c = i * NT + tid, row = c / CPR, col = (c % CPR) * 8;
-      const int grow = min(m0 + row, M - 1);
-      ra[i] = *reinterpret_cast<const uint4 *>(A + (size_t)grow * K + k0 + col);
-    }
-#pragma unroll
-    for (int i = 0; i < Cfg::B_CHUNKS; ++i) {
-      const int c = i * NT + tid, row = c / CPR, col = (c % CPR) * 8;
-      rb[i] = *reinterpret_cast<const uint4 *>(W + (size_t)(n0 + row) * K + k0 + col);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < Cfg::A_CHUNKS; ++i) {
-      const int c = i * NT + tid, row = c / CPR, col = (c % CPR) * 8;
-      *reinterpret_cast<uint4 *>(&As[buf][row * LS + col]) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < Cfg::B_CHUNKS; ++i) {
-      const int c = i * NT + tid, row = c / CPR, col = (c % CPR) * 8;
-      *reinterpret_cast<uint4 *>(&Bs[buf][row * LS + col]) = rb[i];
-    }
-  };
+  const int wm = wave / Cfg::WGN, wn = wave % Cfg::WGN;
 
   f32x16 acc[Cfg::TM][Cfg::TN];
 #pragma unroll
@@ -147,34 +185,21 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16 *__restrict__
 #pragma unroll
     for (int j = 0; j < Cfg::TN; ++j) acc[i][j] = f32x16{};
 
+  // Software pipeline: the global loads of k-tile t+1 are issued before the
+  // MFMAs of k-tile t and land in the other LDS buffer after them.
   const int nk = K / BK;
-  gload(0);
-  sstore(0);
+  Stage<Cfg> st;
+  stage_load<Cfg>(st, A, W, M, K, m0, n0, 0, tid);
+  stage_store<Cfg>(st, As[0], Bs[0], tid);
   __syncthreads();
-  const int lrow = lane & 31, lk = (lane >> 5) * 8;
-  for (int kt = 0; kt < nk; ++kt) {
+  for (int kt = 0; kt + 1 < nk; ++kt) {
     const int cur = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
-#pragma unroll
-    for (int kk = 0; kk < BK; kk += 16) {
-      bf16x8 af[Cfg::TM], bw[Cfg::TN];
-#pragma unroll
-      for (int i = 0; i < Cfg::TM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8 *>(
-            &As[cur][(wm * Cfg::WM + i * 32 + lrow) * LS + kk + lk]);
-#pragma unroll
-      for (int j = 0; j < Cfg::TN; ++j)
-        bw[j] = *reinterpret_cast<const bf16x8 *>(
-            &Bs[cur][(wn * Cfg::WN + j * 32 + lrow) * LS + kk + lk]);
-#pragma unroll
-      for (int i = 0; i < Cfg::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < Cfg::TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bw[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < nk) sstore(cur ^ 1);
+    stage_load<Cfg>(st, A, W, M, K, m0, n0, (kt + 1) * BK, tid);
+    tile_mfma<Cfg>(acc, As[cur], Bs[cur], wm, wn, lane);
+    stage_store<Cfg>(st, As[cur ^ 1], Bs[cur ^ 1], tid);
     __syncthreads();
   }
+  tile_mfma<Cfg>(acc, As[(nk - 1) & 1], Bs[(nk - 1) & 1], wm, wn, lane);
 
   // 32x32 accumulator layout: lane -> column (lane & 31); register r ->
   // row (r / 4) * 8 + (lane / 32) * 4 + r % 4.
@@ -193,18 +218,32 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16 *__restrict__
   }
 }
 
-using Tile128 = TileCfg<128, 128, 64>;
+// 128x128 tile, 2x2 wavefronts of 64x64: two workgroups per CU; used when
+// the 256x256 grid would leave CUs idle.
+using TileS = TileCfg<128, 128, 64, 2, 2>;
+// 256x256 tile, 2x2 wavefronts of 128x128 (accumulators in AGPRs): one
+// workgroup per CU, four times the MFMA work per k-tile and per LDS byte.
+using TileL = TileCfg<256, 256, 64, 2, 2>;
 
-template <class Epi>
-static hipError_t run_bf16(const void *a, const void *w, int m, int n, int k, const Epi &epi,
-                           hipStream_t s) {
-  using C = Tile128;
-  if (m == 0) return hipSuccess;
-  if (n % C::BN != 0 || k % C::BK != 0) return hipErrorInvalidValue;
+template <class C, class Epi>
+static hipError_t launch_tile(const void *a, const void *w, int m, int n, int k, const Epi &epi,
+                              hipStream_t s) {
   const int grid = ((m + C::BM - 1) / C::BM) * (n / C::BN);
   gemm_bf16_kernel<C, Epi><<<grid, C::NT, 0, s>>>(static_cast<const bf16 *>(a),
                                                   static_cast<const bf16 *>(w), m, n, k, epi);
   return hipGetLastError();
+}
+
+template <class Epi>
+static hipError_t run_bf16(const void *a, const void *w, int m, int n, int k, const Epi &epi,
+                           hipStream_t s) {
+  if (m == 0) return hipSuccess;
+  if (n % TileS::BN != 0 || k % TileS::BK != 0) return hipErrorInvalidValue;
+  // 256 CUs: prefer the large tile when it still yields at least two
+  // workgroups per CU.
+  const long large_tiles = (long)((m + TileL::BM - 1) / TileL::BM) * (n / TileL::BN);
+  if (n % TileL::BN == 0 && large_tiles >= 512) return launch_tile<TileL>(a, w, m, n, k, epi, s);
+  return launch_tile<TileS>(a, w, m, n, k, epi, s);
 }
 
 // ------------------------------------------------------------------ fp32 FMA
@@ -279,8 +318,13 @@ hipError_t launch_gemm_qkv(DType dt, const void *a, const void *w, const float *
 }
 
 hipError_t launch_gemm_resid(DType dt, const void *a, const void *w, const float *bias, int32_t m,
-                             int32_t n, int32_t k, const RowMap *map, float *x, hipStream_t s) {
-  EpiResid e{x, bias, map, n};
+                             int32_t n, int32_t k, const RowMap *map, float *x, int32_t tag,
+                             hipStream_t s) {
+  if (tag == 0) {
+    EpiResid<0> e{x, bias, map, n};
+    return dt == DType::F32 ? run_f32(a, w, m, n, k, e, s) : run_bf16(a, w, m, n, k, e, s);
+  }
+  EpiResid<1> e{x, bias, map, n};
   return dt == DType::F32 ? run_f32(a, w, m, n, k, e, s) : run_bf16(a, w, m, n, k, e, s);
 }
 

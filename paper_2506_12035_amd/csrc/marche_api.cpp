@@ -61,13 +61,19 @@ marche_status_t check_model(const marche_model_t *m) {
 
 // ------------------------------------------------------------------ profiling
 
+// One class per kernel symbol family.  The attention kernel is instantiated
+// per query-chunk width (1, 2 or 4 wavefronts of 32 queries), chosen from the
+// largest active set of the call.
 enum KClass {
-  K_ROW_MAP, K_GATHER_LN, K_GEMM_QKV, K_ATTN, K_ATTN_SCORES, K_GEMM_O, K_GEMM_FC1, K_GEMM_FC2,
-  K_SELECT, K_DECODER_INPUT, K_FILL, K_NCLASS
+  K_ROW_MAP, K_GATHER_LN, K_GEMM_QKV, K_ATTN_W1, K_ATTN_W2, K_ATTN_W4, K_ATTN_SCORES, K_GEMM_O,
+  K_GEMM_FC1, K_GEMM_FC2, K_SELECT, K_DECODER_INPUT, K_FILL, K_NCLASS
 };
 const char *const kClassNames[K_NCLASS] = {
-    "row_map", "gather_ln",  "gemm_qkv", "attention", "attn_scores", "gemm_o",
-    "gemm_fc1", "gemm_fc2", "select_topk", "decoder_input", "fill_zero"};
+    "row_map",     "gather_ln", "gemm_qkv", "attention_q32", "attention_q64", "attention_q128",
+    "attn_scores", "gemm_o",    "gemm_fc1", "gemm_fc2",      "select_topk",   "decoder_input",
+    "fill_zero"};
+
+int attn_class(int a_max) { return a_max <= 32 ? K_ATTN_W1 : (a_max <= 64 ? K_ATTN_W2 : K_ATTN_W4); }
 
 struct Pending {
   int cls;
@@ -274,7 +280,7 @@ marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layer
     AttnArgs aa{buf1, kc, vc, buf0, a_off, map, batch, H, N, dh, D, M, a_max};
     // Algorithmic traffic: every cached K/V element of the batch read once,
     // plus the queries read and the outputs written.
-    LAUNCH(K_ATTN, 4.0 * M * N * D, es * (2.0 * batch * N * D + 2.0 * M * D),
+    LAUNCH(attn_class(a_max), 4.0 * M * N * D, es * (2.0 * batch * N * D + 2.0 * M * D),
            launch_attention(dt, aa, stream));
     if (want_scores && l == score_layer) {
       LAUNCH(K_ATTN_SCORES, 2.0 * batch * gen_max * N * D,
@@ -283,7 +289,7 @@ marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layer
     }
     LAUNCH(K_GEMM_O, 2.0 * M * D * D, gemm_bytes_act * ((double)M * D + (double)D * D) + 8.0 * M * D,
            launch_gemm_resid(dt, buf0, L.w_o, static_cast<const float *>(L.b_o), M, D, D, map, x,
-                             stream));
+                             0, stream));
     LAUNCH(K_GATHER_LN, 0, (double)M * D * (4 + es),
            launch_gather_ln(dt, buf1, x, map, static_cast<const float *>(L.ln2_g),
                             static_cast<const float *>(L.ln2_b), M, D, m->ln_eps, stream));
@@ -294,7 +300,7 @@ marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layer
     LAUNCH(K_GEMM_FC2, 2.0 * M * D * F,
            gemm_bytes_act * ((double)M * F + (double)D * F) + 8.0 * M * D,
            launch_gemm_resid(dt, hid, L.w_2, static_cast<const float *>(L.b_2), M, D, F, map, x,
-                             stream));
+                             1, stream));
   }
   return MARCHE_OK;
 }

@@ -51,8 +51,10 @@ struct QkvOut {
 };
 hipError_t launch_gemm_qkv(DType dt, const void *a, const void *w, const float *bias, int32_t m,
                            int32_t n, int32_t k, const RowMap *map, QkvOut out, hipStream_t s);
+// tag: 0 = output projection, 1 = fc2 (separate kernel symbols)
 hipError_t launch_gemm_resid(DType dt, const void *a, const void *w, const float *bias, int32_t m,
-                             int32_t n, int32_t k, const RowMap *map, float *x, hipStream_t s);
+                             int32_t n, int32_t k, const RowMap *map, float *x, int32_t tag,
+                             hipStream_t s);
 hipError_t launch_gemm_gelu(DType dt, const void *a, const void *w, const float *bias, int32_t m,
                             int32_t n, int32_t k, void *h, hipStream_t s);
 

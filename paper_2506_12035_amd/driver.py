@@ -102,7 +102,13 @@ class Engine:
         self.e_mask = torch.from_numpy(emb.mask).to(self.device)
         self.e_pos = torch.from_numpy(emb.pos).to(self.device)
         self.rank = _dev_i32(rank, self.device)
-        self.plans = [self._plan(t) for t in range(cfg.n_steps)]
+        self.set_schedule(self.full_every, self.policy, self.budget)
+
+    def set_schedule(self, full_every: int, policy: str, budget: int) -> None:
+        """(Re)build the resident index lists of every step for a schedule:
+        ``full_every`` = 1 with any budget is full recomputation."""
+        self.full_every, self.policy, self.budget = full_every, policy, budget
+        self.plans = [self._plan(t) for t in range(self.cfg.n_steps)]
 
     @property
     def stream(self):
