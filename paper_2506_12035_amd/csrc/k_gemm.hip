@@ -9,12 +9,12 @@
 //   - adds into the float32 residual stream row     (output projection, fc2)
 //   - applies exact GELU and stores the hidden row  (fc1)
 //
-// bf16 path: workgroup tile BM x BN x BK, 2x2 wavefronts, each wavefront a
-// (BM/2) x (BN/2) block of 32x32 MFMA tiles (v_mfma_f32_32x32x16_bf16, fp32
-// accumulators).  Tiles are staged global -> registers -> LDS with double
-// buffering: the loads of k-tile t+1 are in flight while k-tile t is computed.
-// LDS rows are padded by 16 bytes, which makes the 16-byte MFMA operand reads
-// (32 rows at one k offset) bank-conflict free.
+// bf16 path: workgroup tile BM x BN x BK, a grid of wavefronts each owning a
+// block of 32x32 MFMA tiles (v_mfma_f32_32x32x16_bf16, fp32 accumulators).
+// Tiles are staged global -> registers -> LDS (double-buffered LDS, one or
+// two k-tiles of register prefetch).  LDS rows are padded by 16 bytes, which
+// makes the 16-byte MFMA operand reads (32 rows at one k offset) bank-conflict
+// free.
 //
 // fp32 path: plain FMA, 64x64 tiles, 4x4 outputs per thread.
 #include "device_common.h"
@@ -22,6 +22,25 @@
 namespace marche {
 
 // ------------------------------------------------------------------ epilogues
+//
+// Every epilogue receives four consecutive output columns col0..col0+3 of one
+// row (col0 a multiple of 4), so each lane issues 8- or 16-byte stores.  Four
+// consecutive columns never straddle a q|k|v third or a head (d_model and
+// head_dim are multiples of 4).
+
+template <typename T>
+__device__ __forceinline__ void store4(T *p, f32x4 v) {
+  if constexpr (sizeof(T) == 4) {
+    *reinterpret_cast<f32x4 *>(p) = v;
+  } else {
+    bf16x4 pk = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
+    *reinterpret_cast<bf16x4 *>(p) = pk;
+  }
+}
+
+__device__ __forceinline__ f32x4 load_bias4(const float *bias, int col0) {
+  return *reinterpret_cast<const f32x4 *>(bias + col0);
+}
 
 template <typename T>
 struct EpiQkv {
@@ -31,13 +50,13 @@ struct EpiQkv {
   const float *bias;
   const RowMap *map;
   int d_model, head_dim, n_heads, n_tokens;
-  __device__ __forceinline__ void operator()(int row, int col, float v) const {
-    v += bias[col];
-    if (col < d_model) {
-      q[(size_t)row * d_model + col] = from_f32<T>(v);
+  __device__ __forceinline__ void operator()(int row, int col0, f32x4 v) const {
+    v += load_bias4(bias, col0);
+    if (col0 < d_model) {
+      store4(q + (size_t)row * d_model + col0, v);
       return;
     }
-    int c = col - d_model;
+    int c = col0 - d_model;
     T *dst = kc;
     if (c >= d_model) {
       c -= d_model;
@@ -45,7 +64,7 @@ struct EpiQkv {
     }
     const int h = c / head_dim, d = c - h * head_dim;
     const RowMap m = map[row];
-    dst[((size_t)(m.b * n_heads + h) * n_tokens + m.tok) * head_dim + d] = from_f32<T>(v);
+    store4(dst + ((size_t)(m.b * n_heads + h) * n_tokens + m.tok) * head_dim + d, v);
   }
 };
 
@@ -57,9 +76,9 @@ struct EpiResid {
   const float *bias;
   const RowMap *map;
   int n;
-  __device__ __forceinline__ void operator()(int row, int col, float v) const {
-    float *p = x + (size_t)map[row].x_row * n + col;
-    *p = *p + (v + bias[col]);
+  __device__ __forceinline__ void operator()(int row, int col0, f32x4 v) const {
+    f32x4 *p = reinterpret_cast<f32x4 *>(x + (size_t)map[row].x_row * n + col0);
+    *p = *p + (v + load_bias4(bias, col0));
   }
 };
 
@@ -68,27 +87,37 @@ struct EpiGelu {
   T *h;
   const float *bias;
   int n;
-  __device__ __forceinline__ void operator()(int row, int col, float v) const {
-    h[(size_t)row * n + col] = from_f32<T>(gelu_erf(v + bias[col]));
+  __device__ __forceinline__ void operator()(int row, int col0, f32x4 v) const {
+    v += load_bias4(bias, col0);
+    f32x4 g = {gelu_erf(v[0]), gelu_erf(v[1]), gelu_erf(v[2]), gelu_erf(v[3])};
+    store4(h + (size_t)row * n + col0, g);
   }
 };
 
 // ------------------------------------------------------------------ bf16 MFMA
+//
+// The MFMA A operand is a 32-row slice of W (output columns) and the B
+// operand a 32-row slice of the activations (output rows), so each 32x32
+// accumulator holds a block of C^T: lane l owns output row (l & 31) and, in
+// register r, output column (r / 4) * 8 + (l / 32) * 4 + r % 4 -- four
+// consecutive columns per group of four registers, which the epilogue stores
+// together.
 
-template <int BM_, int BN_, int BK_, int WGM_, int WGN_>
+template <int BM_, int BN_, int BK_, int WGM_, int WGN_, int PF_, int MINB_>
 struct TileCfg {
   static constexpr int BM = BM_, BN = BN_, BK = BK_;
   static constexpr int WGM = WGM_, WGN = WGN_;  // wavefront grid
+  static constexpr int PF = PF_;                // k-tiles staged in registers ahead
+  static constexpr int MINB = MINB_;            // workgroups per CU to budget registers for
   static constexpr int NT = WGM * WGN * 64;
   static constexpr int WM = BM / WGM, WN = BN / WGN;
   static constexpr int TM = WM / 32, TN = WN / 32;
-  static constexpr int LDS_STRIDE = BK + 8;    // elements; +16 bytes per row
-  static constexpr int CPR = BK / 8;           // 16-byte chunks per tile row
+  static constexpr int LS = BK + 8;             // LDS row stride (elements): +16 bytes
+  static constexpr int CPR = BK / 8;            // 16-byte chunks per tile row
   static constexpr int A_CHUNKS = BM * CPR / NT;
   static constexpr int B_CHUNKS = BN * CPR / NT;
-  static constexpr int LDS_BYTES = 2 * (BM + BN) * LDS_STRIDE * 2;
   static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile not divisible");
-  static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
+  static_assert(2 * (BM + BN) * LS * 2 <= 160 * 1024, "LDS budget");
 };
 
 // Grouped tile order: GROUP consecutive tile rows sweep all tile columns
@@ -104,126 +133,150 @@ __device__ __forceinline__ void tile_coords(int id, int tiles_m, int tiles_n, in
   tn = in / gm;
 }
 
-template <class Cfg>
+template <class C>
 struct Stage {
-  u32x4 a[Cfg::A_CHUNKS];
-  u32x4 b[Cfg::B_CHUNKS];
+  u32x4 a[C::A_CHUNKS];
+  u32x4 b[C::B_CHUNKS];
 };
 
-template <class Cfg>
-__device__ __forceinline__ void stage_load(Stage<Cfg> &st, const bf16 *__restrict__ A,
+template <class C>
+__device__ __forceinline__ void stage_load(Stage<C> &st, const bf16 *__restrict__ A,
                                            const bf16 *__restrict__ W, int M, int K, int m0,
                                            int n0, int k0, int tid) {
 #pragma unroll
-  for (int i = 0; i < Cfg::A_CHUNKS; ++i) {
-    const int c = i * Cfg::NT + tid, row = c / Cfg::CPR, col = (c % Cfg::CPR) * 8;
-    const int grow = min(m0 + row, M - 1);
-    st.a[i] = *reinterpret_cast<const u32x4 *>(A + (size_t)grow * K + k0 + col);
+  for (int i = 0; i < C::A_CHUNKS; ++i) {
+    const int c = i * C::NT + tid, row = c / C::CPR, col = (c % C::CPR) * 8;
+    st.a[i] = *reinterpret_cast<const u32x4 *>(A + (size_t)min(m0 + row, M - 1) * K + k0 + col);
   }
 #pragma unroll
-  for (int i = 0; i < Cfg::B_CHUNKS; ++i) {
-    const int c = i * Cfg::NT + tid, row = c / Cfg::CPR, col = (c % Cfg::CPR) * 8;
+  for (int i = 0; i < C::B_CHUNKS; ++i) {
+    const int c = i * C::NT + tid, row = c / C::CPR, col = (c % C::CPR) * 8;
     st.b[i] = *reinterpret_cast<const u32x4 *>(W + (size_t)(n0 + row) * K + k0 + col);
   }
 }
 
-template <class Cfg>
-__device__ __forceinline__ void stage_store(const Stage<Cfg> &st, bf16 *As, bf16 *Bs, int tid) {
+template <class C>
+__device__ __forceinline__ void stage_store(const Stage<C> &st, bf16 *As, bf16 *Bs, int tid) {
 #pragma unroll
-  for (int i = 0; i < Cfg::A_CHUNKS; ++i) {
-    const int c = i * Cfg::NT + tid, row = c / Cfg::CPR, col = (c % Cfg::CPR) * 8;
-    *reinterpret_cast<u32x4 *>(&As[row * Cfg::LDS_STRIDE + col]) = st.a[i];
+  for (int i = 0; i < C::A_CHUNKS; ++i) {
+    const int c = i * C::NT + tid, row = c / C::CPR, col = (c % C::CPR) * 8;
+    *reinterpret_cast<u32x4 *>(&As[row * C::LS + col]) = st.a[i];
   }
 #pragma unroll
-  for (int i = 0; i < Cfg::B_CHUNKS; ++i) {
-    const int c = i * Cfg::NT + tid, row = c / Cfg::CPR, col = (c % Cfg::CPR) * 8;
-    *reinterpret_cast<u32x4 *>(&Bs[row * Cfg::LDS_STRIDE + col]) = st.b[i];
+  for (int i = 0; i < C::B_CHUNKS; ++i) {
+    const int c = i * C::NT + tid, row = c / C::CPR, col = (c % C::CPR) * 8;
+    *reinterpret_cast<u32x4 *>(&Bs[row * C::LS + col]) = st.b[i];
   }
 }
 
-// One BK-deep slab of MFMAs for this wavefront's TM x TN block of 32x32 tiles.
-template <class Cfg>
-__device__ __forceinline__ void tile_mfma(f32x16 (&acc)[Cfg::TM][Cfg::TN], const bf16 *As,
+// One BK-deep slab of MFMAs for this wavefront's block of 32x32 tiles.
+template <class C>
+__device__ __forceinline__ void tile_mfma(f32x16 (&acc)[C::TN][C::TM], const bf16 *As,
                                           const bf16 *Bs, int wm, int wn, int lane) {
-  constexpr int LS = Cfg::LDS_STRIDE;
   const int lrow = lane & 31, lk = (lane >> 5) * 8;
 #pragma unroll
-  for (int kk = 0; kk < Cfg::BK; kk += 16) {
-    bf16x8 af[Cfg::TM], bw[Cfg::TN];
+  for (int kk = 0; kk < C::BK; kk += 16) {
+    bf16x8 af[C::TM], bw[C::TN];
 #pragma unroll
-    for (int i = 0; i < Cfg::TM; ++i)
-      af[i] = *reinterpret_cast<const bf16x8 *>(&As[(wm * Cfg::WM + i * 32 + lrow) * LS + kk + lk]);
+    for (int i = 0; i < C::TM; ++i)
+      af[i] = *reinterpret_cast<const bf16x8 *>(&As[(wm * C::WM + i * 32 + lrow) * C::LS + kk + lk]);
 #pragma unroll
-    for (int j = 0; j < Cfg::TN; ++j)
-      bw[j] = *reinterpret_cast<const bf16x8 *>(&Bs[(wn * Cfg::WN + j * 32 + lrow) * LS + kk + lk]);
+    for (int j = 0; j < C::TN; ++j)
+      bw[j] = *reinterpret_cast<const bf16x8 *>(&Bs[(wn * C::WN + j * 32 + lrow) * C::LS + kk + lk]);
 #pragma unroll
-    for (int i = 0; i < Cfg::TM; ++i)
+    for (int j = 0; j < C::TN; ++j)
 #pragma unroll
-      for (int j = 0; j < Cfg::TN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bw[j], acc[i][j], 0, 0, 0);
+      for (int i = 0; i < C::TM; ++i)
+        acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bw[j], af[i], acc[j][i], 0, 0, 0);
   }
 }
 
-template <class Cfg, class Epi>
-__global__ __launch_bounds__(Cfg::NT) void gemm_bf16_kernel(const bf16 *__restrict__ A,
-                                                            const bf16 *__restrict__ W, int M,
-                                                            int N, int K, Epi epi) {
-  constexpr int BM = Cfg::BM, BN = Cfg::BN, BK = Cfg::BK, LS = Cfg::LDS_STRIDE;
-  __shared__ __attribute__((aligned(16))) bf16 As[2][BM * LS];
-  __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * LS];
-
-  const int tiles_m = (M + BM - 1) / BM, tiles_n = N / BN;
+template <class C, class Epi>
+__global__ __launch_bounds__(C::NT, C::MINB) void gemm_bf16_kernel(const bf16 *__restrict__ A,
+                                                                   const bf16 *__restrict__ W,
+                                                                   int M, int N, int K, Epi epi) {
+  __shared__ __attribute__((aligned(16))) bf16 As[2][C::BM * C::LS];
+  __shared__ __attribute__((aligned(16))) bf16 Bs[2][C::BN * C::LS];
+  const int tiles_m = (M + C::BM - 1) / C::BM, tiles_n = N / C::BN;
   int tm, tn;
   tile_coords(xcd_remap(blockIdx.x, gridDim.x), tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * BM, n0 = tn * BN;
+  const int m0 = tm * C::BM, n0 = tn * C::BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / Cfg::WGN, wn = wave % Cfg::WGN;
-
-  f32x16 acc[Cfg::TM][Cfg::TN];
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+  f32x16 acc[C::TN][C::TM];
 #pragma unroll
-  for (int i = 0; i < Cfg::TM; ++i)
+  for (int j = 0; j < C::TN; ++j)
 #pragma unroll
-    for (int j = 0; j < Cfg::TN; ++j) acc[i][j] = f32x16{};
+    for (int i = 0; i < C::TM; ++i) acc[j][i] = f32x16{};
 
-  // Software pipeline: the global loads of k-tile t+1 are issued before the
-  // MFMAs of k-tile t and land in the other LDS buffer after them.
-  const int nk = K / BK;
-  Stage<Cfg> st;
-  stage_load<Cfg>(st, A, W, M, K, m0, n0, 0, tid);
-  stage_store<Cfg>(st, As[0], Bs[0], tid);
-  __syncthreads();
-  for (int kt = 0; kt + 1 < nk; ++kt) {
-    const int cur = kt & 1;
-    stage_load<Cfg>(st, A, W, M, K, m0, n0, (kt + 1) * BK, tid);
-    tile_mfma<Cfg>(acc, As[cur], Bs[cur], wm, wn, lane);
-    stage_store<Cfg>(st, As[cur ^ 1], Bs[cur ^ 1], tid);
+  const int nk = K / C::BK;
+  if constexpr (C::PF == 1) {
+    // k-tile t+1 is loaded into registers while k-tile t is multiplied, then
+    // written to the other LDS buffer.
+    Stage<C> st;
+    stage_load<C>(st, A, W, M, K, m0, n0, 0, tid);
+    stage_store<C>(st, As[0], Bs[0], tid);
     __syncthreads();
-  }
-  tile_mfma<Cfg>(acc, As[(nk - 1) & 1], Bs[(nk - 1) & 1], wm, wn, lane);
-
-  // 32x32 accumulator layout: lane -> column (lane & 31); register r ->
-  // row (r / 4) * 8 + (lane / 32) * 4 + r % 4.
-#pragma unroll
-  for (int i = 0; i < Cfg::TM; ++i) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = m0 + wm * Cfg::WM + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-      if (row >= M) continue;
-#pragma unroll
-      for (int j = 0; j < Cfg::TN; ++j) {
-        const int col = n0 + wn * Cfg::WN + j * 32 + (lane & 31);
-        epi(row, col, acc[i][j][r]);
-      }
+    for (int kt = 0; kt + 1 < nk; ++kt) {
+      const int cur = kt & 1;
+      stage_load<C>(st, A, W, M, K, m0, n0, (kt + 1) * C::BK, tid);
+      tile_mfma<C>(acc, As[cur], Bs[cur], wm, wn, lane);
+      stage_store<C>(st, As[cur ^ 1], Bs[cur ^ 1], tid);
+      __syncthreads();
     }
+    tile_mfma<C>(acc, As[(nk - 1) & 1], Bs[(nk - 1) & 1], wm, wn, lane);
+  } else {
+    // Two register stages: k-tile t+2 is loaded while k-tile t is multiplied
+    // and k-tile t+1 (loaded one iteration earlier) goes to LDS after it, so
+    // every load has two iterations to land.
+    Stage<C> s0, s1;
+    stage_load<C>(s0, A, W, M, K, m0, n0, 0, tid);
+    if (nk > 1) stage_load<C>(s1, A, W, M, K, m0, n0, C::BK, tid);
+    stage_store<C>(s0, As[0], Bs[0], tid);
+    __syncthreads();
+    int kt = 0;
+    for (; kt + 2 < nk; kt += 2) {
+      stage_load<C>(s0, A, W, M, K, m0, n0, (kt + 2) * C::BK, tid);
+      tile_mfma<C>(acc, As[0], Bs[0], wm, wn, lane);
+      stage_store<C>(s1, As[1], Bs[1], tid);
+      __syncthreads();
+      if (kt + 3 < nk) stage_load<C>(s1, A, W, M, K, m0, n0, (kt + 3) * C::BK, tid);
+      tile_mfma<C>(acc, As[1], Bs[1], wm, wn, lane);
+      stage_store<C>(s0, As[0], Bs[0], tid);
+      __syncthreads();
+    }
+    if (kt + 1 < nk) {  // two k-tiles left: buffer 0 holds kt, s1 holds kt + 1
+      tile_mfma<C>(acc, As[0], Bs[0], wm, wn, lane);
+      stage_store<C>(s1, As[1], Bs[1], tid);
+      __syncthreads();
+      tile_mfma<C>(acc, As[1], Bs[1], wm, wn, lane);
+    } else {
+      tile_mfma<C>(acc, As[0], Bs[0], wm, wn, lane);
+    }
+  }
+
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i) {
+    const int row = m0 + wm * C::WM + i * 32 + (lane & 31);
+    if (row >= M) continue;
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int col0 = n0 + wn * C::WN + j * 32 + g * 8 + (lane >> 5) * 4;
+        const f32x4 v = {acc[j][i][4 * g + 0], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2],
+                         acc[j][i][4 * g + 3]};
+        epi(row, col0, v);
+      }
   }
 }
 
-// 128x128 tile, 2x2 wavefronts of 64x64: two workgroups per CU; used when
-// the 256x256 grid would leave CUs idle.
-using TileS = TileCfg<128, 128, 64, 2, 2>;
-// 256x256 tile, 2x2 wavefronts of 128x128 (accumulators in AGPRs): one
-// workgroup per CU, four times the MFMA work per k-tile and per LDS byte.
-using TileL = TileCfg<256, 256, 64, 2, 2>;
+// 128x128 tile, 2x2 wavefronts of 64x64, two register stages, registers
+// budgeted for two workgroups per CU.
+using TileS = TileCfg<128, 128, 64, 2, 2, 2, 2>;
+// 256x256 tile, 2x4 wavefronts of 128x64 (two per SIMD), one register stage:
+// for large-M projections to wide outputs (measured faster there).
+using TileL = TileCfg<256, 256, 64, 2, 4, 1, 1>;
 
 template <class C, class Epi>
 static hipError_t launch_tile(const void *a, const void *w, int m, int n, int k, const Epi &epi,
@@ -239,10 +292,9 @@ static hipError_t run_bf16(const void *a, const void *w, int m, int n, int k, co
                            hipStream_t s) {
   if (m == 0) return hipSuccess;
   if (n % TileS::BN != 0 || k % TileS::BK != 0) return hipErrorInvalidValue;
-  // 256 CUs: prefer the large tile when it still yields at least two
-  // workgroups per CU.
   const long large_tiles = (long)((m + TileL::BM - 1) / TileL::BM) * (n / TileL::BN);
-  if (n % TileL::BN == 0 && large_tiles >= 512) return launch_tile<TileL>(a, w, m, n, k, epi, s);
+  if (n % TileL::BN == 0 && n >= 3072 && large_tiles >= 512)
+    return launch_tile<TileL>(a, w, m, n, k, epi, s);
   return launch_tile<TileS>(a, w, m, n, k, epi, s);
 }
 
@@ -285,8 +337,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float *__restrict__
   for (int i = 0; i < 4; ++i) {
     const int row = m0 + ty * 4 + i;
     if (row >= M) continue;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) epi(row, n0 + tx * 4 + j, acc[i][j]);
+    const f32x4 v = {acc[i][0], acc[i][1], acc[i][2], acc[i][3]};
+    epi(row, n0 + tx * 4, v);
   }
 }
 
