@@ -287,14 +287,18 @@ static hipError_t launch_tile(const void *a, const void *w, int m, int n, int k,
   return hipGetLastError();
 }
 
+bool gemm_large_tile(DType dt, int32_t m, int32_t n) {
+  if (dt != DType::BF16) return false;
+  const long large_tiles = (long)((m + TileL::BM - 1) / TileL::BM) * (n / TileL::BN);
+  return n % TileL::BN == 0 && n >= 3072 && large_tiles >= 512;
+}
+
 template <class Epi>
 static hipError_t run_bf16(const void *a, const void *w, int m, int n, int k, const Epi &epi,
                            hipStream_t s) {
   if (m == 0) return hipSuccess;
   if (n % TileS::BN != 0 || k % TileS::BK != 0) return hipErrorInvalidValue;
-  const long large_tiles = (long)((m + TileL::BM - 1) / TileL::BM) * (n / TileL::BN);
-  if (n % TileL::BN == 0 && n >= 3072 && large_tiles >= 512)
-    return launch_tile<TileL>(a, w, m, n, k, epi, s);
+  if (gemm_large_tile(DType::BF16, m, n)) return launch_tile<TileL>(a, w, m, n, k, epi, s);
   return launch_tile<TileS>(a, w, m, n, k, epi, s);
 }
 
