@@ -77,7 +77,12 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
   for (int s = 0; s < QS; ++s)
     qf[s] = *reinterpret_cast<const bf16x8 *>(qrow + s * 16 + (lane >> 5) * 8);
 
-  u32x4 rk[LPT], rv[LPT];
+  // K tiles are staged as 16-byte chunks; V tiles as pairs of keys so that
+  // the transposed write to LDS packs two keys into one 32-bit word (keys 2p
+  // and 2p+1 are adjacent in the permuted layout).
+  constexpr int VPCH = TCH / 2;
+  constexpr int LPV = (VPCH + NT - 1) / NT;
+  u32x4 rk[LPT], rv0[LPV], rv1[LPV];
   auto gload = [&](int t0) {
 #pragma unroll
     for (int i = 0; i < LPT; ++i) {
@@ -85,7 +90,16 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
       if (c < TCH) {
         const int key = min(t0 + c / CPR, N - 1), d = (c % CPR) * 8;
         rk[i] = *reinterpret_cast<const u32x4 *>(kg + (size_t)key * DH + d);
-        rv[i] = *reinterpret_cast<const u32x4 *>(vg + (size_t)key * DH + d);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < LPV; ++i) {
+      const int c = i * NT + tid;
+      if (c < VPCH) {
+        const int kp = c / CPR, d = (c % CPR) * 8;
+        const int k0 = min(t0 + 2 * kp, N - 1), k1 = min(t0 + 2 * kp + 1, N - 1);
+        rv0[i] = *reinterpret_cast<const u32x4 *>(vg + (size_t)k0 * DH + d);
+        rv1[i] = *reinterpret_cast<const u32x4 *>(vg + (size_t)k1 * DH + d);
       }
     }
   };
@@ -96,10 +110,22 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
       if (c < TCH) {
         const int key = c / CPR, d = (c % CPR) * 8;
         *reinterpret_cast<u32x4 *>(&Ks[buf][key * KS + d]) = rk[i];
-        const bf16x8 v = __builtin_bit_cast(bf16x8, rv[i]);
-        const int pos = (key & ~15) | vperm16(key & 15);
+      }
+    }
 #pragma unroll
-        for (int e = 0; e < 8; ++e) Vt[buf][(d + e) * VS + pos] = v[e];
+    for (int i = 0; i < LPV; ++i) {
+      const int c = i * NT + tid;
+      if (c < VPCH) {
+        const int kp = c / CPR, d = (c % CPR) * 8;
+        const int pos = ((2 * kp) & ~15) | vperm16((2 * kp) & 15);
+        unsigned *vt = reinterpret_cast<unsigned *>(&Vt[buf][d * VS + pos]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const unsigned w0 = rv0[i][e >> 1], w1 = rv1[i][e >> 1];
+          const unsigned lo = (e & 1) ? (w0 >> 16) : (w0 & 0xFFFFu);
+          const unsigned hi = (e & 1) ? (w1 & 0xFFFF0000u) : (w1 << 16);
+          vt[e * (VS / 2)] = lo | hi;
+        }
       }
     }
   };
@@ -133,15 +159,25 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
       }
     }
     float mx = -INFINITY;
+    if (t0 + TK <= N) {  // every key of the tile exists
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = t0 + kb * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        const float v = key < N ? s[kb][r] * sl2 : -INFINITY;
-        s[kb][r] = v;
-        mx = fmaxf(mx, v);
-      }
+        for (int r = 0; r < 16; ++r) {
+          s[kb][r] *= sl2;
+          mx = fmaxf(mx, s[kb][r]);
+        }
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = t0 + kb * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+          const float v = key < N ? s[kb][r] * sl2 : -INFINITY;
+          s[kb][r] = v;
+          mx = fmaxf(mx, v);
+        }
+    }
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float m_new = fmaxf(m_run, mx);
     const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -303,6 +339,22 @@ __device__ __forceinline__ float block_reduce(float v, bool is_max, float *red) 
   return r;
 }
 
+// Eight consecutive elements as float (16- or 32-byte aligned source).
+__device__ __forceinline__ void load8(const bf16 *p, float (&out)[8]) {
+  const bf16x8 v = *reinterpret_cast<const bf16x8 *>(p);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) out[e] = (float)v[e];
+}
+__device__ __forceinline__ void load8(const float *p, float (&out)[8]) {
+  const f32x4 a = *reinterpret_cast<const f32x4 *>(p);
+  const f32x4 b = *reinterpret_cast<const f32x4 *>(p + 4);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    out[e] = a[e];
+    out[e + 4] = b[e];
+  }
+}
+
 template <typename T, int DH>
 __global__ __launch_bounds__(SC_THREADS) void attn_scores_kernel(AttnArgs a,
                                                                  const int32_t *__restrict__ n_gen,
@@ -340,12 +392,15 @@ __global__ __launch_bounds__(SC_THREADS) void attn_scores_kernel(AttnArgs a,
 #pragma unroll
       for (int qq = 0; qq < 8; ++qq) dot[qq] = 0.f;
       const T *kr = kg + (size_t)j * DH;
-#pragma unroll 4
-      for (int d = 0; d < DH; ++d) {
-        const float kv = to_f32(kr[d]);
+#pragma unroll 2
+      for (int d0 = 0; d0 < DH; d0 += 8) {
+        float kv[8];
+        load8(kr + d0, kv);
 #pragma unroll
-        for (int qq = 0; qq < 8; ++qq)
-          if (qq < nq) dot[qq] = fmaf(qs[qq * DH + d], kv, dot[qq]);
+        for (int e = 0; e < 8; ++e)
+#pragma unroll
+          for (int qq = 0; qq < 8; ++qq)
+            if (qq < nq) dot[qq] = fmaf(qs[qq * DH + d0 + e], kv[e], dot[qq]);
       }
 #pragma unroll
       for (int qq = 0; qq < 8; ++qq)

@@ -146,6 +146,9 @@ BF16_SHAPES = {
     "mar-l": dict(cid=3, n_tokens=320),
     "mar-h": dict(cid=4, n_tokens=320),
     "hires": dict(cid=5, n_tokens=1088),
+    # a key count that is not a multiple of the 64-key tile: masked tail
+    "ragged-keys": dict(cid=3, n_tokens=300),
+    "ragged-keys-dh80": dict(cid=4, n_tokens=203),
 }
 
 
@@ -162,7 +165,7 @@ def _ragged_case(cfg, B, sizes, gens, seed):
 @pytest.mark.parametrize("shape", list(BF16_SHAPES))
 def test_bf16_layer_ragged(shape):
     spec = BF16_SHAPES[shape]
-    cfg = workload.CONFIGS[spec["cid"]]
+    cfg = workload.CONFIGS[spec["cid"]].with_(n_tokens=spec["n_tokens"])
     N = cfg.n_tokens
     # ragged active sets: a single token, a typical cache-aware set, a set that
     # spans two query chunks, and every token (a full layer)
