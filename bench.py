@@ -168,6 +168,16 @@ def main() -> int:
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=20.0)
+    ap.add_argument("--strategy", default="marche",
+                    help="active-set construction: marche, low-attention, random, no-caching, "
+                         "no-generating")
+    ap.add_argument("--schedule-sweep", action="store_true",
+                    help="also time one generation per schedule variant: selection layer 1-4, "
+                         "full-refresh period 2-7 and off, fixed 64-token budget, and each "
+                         "active-set strategy (latency only)")
+    ap.add_argument("--ratio-sweep", action="store_true",
+                    help="also time one generation at each refresh ratio of the MAR-H sweep "
+                         "(0, 5, 10, 25, 100%%)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB five times (the "
                          "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -215,7 +225,7 @@ def main() -> int:
     log(f"[bench] workload {cfg.name}: generating weights")
     weights = workload.all_weights(cfg)
     log("[bench] uploading")
-    eng = driver.Engine(cfg, batch=B, weights=weights)
+    eng = driver.Engine(cfg, batch=B, weights=weights, strategy=args.strategy)
     torch.cuda.synchronize()
 
     log(f"[bench] warmup {args.warmup} steps")
@@ -244,7 +254,7 @@ def main() -> int:
                    "n_image_tokens": cfg.n_img, "n_layers": cfg.n_layers,
                    "d_model": cfg.d_model, "n_heads": cfg.n_heads, "head_dim": cfg.head_dim,
                    "refresh_ratio": cfg.ratio_bp / 10000, "sel_layer": cfg.sel_layer,
-                   "full_every": cfg.full_every, "decode_steps": T,
+                   "full_every": cfg.full_every, "decode_steps": T, "strategy": args.strategy,
                    "full_steps_in_schedule": sum(p.full for p in eng.plans)},
         "step_us": step_us,
     }
@@ -260,6 +270,43 @@ def main() -> int:
         out["full_recompute"] = {"images_per_s": fv, "step_us": statistics.median(fper)}
         out["speedup_vs_full_recompute"] = value / fv
         log(f"[bench] full recompute {fv:.2f} images/s -> speedup {value / fv:.3f}")
+        eng.set_schedule(cfg.full_every, "ratio", cfg.ratio_bp)
+
+    if args.schedule_sweep:
+        variants = [dict(sel_layer=s_) for s_ in (1, 2, 3, 4)]
+        variants += [dict(full_every=f_) for f_ in (2, 3, 4, 5, 6, 7, 0)]
+        variants += [dict(policy="fixed", budget=64)]
+        variants += [dict(strategy=st) for st in driver.STRATEGIES]
+        base = dict(sel_layer=cfg.sel_layer, full_every=cfg.full_every, policy="ratio",
+                    budget=cfg.ratio_bp, strategy=args.strategy)
+        rows = []
+        for v in variants:
+            conf = dict(base, **v)
+            eng.configure(**conf)
+            for i in range(T):
+                eng.step(i)
+            swall, sper, skinds = timed(eng, T, 0, T)
+            ca = [p for p, f in zip(sper, skinds) if not f]
+            rows.append({**v, "images_per_s": B / swall,
+                         "cache_aware_step_us": statistics.median(ca) if ca else None,
+                         "full_steps": sum(skinds)})
+            log(f"[bench] {v}: {B / swall:.2f} images/s")
+        out["schedule_sweep"] = rows
+        eng.configure(**base)
+
+    if args.ratio_sweep:
+        sweep = []
+        for bp in workload.MAR_H_RATIO_SWEEP_BP:
+            eng.set_schedule(cfg.full_every, "ratio", bp)
+            for i in range(T):
+                eng.step(i)
+            swall, sper, skinds = timed(eng, T, 0, T)
+            ca = [p for p, f in zip(sper, skinds) if not f]
+            sweep.append({"refresh_ratio": bp / 10000, "images_per_s": B / swall,
+                          "cache_aware_step_us": statistics.median(ca) if ca else None,
+                          "mean_active": statistics.mean(p.g + p.n + p.k for p in eng.plans if not p.full)})
+            log(f"[bench] ratio {bp / 100:.0f}%: {B / swall:.2f} images/s")
+        out["ratio_sweep"] = sweep
         eng.set_schedule(cfg.full_every, "ratio", cfg.ratio_bp)
 
     if not args.no_roofline:

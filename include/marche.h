@@ -155,6 +155,22 @@ marche_status_t select_refresh(const float *scores, int32_t n_parts, const int32
                                int32_t k, int32_t *out_idx, const int32_t *out_off,
                                marche_stream_t stream);
 
+/* Order of a refresh selection: the highest head-aggregated attention mass
+ * (Section 4.2, the method) or the lowest (the low-attention ablation of the
+ * refresh-strategy study, Table 3). */
+typedef enum { MARCHE_SELECT_HIGHEST = 0, MARCHE_SELECT_LOWEST = 1 } marche_select_order_t;
+
+/* select_refresh with an explicit order.  MARCHE_SELECT_LOWEST picks the k
+ * candidates with the lowest s_j, equal scores going to the lower token index
+ * and NaN ranking after every number; the output is ascending as for
+ * select_refresh, which equals this call with MARCHE_SELECT_HIGHEST.  Returns
+ * INVALID_ARG for any other order value. */
+marche_status_t select_refresh_ordered(const float *scores, int32_t n_parts,
+                                       const int32_t *excl_idx, const int32_t *excl_off,
+                                       int32_t batch, int32_t n_tokens, int32_t k,
+                                       int32_t *out_idx, const int32_t *out_off, int32_t order,
+                                       marche_stream_t stream);
+
 /* Decoder input of one step (stand-in for Eq. 2's concatenation of encoder
  * features and mask embeddings with positional encodings):
  *   x[b][j] = pos[j] + cls[b]                      for j <  n_buf,

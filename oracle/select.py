@@ -12,8 +12,12 @@ token order.  The ratio budget (a fraction of the candidates, in basis points,
 rounded half up) is the workload's alternative to the fixed budget; 100% makes
 every token active.
 
+The low-attention selection (lowest scores first) is the refresh-strategy
+ablation of Table 3.
+
 Pins (tests/test_oracle_select.py): brute-force rank definition and exhaustive
-subset enumeration on tiny inputs; the paper's 5 + 9 + 50 = 64 example.
+subset enumeration on tiny inputs (both orders); the paper's 5 + 9 + 50 = 64
+example.
 """
 from __future__ import annotations
 
@@ -27,32 +31,39 @@ def total_scores(scores_per_head: np.ndarray) -> np.ndarray:
     return np.asarray(scores_per_head, np.float64).sum(axis=0)
 
 
-def _rank_key(s: float) -> float:
-    return -np.inf if np.isnan(s) else float(s)
+def _rank_key(s: float, lowest: bool = False) -> float:
+    """Preference value: larger is preferred.  NaN is never preferred."""
+    if np.isnan(s):
+        return -np.inf
+    return -float(s) if lowest else float(s)
 
 
-def select_topk(scores: Sequence[float], excl: Iterable[int], k: int) -> List[int]:
-    """The k candidates with the highest score; ties to the lower index;
-    returned ascending.  Fewer than k candidates is an error."""
+def select_topk(scores: Sequence[float], excl: Iterable[int], k: int,
+                lowest: bool = False) -> List[int]:
+    """The k candidates with the highest score (or, with ``lowest``, the lowest:
+    the low-attention ablation of Table 3); ties to the lower index; returned
+    ascending.  Fewer than k candidates is an error."""
     excl = set(int(e) for e in excl)
     cand = [j for j in range(len(scores)) if j not in excl]
     if k > len(cand):
         raise ValueError("k exceeds the number of candidates")
-    ranked = sorted(cand, key=lambda j: (-_rank_key(scores[j]), j))
+    ranked = sorted(cand, key=lambda j: (-_rank_key(scores[j], lowest), j))
     return sorted(ranked[:k])
 
 
-def select_topk_bruteforce(scores: Sequence[float], excl: Iterable[int], k: int) -> List[int]:
+def select_topk_bruteforce(scores: Sequence[float], excl: Iterable[int], k: int,
+                           lowest: bool = False) -> List[int]:
     """Rank definition: candidate j is chosen iff fewer than k candidates beat
-    it, where l beats j when s_l > s_j, or s_l == s_j and l < j."""
+    it, where l beats j when l is preferred (higher score, or lower with
+    ``lowest``), or equally preferred and l < j."""
     excl = set(int(e) for e in excl)
     cand = [j for j in range(len(scores)) if j not in excl]
     out = []
     for j in cand:
-        sj = _rank_key(scores[j])
+        sj = _rank_key(scores[j], lowest)
         beaten_by = 0
         for l in cand:
-            sl = _rank_key(scores[l])
+            sl = _rank_key(scores[l], lowest)
             if sl > sj or (sl == sj and l < j):
                 beaten_by += 1
         if beaten_by < k:

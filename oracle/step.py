@@ -63,6 +63,7 @@ class StepResult:
     full: bool
     scores: Optional[np.ndarray] = None          # [H][N] at the selection layer
     layers: List[block.LayerResult] = field(default_factory=list)
+    include_gen: bool = True                     # G part of the cache-aware active set
 
     @property
     def z(self) -> np.ndarray:
@@ -72,7 +73,8 @@ class StepResult:
     def active(self) -> Optional[List[int]]:
         if self.refresh is None:
             return None
-        return list(self.gen) + list(self.cache_tokens) + list(self.refresh)
+        g = list(self.gen) if self.include_gen else []
+        return g + list(self.cache_tokens) + list(self.refresh)
 
 
 def marche_step(params: Sequence[Dict[str, np.ndarray]], x_in: np.ndarray,
@@ -81,13 +83,21 @@ def marche_step(params: Sequence[Dict[str, np.ndarray]], x_in: np.ndarray,
                 eps: float, sel_layer: int, full: bool, k_refresh: int,
                 keep_layers: bool = False,
                 refresh_override: Optional[Callable[[np.ndarray, List[int]], List[int]]] = None,
-                layer_range: Optional[range] = None) -> StepResult:
+                layer_range: Optional[range] = None, select_lowest: bool = False,
+                include_gen: bool = True) -> StepResult:
     """One decoding step of one image.
 
     ``sel_layer`` is 1-based; layers 1..sel_layer run with full attention in
-    every step.  ``refresh_override`` (used by parity tests) receives the
-    selection-layer scores and the oracle's own refresh set and returns the set
-    to continue with.  ``layer_range`` restricts the layers run (0-based).
+    every step.  ``refresh_override`` (used by parity tests and by the random
+    refresh ablation) receives the selection-layer scores and the oracle's own
+    refresh set and returns the set to continue with.  ``layer_range``
+    restricts the layers run (0-based).
+
+    Ablations of the active-set construction (Tables 2-3): ``select_lowest``
+    refreshes the tokens with the lowest attention mass; passing no caching
+    tokens gives A = G u R; ``include_gen=False`` leaves the generating tokens
+    out of the active set (A = N u R; they are still excluded from R and still
+    provide the scores).
     """
     L = len(params)
     x = np.asarray(x_in, F64)
@@ -110,19 +120,20 @@ def marche_step(params: Sequence[Dict[str, np.ndarray]], x_in: np.ndarray,
             if want_score:
                 scores = res.scores
                 refresh = select.select_topk(select.total_scores(scores), gen + cache_tokens,
-                                             k_refresh)
+                                             k_refresh, lowest=select_lowest)
                 if refresh_override is not None:
                     refresh = list(refresh_override(scores, refresh))
-                active = gen + cache_tokens + refresh
+                active = (gen if include_gen else []) + cache_tokens + refresh
         else:
             if active is None:
                 raise ValueError("cache-aware layer reached before the selection layer")
-            res = block.cache_aware_layer(params[l], x, kcs[l], vcs[l], active, gen, n_heads, eps)
+            res = block.cache_aware_layer(params[l], x, kcs[l], vcs[l], active,
+                                          gen if include_gen else [], n_heads, eps)
         x = res.x_out
         kcs[l], vcs[l] = res.k_cache, res.v_cache
         if keep_layers:
             layers.append(res)
-    return StepResult(x, kcs, vcs, gen, cache_tokens, refresh, full, scores, layers)
+    return StepResult(x, kcs, vcs, gen, cache_tokens, refresh, full, scores, layers, include_gen)
 
 
 def refresh_count(policy: str, value: int, n_tokens: int, n_gen: int, n_cache: int) -> int:

@@ -18,8 +18,11 @@ LIB_PATH = os.path.join(_HERE, "libmarche.so")
 MARCHE_OK, MARCHE_ERR_INVALID_ARG, MARCHE_ERR_UNSUPPORTED, MARCHE_ERR_HIP, MARCHE_ERR_WORKSPACE = range(5)
 MARCHE_F32, MARCHE_BF16 = 0, 1
 
+MARCHE_SELECT_HIGHEST, MARCHE_SELECT_LOWEST = 0, 1
+
 EXPORTED = (
     "kv_cache_init", "marche_step_workspace_bytes", "marche_step", "select_refresh",
+    "select_refresh_ordered",
     "marche_decoder_input", "marche_status_string", "marche_last_error",
     "marche_profile_enable", "marche_profile_collect", "marche_profile_entry",
     "marche_profile_reset",
@@ -65,6 +68,7 @@ def lib() -> C.CDLL:
         L.marche_step.argtypes = [C.POINTER(Model), C.POINTER(Layer), C.POINTER(KVCache), i32, i32,
                                   i32, vp, vp, vp, vp, i32, i32, i32, vp, i32, vp, sz, vp]
         L.select_refresh.argtypes = [vp, i32, vp, vp, i32, i32, i32, vp, vp, vp]
+        L.select_refresh_ordered.argtypes = [vp, i32, vp, vp, i32, i32, i32, vp, vp, i32, vp]
         L.marche_decoder_input.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, vp]
         L.marche_status_string.argtypes = [C.c_int]
         L.marche_status_string.restype = C.c_char_p
@@ -78,7 +82,8 @@ def lib() -> C.CDLL:
                                            C.POINTER(C.c_double)]
         L.marche_profile_reset.argtypes = []
         L.marche_profile_reset.restype = None
-        for name in ("kv_cache_init", "marche_step", "select_refresh", "marche_decoder_input",
+        for name in ("kv_cache_init", "marche_step", "select_refresh", "select_refresh_ordered",
+                     "marche_decoder_input",
                      "marche_profile_enable", "marche_profile_entry"):
             getattr(L, name).restype = C.c_int
         _lib = L
@@ -150,9 +155,11 @@ def marche_step(model: Model, layers, cache: KVCache, layer_begin: int, layer_en
 
 
 def select_refresh(scores, n_parts: int, excl_idx, excl_off, batch: int, n_tokens: int, k: int,
-                   out_idx, out_off, stream=None) -> None:
-    _check(lib().select_refresh(_ptr(scores), n_parts, _ptr(excl_idx), _ptr(excl_off), batch,
-                                n_tokens, k, _ptr(out_idx), _ptr(out_off), _stream(stream)))
+                   out_idx, out_off, stream=None, lowest: bool = False) -> None:
+    order = MARCHE_SELECT_LOWEST if lowest else MARCHE_SELECT_HIGHEST
+    _check(lib().select_refresh_ordered(_ptr(scores), n_parts, _ptr(excl_idx), _ptr(excl_off),
+                                        batch, n_tokens, k, _ptr(out_idx), _ptr(out_off), order,
+                                        _stream(stream)))
 
 
 def decoder_input(x, cls, value, mask, pos, rank, batch: int, n_tokens: int, n_buf: int,

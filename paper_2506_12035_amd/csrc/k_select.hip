@@ -4,7 +4,8 @@
 //     (order-preserving bits of s_j) << 32  |  (0xFFFFFFFF - j)
 // so that sorting keys in descending order ranks higher scores first and,
 // among equal scores, lower token indices first; NaN is mapped to -inf and
-// -0.0 to +0.0 before encoding.  Excluded tokens (generating and caching
+// -0.0 to +0.0 before encoding.  For the lowest-first order the score bits are
+// inverted (and NaN mapped to +inf).  Excluded tokens (generating and caching
 // tokens) get key 0, below every candidate.  A bitonic sort in LDS orders the
 // keys; the first k are flagged and written out in ascending token order with
 // a block-wide prefix count.  Everything is deterministic.
@@ -15,17 +16,22 @@ namespace marche {
 constexpr int SEL_THREADS = 256;
 constexpr int SEL_MAX_N = 4096;
 
-__device__ __forceinline__ uint32_t order_bits(float f) {
-  if (f != f) f = -INFINITY;  // NaN ranks below every number
-  if (f == 0.0f) f = 0.0f;    // -0.0 ties with +0.0
+// Order-preserving unsigned image of a float: larger float, larger key.
+// NaN is placed after every number in the chosen order; -0.0 ties with +0.0.
+__device__ __forceinline__ uint32_t order_bits(float f, bool lowest) {
+  if (f != f) f = lowest ? INFINITY : -INFINITY;
+  if (f == 0.0f) f = 0.0f;
   const uint32_t u = __float_as_uint(f);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  const uint32_t up = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  // lowest first: invert so that the smallest score gets the largest key;
+  // (~up) is never 0 for a non-NaN float, so candidates stay above key 0
+  return lowest ? ~up : up;
 }
 
 __global__ __launch_bounds__(SEL_THREADS) void select_topk_kernel(
     const float *__restrict__ scores, int n_parts, const int32_t *__restrict__ excl_idx,
     const int32_t *__restrict__ excl_off, int n_tokens, int np2, int k,
-    int32_t *__restrict__ out_idx, const int32_t *__restrict__ out_off) {
+    int32_t *__restrict__ out_idx, const int32_t *__restrict__ out_off, bool lowest) {
   extern __shared__ unsigned long long keys[];  // [np2], then int flags[n_tokens]
   int *flags = reinterpret_cast<int *>(keys + np2);
   __shared__ int part[SEL_THREADS];
@@ -37,7 +43,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_topk_kernel(
     if (j < n_tokens) {
       float s = 0.f;
       for (int p = 0; p < n_parts; ++p) s += sb[(size_t)p * n_tokens + j];
-      key = ((unsigned long long)order_bits(s) << 32) | (0xFFFFFFFFu - (uint32_t)j);
+      key = ((unsigned long long)order_bits(s, lowest) << 32) | (0xFFFFFFFFu - (uint32_t)j);
       flags[j] = 0;
     }
     keys[j] = key;
@@ -100,7 +106,8 @@ __global__ __launch_bounds__(SEL_THREADS) void select_topk_kernel(
 
 hipError_t launch_select_topk(const float *scores, int32_t n_parts, const int32_t *excl_idx,
                               const int32_t *excl_off, int32_t batch, int32_t n_tokens, int32_t k,
-                              int32_t *out_idx, const int32_t *out_off, hipStream_t s) {
+                              int32_t *out_idx, const int32_t *out_off, bool lowest,
+                              hipStream_t s) {
   if (batch == 0 || k == 0) return hipSuccess;
   if (n_tokens > SEL_MAX_N) return hipErrorInvalidValue;
   int np2 = 1;
@@ -108,7 +115,7 @@ hipError_t launch_select_topk(const float *scores, int32_t n_parts, const int32_
   if (np2 < 2) np2 = 2;
   const size_t lds = (size_t)np2 * sizeof(unsigned long long) + (size_t)n_tokens * sizeof(int);
   select_topk_kernel<<<batch, SEL_THREADS, lds, s>>>(scores, n_parts, excl_idx, excl_off, n_tokens,
-                                                     np2, k, out_idx, out_off);
+                                                     np2, k, out_idx, out_off, lowest);
   return hipGetLastError();
 }
 

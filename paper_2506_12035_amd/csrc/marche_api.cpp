@@ -312,6 +312,17 @@ marche_status_t select_refresh(const float *scores, int32_t n_parts, const int32
                                const int32_t *excl_off, int32_t batch, int32_t n_tokens,
                                int32_t k, int32_t *out_idx, const int32_t *out_off,
                                marche_stream_t stream_) {
+  return select_refresh_ordered(scores, n_parts, excl_idx, excl_off, batch, n_tokens, k, out_idx,
+                                out_off, MARCHE_SELECT_HIGHEST, stream_);
+}
+
+marche_status_t select_refresh_ordered(const float *scores, int32_t n_parts,
+                                       const int32_t *excl_idx, const int32_t *excl_off,
+                                       int32_t batch, int32_t n_tokens, int32_t k,
+                                       int32_t *out_idx, const int32_t *out_off, int32_t order,
+                                       marche_stream_t stream_) {
+  if (order != MARCHE_SELECT_HIGHEST && order != MARCHE_SELECT_LOWEST)
+    return fail(MARCHE_ERR_INVALID_ARG, "order=%d is not HIGHEST or LOWEST", order);
   if (batch < 0) return fail(MARCHE_ERR_INVALID_ARG, "batch=%d < 0", batch);
   if (n_tokens < 1 || n_tokens > 4096)
     return fail(MARCHE_ERR_INVALID_ARG, "n_tokens=%d outside [1, 4096]", n_tokens);
@@ -325,7 +336,7 @@ marche_status_t select_refresh(const float *scores, int32_t n_parts, const int32
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   LAUNCH(K_SELECT, 0, 4.0 * batch * n_parts * n_tokens,
          launch_select_topk(scores, n_parts, excl_idx, excl_off, batch, n_tokens, k, out_idx,
-                            out_off, stream));
+                            out_off, order == MARCHE_SELECT_LOWEST, stream));
   return MARCHE_OK;
 }
 
@@ -344,7 +355,11 @@ marche_status_t marche_decoder_input(float *x, const float *cls, const float *va
   if (!x || !cls || !mask || !pos || (n_tokens > n_buf && (!value || !rank)))
     return fail(MARCHE_ERR_INVALID_ARG, "NULL input to marche_decoder_input");
   hipStream_t stream = static_cast<hipStream_t>(stream_);
-  LAUNCH(K_DECODER_INPUT, 0, 12.0 * batch * n_tokens * d_model,
+  // Algorithmic traffic: x written once; per-image rows read once (value rows
+  // of the tokens generated so far, the class row); the positional rows and the
+  // mask row are shared by every image.
+  LAUNCH(K_DECODER_INPUT, 0,
+         4.0 * d_model * ((double)batch * n_tokens + (double)batch * n_known + batch + n_tokens + 1),
          launch_decoder_input(x, cls, value, mask, pos, rank, batch, n_tokens, n_buf, d_model,
                               n_known, stream));
   return MARCHE_OK;

@@ -77,8 +77,10 @@ hipError_t launch_attn_scores(DType dt, const AttnArgs &a, const int32_t *n_gen,
                               float *scores, hipStream_t s);
 
 // ---- selection (k_select.hip) ----
+// lowest = false: highest scores first; true: lowest scores first.
 hipError_t launch_select_topk(const float *scores, int32_t n_parts, const int32_t *excl_idx,
                               const int32_t *excl_off, int32_t batch, int32_t n_tokens, int32_t k,
-                              int32_t *out_idx, const int32_t *out_off, hipStream_t s);
+                              int32_t *out_idx, const int32_t *out_off, bool lowest,
+                              hipStream_t s);
 
 }  // namespace marche

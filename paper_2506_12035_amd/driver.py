@@ -30,6 +30,15 @@ def _dev_i32(a: np.ndarray, device) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(device)
 
 
+# Active-set constructions (the method and the ablations of Tables 2-3):
+#   marche         A = G u N u R, R = highest attention mass (Section 4.2)
+#   low-attention  A = G u N u R, R = lowest attention mass
+#   random         A = G u N u R, R drawn at random (seeded) from the candidates
+#   no-caching     A = G u R (caching tokens not forced in; they may be refreshed)
+#   no-generating  A = N u R (generating tokens left out of the later layers)
+STRATEGIES = ("marche", "low-attention", "random", "no-caching", "no-generating")
+
+
 @dataclass
 class StepPlan:
     t: int
@@ -41,11 +50,16 @@ class StepPlan:
     full_idx: torch.Tensor
     full_off: torch.Tensor
     n_gen: torch.Tensor
+    a: int = 0                                # cache-aware active rows per image
     ca_idx: Optional[torch.Tensor] = None
     ca_off: Optional[torch.Tensor] = None
+    ca_gen: Optional[torch.Tensor] = None     # generating rows leading the cache-aware list
+    ca_gen_max: int = 0
     excl_idx: Optional[torch.Tensor] = None
     excl_off: Optional[torch.Tensor] = None
     out_off: Optional[torch.Tensor] = None
+    device_select: bool = True                # R chosen on the device from the scores
+    select_lowest: bool = False
 
 
 class Engine:
@@ -55,12 +69,16 @@ class Engine:
                  n_layers: Optional[int] = None, ratio_bp: Optional[int] = None,
                  policy: str = "ratio", budget: Optional[int] = None,
                  full_every: Optional[int] = None, sel_layer: Optional[int] = None,
-                 weights: Optional[Sequence[Dict[str, np.ndarray]]] = None):
+                 weights: Optional[Sequence[Dict[str, np.ndarray]]] = None,
+                 strategy: str = "marche"):
         if n_layers is not None:
             cfg = cfg.with_(n_layers=n_layers)
         self.cfg = cfg
         self.device = torch.device(device)
         self.B = cfg.batch if batch is None else batch
+        if strategy not in STRATEGIES:
+            raise ValueError(f"strategy must be one of {STRATEGIES}")
+        self.strategy = strategy
         self.policy = policy
         if budget is None:
             if policy != "ratio":
@@ -104,6 +122,23 @@ class Engine:
         self.rank = _dev_i32(rank, self.device)
         self.set_schedule(self.full_every, self.policy, self.budget)
 
+    def configure(self, sel_layer: Optional[int] = None, full_every: Optional[int] = None,
+                  policy: Optional[str] = None, budget: Optional[int] = None,
+                  strategy: Optional[str] = None) -> None:
+        """Switch the decoding schedule (selection layer, refresh period, budget
+        policy, active-set strategy) and rebuild the resident index lists."""
+        if sel_layer is not None:
+            if not 1 <= sel_layer <= self.cfg.n_layers:
+                raise ValueError("sel_layer must lie in [1, n_layers]")
+            self.sel = sel_layer
+        if strategy is not None:
+            if strategy not in STRATEGIES:
+                raise ValueError(f"strategy must be one of {STRATEGIES}")
+            self.strategy = strategy
+        self.set_schedule(self.full_every if full_every is None else full_every,
+                          self.policy if policy is None else policy,
+                          self.budget if budget is None else budget)
+
     def set_schedule(self, full_every: int, policy: str, budget: int) -> None:
         """(Re)build the resident index lists of every step for a schedule:
         ``full_every`` = 1 with any budget is full recomputation."""
@@ -130,22 +165,36 @@ class Engine:
         si = schedule.step_indices(self.orders, c.n_buf, c.n_tokens, c.n_steps, t, self.full_every,
                                    self.policy, self.budget)
         B, N = self.B, c.n_tokens
-        g, n, k = si.gen.shape[1], si.cache.shape[1], si.k
-        plan = StepPlan(t, si.full, si.n_known, g, n, k,
+        g, n = si.gen.shape[1], si.cache.shape[1]
+        plan = StepPlan(t, si.full, si.n_known, g, n, si.k,
                         _dev_i32(si.full_order.reshape(-1), self.device),
                         _dev_i32(np.arange(B + 1) * N, self.device),
                         _dev_i32(np.full(B, g), self.device))
-        if not si.full:
-            a = g + n + k
-            ca = np.full((B, a), -1, np.int32)
-            ca[:, :g] = si.gen
-            ca[:, g:g + n] = si.cache
-            excl = np.concatenate([si.gen, si.cache], axis=1)
-            plan.ca_idx = _dev_i32(ca.reshape(-1), self.device)
-            plan.ca_off = _dev_i32(np.arange(B + 1) * a, self.device)
-            plan.excl_idx = _dev_i32(excl.reshape(-1), self.device)
-            plan.excl_off = _dev_i32(np.arange(B + 1) * (g + n), self.device)
-            plan.out_off = _dev_i32(np.arange(B) * a + g + n, self.device)
+        if si.full:
+            return plan
+        st = self.strategy
+        forced_cache = si.cache if st != "no-caching" else si.cache[:, :0]
+        if st == "no-caching":
+            plan.k = schedule.refresh_count(self.policy, self.budget, N, g, 0)
+        excl = np.concatenate([si.gen, forced_cache], axis=1)       # never refreshed
+        lead = forced_cache if st == "no-generating" else excl     # fixed head of A
+        a = lead.shape[1] + plan.k
+        ca = np.full((B, a), -1, np.int32)
+        ca[:, :lead.shape[1]] = lead
+        if st == "random":
+            cand = np.stack([np.setdiff1d(np.arange(N), excl[b]) for b in range(B)])
+            ca[:, lead.shape[1]:] = workload.random_refresh(c, t, cand, plan.k)
+            plan.device_select = False
+        plan.select_lowest = st == "low-attention"
+        plan.a = a
+        plan.ca_idx = _dev_i32(ca.reshape(-1), self.device)
+        plan.ca_off = _dev_i32(np.arange(B + 1) * a, self.device)
+        ca_g = 0 if st == "no-generating" else g
+        plan.ca_gen = _dev_i32(np.full(B, ca_g), self.device)
+        plan.ca_gen_max = ca_g
+        plan.excl_idx = _dev_i32(excl.reshape(-1), self.device)
+        plan.excl_off = _dev_i32(np.arange(B + 1) * excl.shape[1], self.device)
+        plan.out_off = _dev_i32(np.arange(B) * a + lead.shape[1], self.device)
         return plan
 
     # ------------------------------------------------------------------ step
@@ -164,8 +213,11 @@ class Engine:
                             self.workspace, self.ws_bytes, stream=self.stream)
 
     def select(self, p: StepPlan) -> None:
+        if not p.device_select:
+            return
         binding.select_refresh(self.scores, self.cfg.n_heads, p.excl_idx, p.excl_off, self.B,
-                               self.cfg.n_tokens, p.k, p.ca_idx, p.out_off, stream=self.stream)
+                               self.cfg.n_tokens, p.k, p.ca_idx, p.out_off, stream=self.stream,
+                               lowest=p.select_lowest)
 
     def step(self, t: int, build_input: bool = True) -> None:
         """One decoding step (all layers) of the whole batch, enqueued on the
@@ -179,10 +231,10 @@ class Engine:
             self.run_layers(0, L, p.full_idx, p.full_off, B * N, N, p.g, p.n_gen)
             return
         self.run_layers(0, self.sel, p.full_idx, p.full_off, B * N, N, p.g, p.n_gen,
-                        score_layer=self.sel - 1)
+                        score_layer=self.sel - 1 if p.device_select else -1)
         self.select(p)
-        a = p.g + p.n + p.k
-        self.run_layers(self.sel, L, p.ca_idx, p.ca_off, B * a, a, p.g, p.n_gen)
+        if p.a > 0:
+            self.run_layers(self.sel, L, p.ca_idx, p.ca_off, B * p.a, p.a, p.ca_gen_max, p.ca_gen)
 
     def generate(self, steps: Optional[Sequence[int]] = None) -> None:
         for t in (range(self.cfg.n_steps) if steps is None else steps):
@@ -199,8 +251,16 @@ class Engine:
         return self.v_cache.view(c.n_layers, self.B, c.n_heads, c.n_tokens, c.head_dim)[l]
 
     def active_lists(self, t: int) -> Optional[np.ndarray]:
-        """[B][|A|] cache-aware active list of step t as last computed (G | N | R)."""
+        """[B][|A|] cache-aware active list of step t as last computed."""
         p = self.plans[t]
         if p.full:
             return None
         return p.ca_idx.view(self.B, -1).cpu().numpy()
+
+    def refresh_lists(self, t: int) -> Optional[np.ndarray]:
+        """[B][k] refresh set of step t as last computed (ascending)."""
+        p = self.plans[t]
+        if p.full:
+            return None
+        lead = p.a - p.k
+        return p.ca_idx.view(self.B, p.a)[:, lead:].cpu().numpy()

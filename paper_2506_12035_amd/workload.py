@@ -238,3 +238,15 @@ def planted_rows(cfg: Config, candidates: np.ndarray, k: int, batch: Optional[in
         c = candidates[b] if candidates.ndim == 2 else candidates
         out[b] = np.sort(rng.choice(c, size=k, replace=False))
     return out
+
+
+def random_refresh(cfg: Config, t: int, candidates: np.ndarray, k: int) -> np.ndarray:
+    """Seeded random refresh set of step ``t`` for the random-refresh ablation:
+    ``candidates`` is [B][n_cand] per image; returns [B][k] (ascending), drawn
+    without replacement from each image's candidates."""
+    ss = np.random.SeedSequence([cfg.seed_value, STREAM_PLANTED, 1 + t])
+    rng = np.random.Generator(np.random.PCG64(ss))
+    out = np.empty((candidates.shape[0], k), dtype=np.int32)
+    for b in range(candidates.shape[0]):
+        out[b] = np.sort(rng.choice(candidates[b], size=k, replace=False))
+    return out

@@ -125,6 +125,9 @@ def test_select_refresh_validation():
     assert L.select_refresh(FAKE, 16, FAKE, FAKE, 2, 5000, 3, FAKE, FAKE, None) == binding.MARCHE_ERR_INVALID_ARG
     assert L.select_refresh(None, 16, FAKE, FAKE, 2, 320, 3, FAKE, FAKE, None) == binding.MARCHE_ERR_INVALID_ARG
     assert L.select_refresh(FAKE, 16, FAKE, FAKE, 2, 320, 0, FAKE, FAKE, None) == binding.MARCHE_OK
+    assert L.select_refresh_ordered(FAKE, 16, FAKE, FAKE, 2, 320, 3, FAKE, FAKE, 2, None) == binding.MARCHE_ERR_INVALID_ARG
+    assert "order" in binding.last_error()
+    assert L.select_refresh_ordered(FAKE, 16, FAKE, FAKE, 2, 320, 0, FAKE, FAKE, 1, None) == binding.MARCHE_OK
 
 
 def test_kv_cache_init_and_decoder_input_validation():

@@ -59,7 +59,7 @@ def _check_layer(cfg, x, kc, vc, active, n_gen, gpu, ref, tol):
     return worst
 
 
-def _select_gpu(scores, excl_lists, k):
+def _select_gpu(scores, excl_lists, k, lowest=False):
     B, H, N = scores.shape
     excl = np.concatenate([np.asarray(e, np.int32) for e in excl_lists])
     eoff = np.zeros(B + 1, np.int32)
@@ -69,7 +69,7 @@ def _select_gpu(scores, excl_lists, k):
     s_dev = torch.from_numpy(np.ascontiguousarray(scores, np.float32)).to(DEV)
     say(f"  select_refresh: B={B} parts={H} N={N} k={k}")
     binding.select_refresh(s_dev, H, torch.from_numpy(excl).to(DEV), torch.from_numpy(eoff).to(DEV),
-                           B, N, k, out, ooff)
+                           B, N, k, out, ooff, lowest=lowest)
     torch.cuda.synchronize()
     return out.cpu().numpy().reshape(B, k)
 
@@ -221,3 +221,18 @@ def test_select_refresh_edge_cases():
     # fewer candidates than k: trailing slots are -1
     sel2 = _select_gpu(s[:1], [list(range(33))], 6)
     assert list(sel2[0]) == [33, 34, 35, 36, -1, -1]
+
+
+def test_select_refresh_lowest_first():
+    # low-attention ablation: identical fp32 scores give the oracle's set exactly
+    rng = np.random.default_rng(9)
+    N, H, B = 1088, 16, 5
+    s = rng.random((B, H, N)).astype(np.float32)
+    s[1] = 0.5                       # all equal: lowest candidate indices
+    s[2, :, 11] = np.nan             # NaN is never preferred
+    excl = [rng.choice(N, 40, replace=False) for _ in range(B)]
+    k = 31
+    sel = _select_gpu(s, excl, k, lowest=True)
+    for b in range(B):
+        assert list(sel[b]) == select.select_topk(_fp32_head_sum(s[b]), excl[b], k, lowest=True)
+    assert 11 not in sel[2]

@@ -34,6 +34,19 @@ CASES = {
     "mar-l": dict(cid=3, images=(0, 127), windows=((0, 1, 2), (60, 61, 62))),
     "mar-h": dict(cid=4, images=(255,), windows=((0, 1, 2),)),
     "hires": dict(cid=5, images=(31,), windows=((0, 1, 2),)),
+    # ends of the MAR-H refresh-ratio sweep: no refreshing tokens (A = G u N)
+    # and every token active (the cache-aware layers recompute everything)
+    "mar-h-ratio0": dict(cid=4, images=(0,), windows=((30, 31, 32),), ratio_bp=0),
+    "mar-h-ratio100": dict(cid=4, images=(7,), windows=((0, 1, 2),), ratio_bp=10000),
+    # active-set ablations (Tables 2-3) as driver switches, on the MAR-B stack
+    "mar-b-low-attention": dict(cid=2, images=(5,), windows=((30, 31, 32),), strategy="low-attention"),
+    "mar-b-random": dict(cid=2, images=(6,), windows=((30, 31, 32),), strategy="random"),
+    "mar-b-no-caching": dict(cid=2, images=(7,), windows=((30, 31, 32),), strategy="no-caching"),
+    "mar-b-no-generating": dict(cid=2, images=(8,), windows=((30, 31, 32),), strategy="no-generating"),
+    # selection layer 1 and 4, refresh period 5, fixed active budget of 64 (Section 4.3)
+    "mar-b-sel1-period5": dict(cid=2, images=(9,), windows=((0, 1, 2),), sel_layer=1, full_every=5),
+    "mar-b-sel4-fixed64": dict(cid=2, images=(10,), windows=((0, 1, 2),), sel_layer=4, policy="fixed",
+                               budget=64),
 }
 
 
@@ -44,21 +57,23 @@ def _gpu_step_layerwise(eng, t, images):
     img = list(images)
     eng.decoder_input(t)
     rec = {"x_in": eng.x[img].cpu().numpy(), "layers": [], "R": None, "scores": None}
-    a = p.g + p.n + p.k
+    a = p.a
     for l in range(L):
         full_layer = p.full or l < sel
         k_before = eng.k_layer(l)[img].clone()
         v_before = eng.v_layer(l)[img].clone()
         if full_layer:
-            score_layer = sel - 1 if (not p.full and l == sel - 1) else -1
+            sel_here = not p.full and l == sel - 1
+            score_layer = l if (sel_here and p.device_select) else -1
             eng.run_layers(l, l + 1, p.full_idx, p.full_off, B * N, N, p.g, p.n_gen, score_layer)
-            if score_layer >= 0:
+            if sel_here:
                 eng.select(p)
-                rec["scores"] = eng.scores[img].cpu().numpy()
-                rec["R"] = p.ca_idx.view(B, a)[img, p.g + p.n:].cpu().numpy()
+                if p.device_select:
+                    rec["scores"] = eng.scores[img].cpu().numpy()
+                rec["R"] = p.ca_idx.view(B, a)[img, a - p.k:].cpu().numpy()
             act = None
         else:
-            eng.run_layers(l, l + 1, p.ca_idx, p.ca_off, B * a, a, p.g, p.n_gen)
+            eng.run_layers(l, l + 1, p.ca_idx, p.ca_off, B * a, a, p.ca_gen_max, p.ca_gen)
             act = p.ca_idx.view(B, a)[img].cpu().numpy()
         torch.cuda.synchronize()
         kk = eng.k_layer(l)[img]
@@ -73,21 +88,30 @@ def _gpu_step_layerwise(eng, t, images):
     return rec
 
 
-def _validated_override(gpu_R, tol, note):
+def _validated_override(gpu_R, tol, note, lowest=False):
+    """Gap rule for the GPU refresh set (highest or lowest attention mass)."""
     def override(scores, ref_R):
         s = scores.sum(axis=0)
         excl = override.excl
         k = len(ref_R)
         got = sorted(int(v) for v in gpu_R)
         cand = np.setdiff1d(np.arange(len(s)), excl)
-        ordered = np.sort(s[cand])[::-1]
-        gap = (ordered[k - 1] - ordered[k]) / ordered[k - 1] if 0 < k < len(ordered) else np.inf
+        ordered = np.sort(s[cand])
+        if not lowest:
+            ordered = ordered[::-1]
+        if 0 < k < len(ordered):
+            gap = abs(ordered[k - 1] - ordered[k]) / max(abs(ordered[k - 1]), abs(ordered[k]))
+        else:
+            gap = np.inf
         assert len(set(got)) == k and not set(got) & set(excl), "GPU refresh set invalid"
         if gap > tol:
             assert got == list(ref_R), f"refresh set differs with gap {gap:.2e}"
             note["exact"] += 1
         else:
-            assert all(s[j] >= ordered[k - 1] * (1 - tol) for j in got), "GPU refresh set outside tolerance"
+            if lowest:
+                assert all(s[j] <= ordered[k - 1] * (1 + tol) for j in got), "GPU refresh set outside tolerance"
+            else:
+                assert all(s[j] >= ordered[k - 1] * (1 - tol) for j in got), "GPU refresh set outside tolerance"
             note["ambiguous"] += 1
             note["agree"] += len(set(got) & set(ref_R)) / max(k, 1)
         return got
@@ -99,10 +123,16 @@ def _validated_override(gpu_R, tol, note):
 def test_stack_parity(case):
     spec = CASES[case]
     cfg = workload.CONFIGS[spec["cid"]]
+    for key in ("ratio_bp", "sel_layer", "full_every"):
+        if key in spec:
+            cfg = cfg.with_(**{key: spec[key]})
+    strategy = spec.get("strategy", "marche")
+    policy = spec.get("policy", "ratio")
+    budget = spec.get("budget", cfg.ratio_bp)
     tol = TOL[cfg.dtype]
     say(f"stack {case}: {cfg.name}, generating weights")
     weights = workload.all_weights(cfg)
-    eng = driver.Engine(cfg, weights=weights)
+    eng = driver.Engine(cfg, weights=weights, strategy=strategy, policy=policy, budget=budget)
     p64 = [{k: np.asarray(v, np.float64) for k, v in w.items()} for w in weights]
     emb = workload.embeddings(cfg)
     orders = workload.orders(cfg)
@@ -137,15 +167,26 @@ def test_stack_parity(case):
                 # the decoder input is pure data movement: bitwise equal
                 np.testing.assert_array_equal(g["x_in"][i], x_in.astype(np.float32))
                 full = osched.is_full_step(t, cfg.full_every)
-                k = ostep.refresh_count("ratio", cfg.ratio_bp, N, len(gen), len(cache))
+                forced = [] if strategy == "no-caching" else cache
+                k = ostep.refresh_count(policy, budget, N, len(gen), len(forced))
                 ov = None
-                if not full:
-                    ov = _validated_override(g["R"][i], tol, note)
-                    ov.excl = gen + cache
+                if not full and strategy == "random":
+                    # the random sets are seeded inputs, drawn by the workload module
+                    cand_all = np.stack([np.setdiff1d(np.arange(N), osched.generating_tokens(
+                        orders[bb], cfg.n_buf, cfg.n_steps, t) + osched.caching_tokens(
+                        orders[bb], cfg.n_buf, cfg.n_steps, t)) for bb in range(cfg.batch)])
+                    r_rand = workload.random_refresh(cfg, t, cand_all, k)[b].tolist()
+                    np.testing.assert_array_equal(sorted(g["R"][i]), r_rand)
+                    ov = lambda scores, ref, r=r_rand: r
+                elif not full:
+                    ov = _validated_override(g["R"][i], tol, note, lowest=strategy == "low-attention")
+                    ov.excl = gen + forced
                 say(f"  oracle image {b} step {t}")
-                res = ostep.marche_step(p64, x_in, kcs, vcs, gen, cache, n_heads=H, eps=cfg.ln_eps,
+                res = ostep.marche_step(p64, x_in, kcs, vcs, gen, forced, n_heads=H, eps=cfg.ln_eps,
                                         sel_layer=cfg.sel_layer, full=full, k_refresh=k,
-                                        keep_layers=True, refresh_override=ov)
+                                        keep_layers=True, refresh_override=ov,
+                                        select_lowest=strategy == "low-attention",
+                                        include_gen=strategy != "no-generating")
                 x_prev_g = g["x_in"][i].astype(np.float64)
                 x_prev_o = x_in
                 for l, (lg, lo) in enumerate(zip(g["layers"], res.layers)):
@@ -161,12 +202,14 @@ def test_stack_parity(case):
                         assert e <= tol, f"image {b} step {t} layer {l}: {key} rel err {e:.3e} > {tol}"
                     x_prev_g = lg["x"][i].astype(np.float64)
                     x_prev_o = lo.x_out
-                if not full:
+                if not full and g["scores"] is not None:
                     e = rel_err(g["scores"][i], res.scores)
                     worst["scores"] = max(worst.get("scores", 0.0), e)
                     assert e <= tol, f"scores rel err {e:.3e}"
+                if strategy != "no-generating":
                     z_err = rel_err(g["layers"][-1]["x"][i][gen], res.z)
                     worst["z"] = max(worst.get("z", 0.0), z_err)
+                    assert z_err <= tol, f"z rel err {z_err:.3e}"
                 kcs, vcs = res.k_caches, res.v_caches
     say(f"  {case}: worst rel err {({k: f'{v:.2e}' for k, v in worst.items()})}; refresh sets: "
         f"{note['exact']} exact, {note['ambiguous']} ambiguous "

@@ -68,3 +68,28 @@ def test_budget_ratio_special_cases():
 def test_total_scores_sums_heads():
     s = RNG.random((3, 9))
     np.testing.assert_allclose(select.total_scores(s), s[0] + s[1] + s[2], rtol=1e-15)
+
+
+@pytest.mark.parametrize("trial", range(25))
+def test_lowest_first_matches_bruteforce_and_enumeration(trial):
+    # the low-attention ablation: the k candidates with the lowest scores
+    rng = np.random.default_rng(100 + trial)
+    n = int(rng.integers(1, 12))
+    s = rng.integers(0, 4, size=n).astype(float)
+    excl = rng.choice(n, int(rng.integers(0, n)), replace=False).tolist()
+    cand = [j for j in range(n) if j not in excl]
+    k = int(rng.integers(0, len(cand) + 1))
+    got = select.select_topk(s, excl, k, lowest=True)
+    assert got == select.select_topk_bruteforce(s, excl, k, lowest=True)
+    best = min((sum(s[j] for j in c) for c in itertools.combinations(cand, k)), default=0.0)
+    assert sum(s[j] for j in got) == best
+    minimal = [list(c) for c in itertools.combinations(cand, k) if sum(s[j] for j in c) == best]
+    assert got == min(minimal)
+    # lowest-first on s equals highest-first on -s
+    assert got == select.select_topk(-s, excl, k)
+
+
+def test_lowest_first_nan_last():
+    s = np.array([0.3, np.nan, 0.1, 0.2])
+    assert select.select_topk(s, [], 3, lowest=True) == [0, 2, 3]
+    assert select.select_topk(s, [], 4, lowest=True) == [0, 1, 2, 3]
