@@ -23,10 +23,17 @@ namespace marche {
 
 // ------------------------------------------------------------------ epilogues
 //
-// Every epilogue receives four consecutive output columns col0..col0+3 of one
+// Every epilogue works on four consecutive output columns col0..col0+3 of one
 // row (col0 a multiple of 4), so each lane issues 8- or 16-byte stores.  Four
 // consecutive columns never straddle a q|k|v third or a head (d_model and
 // head_dim are multiples of 4).
+//
+// The write-back runs in three phases so that no load waits behind a store
+// (on this architecture the vector-memory counter also counts stores):
+//   row(r)            per-row addressing data (may load the row map),
+//   bias(col0)        the bias of four columns,
+//   prior(row, col0)  the value the result is added to (residual epilogues),
+// all issued before the first store(row, r, col0, v), v = acc + bias + prior.
 
 template <typename T>
 __device__ __forceinline__ void store4(T *p, f32x4 v) {
@@ -44,16 +51,20 @@ __device__ __forceinline__ f32x4 load_bias4(const float *bias, int col0) {
 
 template <typename T>
 struct EpiQkv {
+  static constexpr bool kPrior = false;
   T *q;
   T *kc;
   T *vc;
   const float *bias;
   const RowMap *map;
   int d_model, head_dim, n_heads, n_tokens;
-  __device__ __forceinline__ void operator()(int row, int col0, f32x4 v) const {
-    v += load_bias4(bias, col0);
+  using Row = RowMap;
+  __device__ __forceinline__ Row row(int r) const { return map[r]; }
+  __device__ __forceinline__ f32x4 bias4(int col0) const { return load_bias4(bias, col0); }
+  __device__ __forceinline__ f32x4 prior(const Row &, int) const { return f32x4{}; }
+  __device__ __forceinline__ void store(const Row &m, int r, int col0, f32x4 v) const {
     if (col0 < d_model) {
-      store4(q + (size_t)row * d_model + col0, v);
+      store4(q + (size_t)r * d_model + col0, v);
       return;
     }
     int c = col0 - d_model;
@@ -63,7 +74,6 @@ struct EpiQkv {
       dst = vc;
     }
     const int h = c / head_dim, d = c - h * head_dim;
-    const RowMap m = map[row];
     store4(dst + ((size_t)(m.b * n_heads + h) * n_tokens + m.tok) * head_dim + d, v);
   }
 };
@@ -72,27 +82,102 @@ struct EpiQkv {
 // symbols, so per-kernel profiles can tell them apart.
 template <int TAG>
 struct EpiResid {
+  static constexpr bool kPrior = true;
   float *x;
   const float *bias;
   const RowMap *map;
   int n;
-  __device__ __forceinline__ void operator()(int row, int col0, f32x4 v) const {
-    f32x4 *p = reinterpret_cast<f32x4 *>(x + (size_t)map[row].x_row * n + col0);
-    *p = *p + (v + load_bias4(bias, col0));
+  using Row = int32_t;  // residual-stream row
+  __device__ __forceinline__ Row row(int r) const { return map[r].x_row; }
+  __device__ __forceinline__ f32x4 bias4(int col0) const { return load_bias4(bias, col0); }
+  __device__ __forceinline__ f32x4 prior(const Row &xr, int col0) const {
+    return *reinterpret_cast<const f32x4 *>(x + (size_t)xr * n + col0);
+  }
+  __device__ __forceinline__ void store(const Row &xr, int, int col0, f32x4 v) const {
+    *reinterpret_cast<f32x4 *>(x + (size_t)xr * n + col0) = v;
   }
 };
 
 template <typename T>
 struct EpiGelu {
+  static constexpr bool kPrior = false;
   T *h;
   const float *bias;
   int n;
-  __device__ __forceinline__ void operator()(int row, int col0, f32x4 v) const {
-    v += load_bias4(bias, col0);
+  using Row = int32_t;
+  __device__ __forceinline__ Row row(int r) const { return r; }
+  __device__ __forceinline__ f32x4 bias4(int col0) const { return load_bias4(bias, col0); }
+  __device__ __forceinline__ f32x4 prior(const Row &, int) const { return f32x4{}; }
+  __device__ __forceinline__ void store(const Row &, int r, int col0, f32x4 v) const {
     f32x4 g = {gelu_erf(v[0]), gelu_erf(v[1]), gelu_erf(v[2]), gelu_erf(v[3])};
-    store4(h + (size_t)row * n + col0, g);
+    store4(h + (size_t)r * n + col0, g);
   }
 };
+
+// Empty uses that pin loaded values to this point: without them the compiler
+// sinks the loads into the row-guarded store blocks, one wait per block.
+__device__ __forceinline__ void keep(const f32x4 &v) { asm volatile("" ::"v"(v)); }
+__device__ __forceinline__ void keep(int32_t v) { asm volatile("" ::"v"(v)); }
+__device__ __forceinline__ void keep(const RowMap &m) {
+  asm volatile("" ::"v"(m.x_row), "v"(m.b), "v"(m.tok));
+}
+
+// Write-back of one wavefront's TM x TN block of 32x32 accumulators (C^T
+// layout: lane l owns output row l & 31 of each block and, in register group g,
+// columns g * 8 + (l / 32) * 4 .. + 3).  Rows at or beyond M are clamped for
+// the loads and skipped for the stores.  Residual priors are loaded for IB
+// block rows at a time, at most 16 four-column groups (64 registers).
+template <int TM, int TN, class Epi>
+__device__ __forceinline__ void write_back(const f32x16 (&acc)[TN][TM], const Epi &epi, int row0,
+                                           int col_base, int M, int lane) {
+  typename Epi::Row rinfo[TM];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) rinfo[i] = epi.row(min(row0 + i * 32 + (lane & 31), M - 1));
+  f32x4 b[TN][4];
+#pragma unroll
+  for (int j = 0; j < TN; ++j)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) b[j][g] = epi.bias4(col_base + j * 32 + g * 8 + (lane >> 5) * 4);
+#pragma unroll
+  for (int i = 0; i < TM; ++i) keep(rinfo[i]);
+  constexpr int IB = (16 / (TN * 4)) < 1 ? 1 : ((16 / (TN * 4)) > TM ? TM : 16 / (TN * 4));
+#pragma unroll
+  for (int i0 = 0; i0 < TM; i0 += IB) {
+    f32x4 pr[IB][TN][4];
+#pragma unroll
+    for (int ii = 0; ii < IB; ++ii)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          pr[ii][j][g] = Epi::kPrior
+                             ? epi.prior(rinfo[i0 + ii], col_base + j * 32 + g * 8 + (lane >> 5) * 4)
+                             : f32x4{};
+    if constexpr (Epi::kPrior) {
+#pragma unroll
+      for (int ii = 0; ii < IB; ++ii)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) keep(pr[ii][j][g]);
+    }
+#pragma unroll
+    for (int ii = 0; ii < IB; ++ii) {
+      const int i = i0 + ii;
+      const int row = row0 + i * 32 + (lane & 31);
+      if (row >= M) continue;
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 a = {acc[j][i][4 * g + 0], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2],
+                           acc[j][i][4 * g + 3]};
+          epi.store(rinfo[i], row, col_base + j * 32 + g * 8 + (lane >> 5) * 4,
+                    a + b[j][g] + pr[ii][j][g]);
+        }
+    }
+  }
+}
 
 // ------------------------------------------------------------------ bf16 MFMA
 //
@@ -255,20 +340,7 @@ __global__ __launch_bounds__(C::NT, C::MINB) void gemm_bf16_kernel(const bf16 *_
     }
   }
 
-#pragma unroll
-  for (int i = 0; i < C::TM; ++i) {
-    const int row = m0 + wm * C::WM + i * 32 + (lane & 31);
-    if (row >= M) continue;
-#pragma unroll
-    for (int j = 0; j < C::TN; ++j)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int col0 = n0 + wn * C::WN + j * 32 + g * 8 + (lane >> 5) * 4;
-        const f32x4 v = {acc[j][i][4 * g + 0], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2],
-                         acc[j][i][4 * g + 3]};
-        epi(row, col0, v);
-      }
-  }
+  write_back<C::TM, C::TN>(acc, epi, m0 + wm * C::WM, n0 + wn * C::WN, M, lane);
 }
 
 // 128x128 tile, 2x2 wavefronts of 64x64, two register stages, registers
@@ -337,12 +409,14 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float *__restrict__
     }
     __syncthreads();
   }
+  const f32x4 b = epi.bias4(n0 + tx * 4);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = m0 + ty * 4 + i;
     if (row >= M) continue;
+    const typename Epi::Row r = epi.row(row);
     const f32x4 v = {acc[i][0], acc[i][1], acc[i][2], acc[i][3]};
-    epi(row, n0 + tx * 4, v);
+    epi.store(r, row, n0 + tx * 4, v + b + (Epi::kPrior ? epi.prior(r, n0 + tx * 4) : f32x4{}));
   }
 }
 
