@@ -124,6 +124,8 @@ size_t marche_step_workspace_bytes(const marche_model_t *m, int32_t batch, int32
  *   x[b][i] += o_i W_o^T + b_o;   x[b][i] += W_2 GELU(W_1 LN2(x[b][i]) + b_1) + b_2
  * Rows of x and of the cache outside A_b are neither read by the MLP nor
  * written.  x is [batch][n_tokens][d_model] float32, updated in place.
+ * batch*n_tokens*d_model and a_total*max(3*d_model, d_mlp) must stay below
+ * 2^31 (UNSUPPORTED otherwise).
  *
  * Scores (Section 4.2): when `scores` is non-NULL and score_layer lies in
  * [layer_begin, layer_end), that layer also writes

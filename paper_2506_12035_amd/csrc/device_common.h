@@ -22,9 +22,23 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-// Exact-erf GELU: z * Phi(z).
+// erf(u) for u >= 0 by the rational approximation of Abramowitz & Stegun
+// 7.1.26 (after Hastings): erf(u) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5))))
+// exp(-u^2) with t = 1 / (1 + p u), absolute error below 1.5e-7 for every
+// u >= 0.  Branch-free: one reciprocal, one exp2, five FMAs.
+__device__ __forceinline__ float erf_nonneg(float u) {
+  constexpr float p = 0.3275911f, a1 = 0.254829592f, a2 = -0.284496736f, a3 = 1.421413741f,
+                  a4 = -1.453152027f, a5 = 1.061405429f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(p, u, 1.0f));
+  const float poly = t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, a5, a4), a3), a2), a1);
+  const float e = __builtin_amdgcn_exp2f(-(u * u) * 1.4426950408889634f);
+  return 1.0f - poly * e;
+}
+
+// Exact-erf GELU: z * Phi(z) = z (1 + erf(z / sqrt 2)) / 2, erf odd.
 __device__ __forceinline__ float gelu_erf(float z) {
-  return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f));
+  const float e = erf_nonneg(fabsf(z) * 0.70710678118654752f);
+  return 0.5f * z * (1.0f + copysignf(e, z));
 }
 
 template <typename T>

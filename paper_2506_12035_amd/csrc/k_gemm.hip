@@ -62,9 +62,10 @@ struct EpiQkv {
   __device__ __forceinline__ Row row(int r) const { return map[r]; }
   __device__ __forceinline__ f32x4 bias4(int col0) const { return load_bias4(bias, col0); }
   __device__ __forceinline__ f32x4 prior(const Row &, int) const { return f32x4{}; }
+  // 32-bit element offsets: the host limits every buffer to < 2^31 elements.
   __device__ __forceinline__ void store(const Row &m, int r, int col0, f32x4 v) const {
     if (col0 < d_model) {
-      store4(q + (size_t)r * d_model + col0, v);
+      store4(q + (uint32_t)(r * d_model + col0), v);
       return;
     }
     int c = col0 - d_model;
@@ -74,7 +75,7 @@ struct EpiQkv {
       dst = vc;
     }
     const int h = c / head_dim, d = c - h * head_dim;
-    store4(dst + ((size_t)(m.b * n_heads + h) * n_tokens + m.tok) * head_dim + d, v);
+    store4(dst + (uint32_t)(((m.b * n_heads + h) * n_tokens + m.tok) * head_dim + d), v);
   }
 };
 
@@ -87,14 +88,14 @@ struct EpiResid {
   const float *bias;
   const RowMap *map;
   int n;
-  using Row = int32_t;  // residual-stream row
-  __device__ __forceinline__ Row row(int r) const { return map[r].x_row; }
+  using Row = int32_t;  // element offset of the residual-stream row (< 2^31)
+  __device__ __forceinline__ Row row(int r) const { return map[r].x_row * n; }
   __device__ __forceinline__ f32x4 bias4(int col0) const { return load_bias4(bias, col0); }
   __device__ __forceinline__ f32x4 prior(const Row &xr, int col0) const {
-    return *reinterpret_cast<const f32x4 *>(x + (size_t)xr * n + col0);
+    return *reinterpret_cast<const f32x4 *>(x + (uint32_t)(xr + col0));
   }
   __device__ __forceinline__ void store(const Row &xr, int, int col0, f32x4 v) const {
-    *reinterpret_cast<f32x4 *>(x + (size_t)xr * n + col0) = v;
+    *reinterpret_cast<f32x4 *>(x + (uint32_t)(xr + col0)) = v;
   }
 };
 
@@ -110,7 +111,7 @@ struct EpiGelu {
   __device__ __forceinline__ f32x4 prior(const Row &, int) const { return f32x4{}; }
   __device__ __forceinline__ void store(const Row &, int r, int col0, f32x4 v) const {
     f32x4 g = {gelu_erf(v[0]), gelu_erf(v[1]), gelu_erf(v[2]), gelu_erf(v[3])};
-    store4(h + (size_t)r * n + col0, g);
+    store4(h + (uint32_t)(r * n + col0), g);
   }
 };
 
@@ -126,44 +127,65 @@ __device__ __forceinline__ void keep(const RowMap &m) {
 // layout: lane l owns output row l & 31 of each block and, in register group g,
 // columns g * 8 + (l / 32) * 4 .. + 3).  Rows at or beyond M are clamped for
 // the loads and skipped for the stores.  Residual priors are loaded for IB
-// block rows at a time, at most 16 four-column groups (64 registers).
-template <int TM, int TN, class Epi>
+// block rows at a time (at most 16 four-column groups, 64 registers), each
+// batch's loads issued before the previous batch's stores.
+//
+// With BIAS_LDS, the biases of the block's columns come from LDS
+// (bias_lds[c - col_base] for column c; the caller staged them there), which
+// keeps them out of registers and off the vector-memory counter.
+template <int TM, int TN, bool BIAS_LDS = false, class Epi>
 __device__ __forceinline__ void write_back(const f32x16 (&acc)[TN][TM], const Epi &epi, int row0,
-                                           int col_base, int M, int lane) {
+                                           int col_base, int M, int lane,
+                                           const float *bias_lds = nullptr) {
   typename Epi::Row rinfo[TM];
 #pragma unroll
   for (int i = 0; i < TM; ++i) rinfo[i] = epi.row(min(row0 + i * 32 + (lane & 31), M - 1));
-  f32x4 b[TN][4];
+  f32x4 b[BIAS_LDS ? 1 : TN][4];
+  if constexpr (!BIAS_LDS) {
 #pragma unroll
-  for (int j = 0; j < TN; ++j)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
-    for (int g = 0; g < 4; ++g) b[j][g] = epi.bias4(col_base + j * 32 + g * 8 + (lane >> 5) * 4);
+      for (int g = 0; g < 4; ++g) b[j][g] = epi.bias4(col_base + j * 32 + g * 8 + (lane >> 5) * 4);
+  }
+  auto bias_of = [&](int j, int g) -> f32x4 {
+    if constexpr (BIAS_LDS)
+      return *reinterpret_cast<const f32x4 *>(bias_lds + j * 32 + g * 8 + (lane >> 5) * 4);
+    else
+      return b[j][g];
+  };
 #pragma unroll
   for (int i = 0; i < TM; ++i) keep(rinfo[i]);
   constexpr int IB = (16 / (TN * 4)) < 1 ? 1 : ((16 / (TN * 4)) > TM ? TM : 16 / (TN * 4));
-#pragma unroll
-  for (int i0 = 0; i0 < TM; i0 += IB) {
-    f32x4 pr[IB][TN][4];
+  constexpr int NB = TM / IB;
+  static_assert(TM % IB == 0, "prior batches");
+  f32x4 pr[2][IB][TN][4];
+  auto load_priors = [&](int bi, f32x4 (&dst)[IB][TN][4]) {
 #pragma unroll
     for (int ii = 0; ii < IB; ++ii)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int g = 0; g < 4; ++g)
-          pr[ii][j][g] = Epi::kPrior
-                             ? epi.prior(rinfo[i0 + ii], col_base + j * 32 + g * 8 + (lane >> 5) * 4)
-                             : f32x4{};
+          dst[ii][j][g] = Epi::kPrior ? epi.prior(rinfo[bi * IB + ii],
+                                                  col_base + j * 32 + g * 8 + (lane >> 5) * 4)
+                                      : f32x4{};
+  };
+  load_priors(0, pr[0]);
+#pragma unroll
+  for (int bi = 0; bi < NB; ++bi) {
+    // the next batch's loads go out before this batch's stores
+    if (bi + 1 < NB) load_priors(bi + 1, pr[(bi + 1) & 1]);
     if constexpr (Epi::kPrior) {
 #pragma unroll
       for (int ii = 0; ii < IB; ++ii)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
-          for (int g = 0; g < 4; ++g) keep(pr[ii][j][g]);
+          for (int g = 0; g < 4; ++g) keep(pr[bi & 1][ii][j][g]);
     }
 #pragma unroll
     for (int ii = 0; ii < IB; ++ii) {
-      const int i = i0 + ii;
+      const int i = bi * IB + ii;
       const int row = row0 + i * 32 + (lane & 31);
       if (row >= M) continue;
 #pragma unroll
@@ -173,7 +195,7 @@ __device__ __forceinline__ void write_back(const f32x16 (&acc)[TN][TM], const Ep
           const f32x4 a = {acc[j][i][4 * g + 0], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2],
                            acc[j][i][4 * g + 3]};
           epi.store(rinfo[i], row, col_base + j * 32 + g * 8 + (lane >> 5) * 4,
-                    a + b[j][g] + pr[ii][j][g]);
+                    a + bias_of(j, g) + pr[bi & 1][ii][j][g]);
         }
     }
   }
@@ -346,9 +368,6 @@ __global__ __launch_bounds__(C::NT, C::MINB) void gemm_bf16_kernel(const bf16 *_
 // 128x128 tile, 2x2 wavefronts of 64x64, two register stages, registers
 // budgeted for two workgroups per CU.
 using TileS = TileCfg<128, 128, 64, 2, 2, 2, 2>;
-// 256x256 tile, 2x4 wavefronts of 128x64 (two per SIMD), one register stage:
-// for large-M projections to wide outputs (measured faster there).
-using TileL = TileCfg<256, 256, 64, 2, 4, 1, 1>;
 
 template <class C, class Epi>
 static hipError_t launch_tile(const void *a, const void *w, int m, int n, int k, const Epi &epi,
@@ -359,10 +378,196 @@ static hipError_t launch_tile(const void *a, const void *w, int m, int n, int k,
   return hipGetLastError();
 }
 
-bool gemm_large_tile(DType dt, int32_t m, int32_t n) {
-  if (dt != DType::BF16) return false;
-  const long large_tiles = (long)((m + TileL::BM - 1) / TileL::BM) * (n / TileL::BN);
-  return n % TileL::BN == 0 && n >= 3072 && large_tiles >= 512;
+// ------------------------------------------------------------------ 256x256 tile
+//
+// For projections where every token is active: a 256x256x64 workgroup tile
+// on four wavefronts of 128x128 (16 accumulators each, which live in the
+// accumulation registers).  Operands go from global memory straight into LDS
+// (global_load_lds_dwordx4: no staging registers, no LDS write instructions)
+// through two 64 KB stages of 128-byte rows whose 16-byte chunks are permuted
+// by an XOR with the row pair index, so the 16 rows one fragment read touches
+// per chunk hit 16 distinct bank groups.  Every MFMA is issued in a fixed
+// slot with at most one memory operation beside it (sched_barrier): the eight
+// fragment reads of the next k16 step, the sixteen loads of the next k-tile
+// and the barrier are spread over the 64 MFMAs of a k-tile, and the loads of
+// k-tile t+1 have the whole of k-tile t to land.
+namespace big {
+
+constexpr int kStage = 65536;  // bytes per stage: activation rows [0, 32K), weight rows [32K, 64K)
+
+struct Frag {
+  bf16x8 x[4];  // activation rows (MFMA B operand)
+  bf16x8 w[4];  // weight rows (MFMA A operand)
+};
+
+__device__ __forceinline__ void pin() { __builtin_amdgcn_sched_barrier(0); }
+
+__device__ __forceinline__ int swz(int r, int kc) { return kc ^ ((r >> 1) & 7); }
+
+// Load instruction q (0..63 per k-tile, 16 per wavefront) moves 1 KB: q < 32
+// carries activation rows 8q..8q+7, q >= 32 weight rows 8(q-32)..; lane l
+// writes LDS bytes [16 l, 16 l + 16) of the block, i.e. row 8q + l / 8 at
+// physical chunk l % 8, which holds logical chunk swz(row, l % 8).
+__device__ __forceinline__ void load_lds(unsigned char *stage, int q, const bf16 *A, const bf16 *W,
+                                         int M, int K, int m0, int n0, int k0, int lane) {
+  const int rr = lane >> 3, pc = lane & 7;
+  const bf16 *g;
+  if (q < 32) {
+    const int r = q * 8 + rr;
+    g = A + (size_t)min(m0 + r, M - 1) * K + k0 + swz(r, pc) * 8;
+  } else {
+    const int r = (q - 32) * 8 + rr;
+    g = W + (size_t)(n0 + r) * K + k0 + swz(r, pc) * 8;
+  }
+  const unsigned lds = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void *)(stage + q * 1024);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds))
+               : "memory", "m0");
+}
+
+// Fragment r of k16 step s, in the order the MFMAs need them: x0 w0 x1 x2 x3 w1 w2 w3.
+__device__ __forceinline__ void read_frag(Frag &f, int r, const unsigned char *stage, int s, int wm,
+                                          int wn, int lane) {
+  const bool is_x = (r == 0 || r == 2 || r == 3 || r == 4);
+  const int idx = r <= 1 ? 0 : (r <= 4 ? r - 1 : r - 4);
+  const int kc = s * 2 + (lane >> 5);
+  if (is_x) {
+    const int row = wm * 128 + idx * 32 + (lane & 31);
+    f.x[idx] = *reinterpret_cast<const bf16x8 *>(stage + row * 128 + swz(row, kc) * 16);
+  } else {
+    const int row = wn * 128 + idx * 32 + (lane & 31);
+    f.w[idx] = *reinterpret_cast<const bf16x8 *>(stage + 32768 + row * 128 + swz(row, kc) * 16);
+  }
+}
+
+__device__ __forceinline__ void mfma(f32x16 (&acc)[4][4], const Frag &f, int q) {
+  const int j = q >> 2, i = q & 3;
+  acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.w[j], f.x[i], acc[j][i], 0, 0, 0);
+}
+
+// Own loads landed in LDS, own LDS reads done, then the workgroup barrier.
+__device__ __forceinline__ void barrier() {
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+}  // namespace big
+
+template <class Epi>
+__global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, const bf16 *W, int M,
+                                                               int N, int K, Epi epi) {
+  using namespace big;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * kStage];
+  const int tiles_m = (M + 255) / 256, tiles_n = N / 256;
+  int tm, tn;
+  tile_coords(xcd_remap(blockIdx.x, gridDim.x), tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * 256, n0 = tn * 256;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int q0 = wave * 16;  // this wavefront's load instructions q0 .. q0 + 15
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[j][i] = f32x16{};
+  const int nk = K / 64;
+
+  // k-tile 0 into stage 0; the first quarter of k-tile 1 into stage 1
+#pragma unroll
+  for (int p = 0; p < 16; ++p) load_lds(smem, q0 + p, A, W, M, K, m0, n0, 0, lane);
+  barrier();
+  Frag fa, fb;
+#pragma unroll
+  for (int r = 0; r < 8; ++r) read_frag(fa, r, smem, 0, wm, wn, lane);
+  {
+    const int k1 = min(1, nk - 1) * 64;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      load_lds(smem + kStage, q0 + p, A, W, M, K, m0, n0, k1, lane);
+      pin();
+    }
+  }
+
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    const int cur = kt & 1;
+    const unsigned char *sc = smem + cur * kStage;
+    unsigned char *sn = smem + (cur ^ 1) * kStage;
+    const int k1 = (kt + 1) * 64, k2 = min(kt + 2, nk - 1) * 64;
+    // k16 steps 0..2: fragments of the next step; the rest of k-tile kt+1
+#pragma unroll
+    for (int st = 0; st < 3; ++st) {
+      Frag &fc = (st & 1) ? fb : fa;
+      Frag &fn = (st & 1) ? fa : fb;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        mfma(acc, fc, q);
+        if (q < 8) read_frag(fn, q, sc, st + 1, wm, wn, lane);
+        else if (st == 0) load_lds(sn, q0 + 4 + (q - 8), A, W, M, K, m0, n0, k1, lane);
+        else if (st == 1 && q < 12) load_lds(sn, q0 + 12 + (q - 8), A, W, M, K, m0, n0, k1, lane);
+        pin();
+      }
+    }
+    // k16 step 3: barrier (k-tile kt+1 complete, stage cur free), first
+    // fragments of k-tile kt+1, first quarter of k-tile kt+2 into stage cur
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      mfma(acc, fb, q);
+      pin();
+    }
+    barrier();
+    pin();
+#pragma unroll
+    for (int q = 4; q < 12; ++q) {
+      mfma(acc, fb, q);
+      read_frag(fa, q - 4, sn, 0, wm, wn, lane);
+      pin();
+    }
+#pragma unroll
+    for (int q = 12; q < 16; ++q) {
+      mfma(acc, fb, q);
+      load_lds(smem + cur * kStage, q0 + (q - 12), A, W, M, K, m0, n0, k2, lane);
+      pin();
+    }
+  }
+  {  // last k-tile
+    const unsigned char *sc = smem + ((nk - 1) & 1) * kStage;
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      Frag &fc = (st & 1) ? fb : fa;
+      Frag &fn = (st & 1) ? fa : fb;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        mfma(acc, fc, q);
+        if (st < 3 && q < 8) read_frag(fn, q, sc, st + 1, wm, wn, lane);
+        pin();
+      }
+    }
+  }
+  // the last quarter-tile loads (a clamped repeat of the final k-tile) land,
+  // every wavefront is done with the stages; then the tile's 256 biases go
+  // to LDS for the write-back
+  barrier();
+  float *bias_lds = reinterpret_cast<float *>(smem);
+  if (tid < 64)
+    *reinterpret_cast<f32x4 *>(bias_lds + tid * 4) = epi.bias4(n0 + tid * 4);
+  __syncthreads();
+  write_back<4, 4, true>(acc, epi, m0 + wm * 128, n0 + wn * 128, M, lane, bias_lds + wn * 128);
+}
+
+// The 256x256 tile is chosen when its tiles fill the compute units in whole
+// waves well enough: at least 90% of the last wave, or 80% when K >= 2048
+// (the longer main loop amortises the tile's fixed start and write-back).
+// Otherwise the 128x128 tile, two workgroups per CU, fills the chip in finer
+// steps.  Measured at MAR-L sizes: full-step QKV, fc1 and fc2 and
+// cache-aware QKV take the large tile; the output projection and the other
+// cache-aware GEMMs the small one.
+bool gemm_large_tile(DType dt, int32_t m, int32_t n, int32_t k) {
+  if (dt != DType::BF16 || n % 256 != 0 || m <= 0) return false;
+  const long tiles = (long)((m + 255) / 256) * (n / 256);
+  const long cus = device_cu_count();
+  const long waves = (tiles + cus - 1) / cus;
+  const double fill = (double)tiles / (double)(waves * cus);
+  return fill >= 0.9 || (fill >= 0.8 && k >= 2048);
 }
 
 template <class Epi>
@@ -370,7 +575,12 @@ static hipError_t run_bf16(const void *a, const void *w, int m, int n, int k, co
                            hipStream_t s) {
   if (m == 0) return hipSuccess;
   if (n % TileS::BN != 0 || k % TileS::BK != 0) return hipErrorInvalidValue;
-  if (gemm_large_tile(DType::BF16, m, n)) return launch_tile<TileL>(a, w, m, n, k, epi, s);
+  if (gemm_large_tile(DType::BF16, m, n, k)) {
+    const int grid = ((m + 255) / 256) * (n / 256);
+    gemm_bf16_big_kernel<Epi><<<grid, 256, 0, s>>>(static_cast<const bf16 *>(a),
+                                                    static_cast<const bf16 *>(w), m, n, k, epi);
+    return hipGetLastError();
+  }
   return launch_tile<TileS>(a, w, m, n, k, epi, s);
 }
 

@@ -3,6 +3,8 @@
 // and optional per-kernel timing.  Public contract: include/marche.h.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -14,6 +16,22 @@
 #include "marche_internal.h"
 
 using namespace marche;
+
+int marche::device_cu_count() {
+  static std::atomic<int> cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+  if (dev < 64) {
+    const int v = cached[dev].load(std::memory_order_relaxed);
+    if (v > 0) return v;
+  }
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    cus = 256;
+  if (dev < 64) cached[dev].store(cus, std::memory_order_relaxed);
+  return cus;
+}
 
 namespace {
 
@@ -228,6 +246,15 @@ marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layer
                 a_max, a_total, m->n_tokens);
   if (gen_max < 0 || gen_max > a_max)
     return fail(MARCHE_ERR_INVALID_ARG, "gen_max=%d outside [0, a_max=%d]", gen_max, a_max);
+  {
+    // GEMM epilogues address x, the KV slice of a layer and the packed
+    // activations with 32-bit element offsets
+    const int64_t widest = std::max<int64_t>(3LL * m->d_model, m->d_mlp);
+    if ((int64_t)batch * m->n_tokens * m->d_model >= (1LL << 31) ||
+        (int64_t)a_total * widest >= (1LL << 31))
+      return fail(MARCHE_ERR_UNSUPPORTED,
+                  "batch*n_tokens*d_model or a_total*max(3*d_model, d_mlp) reaches 2^31 elements");
+  }
   if (layer_begin == layer_end || batch == 0 || a_total == 0) return MARCHE_OK;
   if (!x) return fail(MARCHE_ERR_INVALID_ARG, "x is NULL");
   if (!a_idx || !a_off) return fail(MARCHE_ERR_INVALID_ARG, "a_idx / a_off is NULL");
@@ -276,7 +303,7 @@ marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layer
            launch_gather_ln(dt, buf0, x, map, static_cast<const float *>(L.ln1_g),
                             static_cast<const float *>(L.ln1_b), M, D, m->ln_eps, stream));
     QkvOut qo{buf1, kc, vc, D, dh, H, N};
-    LAUNCH(K_GEMM_QKV + gemm_large_tile(dt, M, 3 * D), 2.0 * M * 3 * D * D,
+    LAUNCH(K_GEMM_QKV + gemm_large_tile(dt, M, 3 * D, D), 2.0 * M * 3 * D * D,
            gemm_bytes_act * ((double)M * D + 3.0 * D * D + 3.0 * M * D),
            launch_gemm_qkv(dt, buf0, L.w_qkv, static_cast<const float *>(L.b_qkv), M, 3 * D, D,
                            map, qo, stream));
@@ -290,17 +317,17 @@ marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layer
              es * (double)batch * N * D + 4.0 * batch * H * N,
              launch_attn_scores(dt, aa, n_gen, gen_max, scores, stream));
     }
-    LAUNCH(K_GEMM_O + gemm_large_tile(dt, M, D), 2.0 * M * D * D, gemm_bytes_act * ((double)M * D + (double)D * D) + 8.0 * M * D,
+    LAUNCH(K_GEMM_O + gemm_large_tile(dt, M, D, D), 2.0 * M * D * D, gemm_bytes_act * ((double)M * D + (double)D * D) + 8.0 * M * D,
            launch_gemm_resid(dt, buf0, L.w_o, static_cast<const float *>(L.b_o), M, D, D, map, x,
                              0, stream));
     LAUNCH(K_GATHER_LN, 0, (double)M * D * (4 + es),
            launch_gather_ln(dt, buf1, x, map, static_cast<const float *>(L.ln2_g),
                             static_cast<const float *>(L.ln2_b), M, D, m->ln_eps, stream));
-    LAUNCH(K_GEMM_FC1 + gemm_large_tile(dt, M, F), 2.0 * M * F * D,
+    LAUNCH(K_GEMM_FC1 + gemm_large_tile(dt, M, F, D), 2.0 * M * F * D,
            gemm_bytes_act * ((double)M * D + (double)F * D + (double)M * F),
            launch_gemm_gelu(dt, buf1, L.w_1, static_cast<const float *>(L.b_1), M, F, D, hid,
                             stream));
-    LAUNCH(K_GEMM_FC2 + gemm_large_tile(dt, M, D), 2.0 * M * D * F,
+    LAUNCH(K_GEMM_FC2 + gemm_large_tile(dt, M, D, F), 2.0 * M * D * F,
            gemm_bytes_act * ((double)M * F + (double)D * F) + 8.0 * M * D,
            launch_gemm_resid(dt, hid, L.w_2, static_cast<const float *>(L.b_2), M, D, F, map, x,
                              1, stream));
