@@ -42,6 +42,8 @@ HBM_BOUND = {"gather_ln", "attention_q32", "attention_q64", "attn_scores", "sele
 KERNEL_SOURCES = {
     "gemm": "paper_2506_12035_amd/csrc/k_gemm.hip",
     "attention": "paper_2506_12035_amd/csrc/k_attn.hip",
+    "select": "paper_2506_12035_amd/csrc/k_select.hip",
+    "elementwise": "paper_2506_12035_amd/csrc/k_elementwise.hip",
 }
 
 
@@ -50,7 +52,14 @@ def log(*a):
 
 
 def source_hash(kernel: str) -> str:
-    fam = "attention" if kernel.startswith("attention") or kernel == "attn_scores" else "gemm"
+    if kernel.startswith("attention") or kernel == "attn_scores":
+        fam = "attention"
+    elif kernel.startswith("gemm"):
+        fam = "gemm"
+    elif kernel == "select_topk":
+        fam = "select"
+    else:
+        fam = "elementwise"
     with open(os.path.join(ROOT, KERNEL_SOURCES[fam]), "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
@@ -63,10 +72,67 @@ def traffic_for(kernel: str, workload: str):
         return None
     with open(path) as f:
         rec = json.load(f)
-    e = rec.get(workload, {}).get(kernel)
-    if not e or e.get("source_sha") != source_hash(kernel):
+    e = rec.get(workload, {}).get("classes", {}).get(kernel)
+    if not e or e.get("source_sha") != source_hash(kernel) or not e.get("full_layer_only"):
         return None
     return e.get("bytes_per_launch")
+
+
+def counter_class(name: str):
+    """Timing class of a kernel symbol as rocprofv3 prints it (mangled or not)."""
+    tile = "t256" if "gemm_bf16_big_kernel" in name else "t128"
+    if "gemm_bf16" in name:
+        for key, cls in (("EpiResidILi1E", "fc2"), ("EpiResid<1>", "fc2"), ("EpiResidILi0E", "o"),
+                         ("EpiResid<0>", "o"), ("EpiGelu", "fc1"), ("EpiQkv", "qkv")):
+            if key in name:
+                return f"gemm_{cls}_{tile}"
+    if "attn_mfma_kernel" in name:
+        for nw, q in (("4", "q128"), ("2", "q64"), ("1", "q32")):
+            if f"ELi{nw}EEEv" in name or f", {nw}>(" in name:
+                return f"attention_{q}"
+    for key, cls in (("gather_ln_kernel", "gather_ln"), ("attn_scores_kernel", "attn_scores"),
+                     ("select_topk_kernel", "select_topk"), ("decoder_input_kernel", "decoder_input"),
+                     ("row_map_kernel", "row_map"), ("fill_zero_kernel", "fill_zero")):
+        if key in name:
+            return cls
+    return None
+
+
+def ingest_counters(paths: list, workload: str, full_layer_passes: int, commands: dict) -> dict:
+    """profiles/traffic.json entries from four rocprofv3 --pmc CSVs: FETCH_SIZE and
+    WRITE_SIZE of one step, then of the plain copy (--calibrate-copy).  Counter
+    KiB per dispatch are scaled by known-bytes / counter for the copy.  Only
+    classes whose every launch in the 64-step schedule is a full-layer launch
+    (the kind a one-step run at t = 0 sees) are comparable per launch with the
+    live timing and are marked so."""
+    import csv
+    import collections
+
+    def per_class(path):
+        agg = collections.defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            c = counter_class(r["Kernel_Name"])
+            if c:
+                agg[c].append(float(r["Counter_Value"]) * 1024.0)
+        return agg
+
+    def copy_bytes(path):
+        v = [float(r["Counter_Value"]) * 1024.0 for r in csv.DictReader(open(path))
+             if "copyBuffer" in r["Kernel_Name"]]
+        return max(v)
+
+    fetch, write = per_class(paths[0]), per_class(paths[1])
+    copy_n = commands["copy_bytes"]
+    sf, sw = copy_n / copy_bytes(paths[2]), copy_n / copy_bytes(paths[3])
+    out = {}
+    for c in sorted(set(fetch) | set(write)):
+        f = sum(fetch.get(c, [0.0])) / max(1, len(fetch.get(c, [])))
+        w = sum(write.get(c, [0.0])) / max(1, len(write.get(c, [])))
+        out[c] = {"fetch_bytes": f * sf, "write_bytes": w * sw, "bytes_per_launch": f * sf + w * sw,
+                  "dispatches": len(fetch.get(c, [])), "source_sha": source_hash(c),
+                  "full_layer_only": None}
+    return {"scale": {"fetch": sf, "write": sw}, "classes": out,
+            "full_layer_passes": full_layer_passes}
 
 
 def kernel_rates(prof: dict, dtype: str) -> dict:
@@ -155,6 +221,33 @@ def timed(eng, steps, first, T):
     return wall, per, kinds
 
 
+def ingest_main(args) -> int:
+    from paper_2506_12035_amd import schedule, workload
+
+    cfg = workload.CONFIGS[args.config]
+    T = cfg.n_steps
+    n_full = sum(schedule.full_step(t, cfg.full_every) for t in range(T))
+    passes = n_full * cfg.n_layers + (T - n_full) * cfg.sel_layer
+    fcsv, wcsv, cf, cw, bjson = args.ingest_counters
+    rec = ingest_counters([fcsv, wcsv, cf, cw], cfg.name, passes,
+                          {"copy_bytes": 1024 * (1 << 20)})
+    with open(bjson) as f:
+        lines = [ln for ln in f.read().splitlines() if ln.startswith("{")]
+    launches = {k: v["launches"] for k, v in json.loads(lines[-1]).get("kernels", {}).items()}
+    for c, e in rec["classes"].items():
+        e["full_layer_only"] = launches.get(c) == passes
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    allrec = {}
+    if os.path.exists(path):
+        with open(path) as f:
+            allrec = json.load(f)
+    allrec[cfg.name] = rec
+    with open(path, "w") as f:
+        json.dump(allrec, f, indent=1, sort_keys=True)
+    print(json.dumps(rec, indent=1))
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -181,7 +274,15 @@ def main() -> int:
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB five times (the "
                          "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
+    ap.add_argument("--ingest-counters", nargs=5, default=None,
+                    metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV", "BENCH_JSON"),
+                    help="write profiles/traffic.json from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE "
+                         "CSVs of a one-step run (--steps 1 --warmup 0) and of --calibrate-copy "
+                         "1024, with the bench JSON line of a kernel-trace run of the same "
+                         "workload (to mark classes launched only in full layers); no GPU needed")
     args = ap.parse_args()
+    if args.ingest_counters:
+        return ingest_main(args)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
