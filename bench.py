@@ -221,6 +221,100 @@ def timed(eng, steps, first, T):
     return wall, per, kinds
 
 
+APPB_SIZES = ((32, 256), (64, 256), (128, 256), (32, 512), (32, 1024), (64, 1024),
+              (256, 1024), (32, 2048))
+
+
+def appb_main(args) -> int:
+    """Appendix B on MI355X.  Per (n_active, n_cached): inputs resident in HBM
+    (several copies rotated so that no call finds them in the 256 MB memory-side
+    cache), then
+      concat      = concatenate K_A|K_C and V_A|V_C (this library's copy kernel),
+                    then attend over one segment;
+      torch_cat   = the same with torch.cat as the concatenation;
+      two_segment = one pass over the two segments' own buffers (the method);
+      resident    = attention over one buffer that already holds both segments
+                    (this build's production layout: the QKV epilogue writes the
+                    fresh rows into the cache, so no merge step exists at all).
+    Each timed with HIP events over 20 calls after 3 warm-up calls."""
+    import numpy as np
+    import torch
+
+    from paper_2506_12035_amd import binding, workload
+
+    B, H, dh = 128, 16, 64
+    D = H * dh
+    bf = torch.bfloat16
+    stream = torch.cuda.current_stream()
+    rows = []
+    for na, nc in APPB_SIZES:
+        c = workload.segment_case(B, H, dh, na, nc)
+        per_copy = 2 * (2 * B * na * D + 2 * B * (na + nc) * D)
+        copies = max(2, int(np.ceil(512e6 / per_copy)))
+        dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(bf)
+        base = [dev(c.q), dev(c.k_a), dev(c.v_a), dev(c.k_c), dev(c.v_c)]
+        sets = [[t.clone() for t in base] for _ in range(copies)]
+        resident = [(torch.cat([s_[1], s_[3]], dim=2).contiguous(),
+                     torch.cat([s_[2], s_[4]], dim=2).contiguous()) for s_ in sets]
+        o = torch.empty(B, na, D, device="cuda", dtype=bf)
+        wsb = binding.attention_workspace_bytes(B, H, dh, na, nc, binding.MARCHE_BF16,
+                                                binding.MARCHE_ATTN_CONCAT)
+        ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+
+        def run(kind, i):
+            q, ka, va, kc, vc = sets[i % copies]
+            if kind == "concat":
+                binding.attention_segments(q, o, na, ka, va, na, kc, vc, nc, B, H, dh,
+                                           binding.MARCHE_BF16, binding.MARCHE_ATTN_CONCAT, ws, wsb,
+                                           stream)
+            elif kind == "two_segment":
+                binding.attention_segments(q, o, na, ka, va, na, kc, vc, nc, B, H, dh,
+                                           binding.MARCHE_BF16, binding.MARCHE_ATTN_TWO_SEGMENT,
+                                           None, 0, stream)
+            elif kind == "torch_cat":
+                kr = torch.cat([ka, kc], dim=2)
+                vr = torch.cat([va, vc], dim=2)
+                binding.attention_segments(q, o, na, kr, vr, na + nc, None, None, 0, B, H, dh,
+                                           binding.MARCHE_BF16, binding.MARCHE_ATTN_TWO_SEGMENT,
+                                           None, 0, stream)
+            else:
+                kr, vr = resident[i % copies]
+                binding.attention_segments(q, o, na, kr, vr, na + nc, None, None, 0, B, H, dh,
+                                           binding.MARCHE_BF16, binding.MARCHE_ATTN_TWO_SEGMENT,
+                                           None, 0, stream)
+
+        res = {}
+        for kind in ("concat", "torch_cat", "two_segment", "resident"):
+            for i in range(3):
+                run(kind, i)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for i in range(20):
+                run(kind, i)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            res[kind] = e0.elapsed_time(e1) / 20 * 1e3
+        attn_bytes = 2.0 * (2 * B * na * D + 2 * B * (na + nc) * D)
+        row = {"n_active": na, "n_cached": nc, "us": {k: round(v, 1) for k, v in res.items()},
+               "two_segment_vs_concat": round(1 - res["two_segment"] / res["concat"], 4),
+               "two_segment_vs_torch_cat": round(1 - res["two_segment"] / res["torch_cat"], 4),
+               "resident_vs_concat": round(1 - res["resident"] / res["concat"], 4),
+               "two_segment_hbm_frac": round(attn_bytes / (res["two_segment"] * 1e-6) / 1e9
+                                             / PEAK_HBM_GBS, 4)}
+        log(f"[appb] {na:4d} / {nc:5d}: concat {res['concat']:8.1f} us, torch.cat+attend "
+            f"{res['torch_cat']:8.1f} us, two-segment "
+            f"{res['two_segment']:8.1f} us ({100 * row['two_segment_vs_concat']:+.1f}%), resident "
+            f"{res['resident']:8.1f} us ({100 * row['resident_vs_concat']:+.1f}%), two-segment at "
+            f"{100 * row['two_segment_hbm_frac']:.1f}% of HBM")
+        rows.append(row)
+        del sets, resident, ws
+        torch.cuda.empty_cache()
+    print(json.dumps({"appendix_b": rows, "batch": B, "heads": H, "head_dim": dh,
+                      "dtype": "bf16"}), flush=True)
+    return 0
+
+
 def ingest_main(args) -> int:
     from paper_2506_12035_amd import schedule, workload
 
@@ -274,6 +368,10 @@ def main() -> int:
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB five times (the "
                          "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
+    ap.add_argument("--appb", action="store_true",
+                    help="only run Appendix B's comparison: attention over an active and a cached "
+                         "segment, concatenate-then-attend vs the two-segment pass vs one resident "
+                         "buffer, MAR-L heads at batch 128, over a sweep of segment lengths")
     ap.add_argument("--ingest-counters", nargs=5, default=None,
                     metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV", "BENCH_JSON"),
                     help="write profiles/traffic.json from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE "
@@ -302,6 +400,8 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
+    if args.appb:
+        return appb_main(args)
     if args.calibrate_copy:
         n = args.calibrate_copy * (1 << 20) // 4
         src = torch.arange(n, dtype=torch.float32, device="cuda")

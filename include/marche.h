@@ -187,6 +187,41 @@ marche_status_t marche_decoder_input(float *x, const float *cls, const float *va
                                      int32_t batch, int32_t n_tokens, int32_t n_buf,
                                      int32_t d_model, int32_t n_known, marche_stream_t stream);
 
+/* ---- Appendix B: attention over an active and a cached segment ----
+ * For each image b and head h, the n_query query rows attend over the keys
+ * [K_A ; K_C] -- the n_a keys of the active segment followed by the n_c keys
+ * of the cached segment -- and the same values:
+ *   o[b][i][h] = sum_j softmax_j(q[b][i][h] . K[b][h][j] / sqrt(head_dim)) V[b][h][j].
+ * (In Appendix B's setting n_query = n_a: the active tokens are the queries.)
+ * Layouts (bf16, 16-byte aligned): q and o [batch][n_query][n_heads*head_dim];
+ * k_a, v_a [batch][n_heads][n_a][head_dim]; k_c, v_c [batch][n_heads][n_c][head_dim];
+ * a segment of length 0 may pass NULL.
+ *
+ * MARCHE_ATTN_TWO_SEGMENT: one pass reads the key tiles of K_A and then of K_C
+ *   from their own buffers and merges them with a running maximum and a
+ *   rescaled running sum (Appendix A's online-softmax merge; nothing is
+ *   copied).  Needs no workspace.  With n_c = 0 it is attention over one
+ *   resident buffer, the layout marche_step uses.
+ * MARCHE_ATTN_CONCAT: the baseline Appendix B compares against: K_A and K_C
+ *   (and V_A, V_C) are first concatenated into the workspace, then the same
+ *   attention runs over one segment of n_a + n_c keys.
+ * The two modes differ only in rounding (the key tiles fall differently).
+ * head_dim in {64, 80}, 1 <= n_query <= 4096, n_a, n_c >= 0 with
+ * 1 <= n_a + n_c <= 65536, batch * n_heads <= 65535; UNSUPPORTED for other dtypes or head widths;
+ * WORKSPACE when CONCAT's workspace (marche_attention_workspace_bytes,
+ * 256-byte aligned) is missing or short. */
+typedef enum { MARCHE_ATTN_TWO_SEGMENT = 0, MARCHE_ATTN_CONCAT = 1 } marche_attn_mode_t;
+
+size_t marche_attention_workspace_bytes(int32_t batch, int32_t n_heads, int32_t head_dim,
+                                         int32_t n_a, int32_t n_c, int32_t dtype, int32_t mode);
+
+marche_status_t marche_attention_segments(const void *q, void *o, int32_t n_query,
+                                          const void *k_a, const void *v_a, int32_t n_a,
+                                          const void *k_c, const void *v_c, int32_t n_c,
+                                          int32_t batch, int32_t n_heads, int32_t head_dim,
+                                          int32_t dtype, int32_t mode, void *workspace,
+                                          size_t workspace_bytes, marche_stream_t stream);
+
 /* Name of a status code (static string). */
 const char *marche_status_string(marche_status_t s);
 

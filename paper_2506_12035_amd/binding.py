@@ -19,11 +19,13 @@ MARCHE_OK, MARCHE_ERR_INVALID_ARG, MARCHE_ERR_UNSUPPORTED, MARCHE_ERR_HIP, MARCH
 MARCHE_F32, MARCHE_BF16 = 0, 1
 
 MARCHE_SELECT_HIGHEST, MARCHE_SELECT_LOWEST = 0, 1
+MARCHE_ATTN_TWO_SEGMENT, MARCHE_ATTN_CONCAT = 0, 1
 
 EXPORTED = (
     "kv_cache_init", "marche_step_workspace_bytes", "marche_step", "select_refresh",
     "select_refresh_ordered",
-    "marche_decoder_input", "marche_status_string", "marche_last_error",
+    "marche_decoder_input", "marche_attention_workspace_bytes", "marche_attention_segments",
+    "marche_status_string", "marche_last_error",
     "marche_profile_enable", "marche_profile_collect", "marche_profile_entry",
     "marche_profile_reset",
 )
@@ -70,6 +72,10 @@ def lib() -> C.CDLL:
         L.select_refresh.argtypes = [vp, i32, vp, vp, i32, i32, i32, vp, vp, vp]
         L.select_refresh_ordered.argtypes = [vp, i32, vp, vp, i32, i32, i32, vp, vp, i32, vp]
         L.marche_decoder_input.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, vp]
+        L.marche_attention_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i32, i32]
+        L.marche_attention_workspace_bytes.restype = sz
+        L.marche_attention_segments.argtypes = [vp, vp, i32, vp, vp, i32, vp, vp, i32, i32, i32,
+                                                i32, i32, i32, vp, sz, vp]
         L.marche_status_string.argtypes = [C.c_int]
         L.marche_status_string.restype = C.c_char_p
         L.marche_last_error.argtypes = []
@@ -83,7 +89,7 @@ def lib() -> C.CDLL:
         L.marche_profile_reset.argtypes = []
         L.marche_profile_reset.restype = None
         for name in ("kv_cache_init", "marche_step", "select_refresh", "select_refresh_ordered",
-                     "marche_decoder_input",
+                     "marche_decoder_input", "marche_attention_segments",
                      "marche_profile_enable", "marche_profile_entry"):
             getattr(L, name).restype = C.c_int
         _lib = L
@@ -167,6 +173,20 @@ def decoder_input(x, cls, value, mask, pos, rank, batch: int, n_tokens: int, n_b
     _check(lib().marche_decoder_input(_ptr(x), _ptr(cls), _ptr(value), _ptr(mask), _ptr(pos),
                                       _ptr(rank), batch, n_tokens, n_buf, d_model, n_known,
                                       _stream(stream)))
+
+
+def attention_workspace_bytes(batch: int, n_heads: int, head_dim: int, n_a: int, n_c: int,
+                              dtype: int, mode: int) -> int:
+    return lib().marche_attention_workspace_bytes(batch, n_heads, head_dim, n_a, n_c, dtype, mode)
+
+
+def attention_segments(q, o, n_query: int, k_a, v_a, n_a: int, k_c, v_c, n_c: int, batch: int,
+                       n_heads: int, head_dim: int, dtype: int, mode: int, workspace=None,
+                       workspace_bytes: int = 0, stream=None) -> None:
+    _check(lib().marche_attention_segments(_ptr(q), _ptr(o), n_query, _ptr(k_a), _ptr(v_a), n_a,
+                                           _ptr(k_c), _ptr(v_c), n_c, batch, n_heads, head_dim,
+                                           dtype, mode, _ptr(workspace), workspace_bytes,
+                                           _stream(stream)))
 
 
 def profile_enable(on: bool) -> None:

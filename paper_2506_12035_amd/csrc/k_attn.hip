@@ -19,6 +19,11 @@
 //     transposed in LDS with the keys of every 16-key group permuted to match
 //     the accumulator layout of S^T, so each MFMA operand is one 16-byte read.
 // Softmax runs in the log2 domain with fp32 statistics.
+//
+// The same kernel also takes the two segments as separate buffers (SEG2):
+// key tiles of the first segment, then of the second, in one online-softmax
+// pass -- Appendix A's merge without concatenation, as the stand-alone
+// two-segment attention of Appendix B's comparison.
 #include "device_common.h"
 
 namespace marche {
@@ -32,7 +37,7 @@ __device__ __forceinline__ int vperm16(int k) {
   return (k & 3) | (((k >> 3) & 1) << 2) | (((k >> 2) & 1) << 3);
 }
 
-template <int DH, int NW>
+template <int DH, int NW, bool SEG2 = false>
 __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chunks) {
   constexpr int NT = NW * 64;
   constexpr int KS = DH + 8;        // K tile row stride (elements)
@@ -49,16 +54,28 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
   const int id = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = id / chunks, chunk = id - bh * chunks;
   const int b = bh / a.n_heads, h = bh - b * a.n_heads;
-  const int r0 = a.a_off[b];
-  const int na = a.a_off[b + 1] - r0;
+  const int r0 = a.a_off ? a.a_off[b] : b * a.a_max;
+  const int na = a.a_off ? a.a_off[b + 1] - r0 : a.a_max;
   const int q0 = chunk * NW * 32;
   if (q0 >= na) return;  // uniform over the workgroup
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int N = a.n_tokens, D = a.d_model;
-  const size_t head_base = (size_t)(b * a.n_heads + h) * N * DH;
-  const bf16 *kg = static_cast<const bf16 *>(a.k_cache) + head_base;
-  const bf16 *vg = static_cast<const bf16 *>(a.v_cache) + head_base;
+  const int N2 = SEG2 ? a.n2 : 0;
+  const bf16 *kg = static_cast<const bf16 *>(a.k_cache) + (size_t)(b * a.n_heads + h) * N * DH;
+  const bf16 *vg = static_cast<const bf16 *>(a.v_cache) + (size_t)(b * a.n_heads + h) * N * DH;
+  const bf16 *kg2 = SEG2 ? static_cast<const bf16 *>(a.k2) + (size_t)(b * a.n_heads + h) * N2 * DH : kg;
+  const bf16 *vg2 = SEG2 ? static_cast<const bf16 *>(a.v2) + (size_t)(b * a.n_heads + h) * N2 * DH : vg;
+  const int nt1 = (N + TK - 1) / TK;
+  // key tile t: first segment for t < nt1, else the second; its first key
+  // within the segment and the segment's length
+  auto seg_of = [&](int t, const bf16 *&kb, const bf16 *&vb, int &t0, int &ns) {
+    if (!SEG2 || t < nt1) {
+      kb = kg; vb = vg; t0 = t * TK; ns = N;
+    } else {
+      kb = kg2; vb = vg2; t0 = (t - nt1) * TK; ns = N2;
+    }
+  };
 
   // V^T rows beyond DH (padding up to a multiple of 32) hold zeros.
   if constexpr (DHV > DH) {
@@ -83,13 +100,16 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
   constexpr int VPCH = TCH / 2;
   constexpr int LPV = (VPCH + NT - 1) / NT;
   u32x4 rk[LPT], rv0[LPV], rv1[LPV];
-  auto gload = [&](int t0) {
+  auto gload = [&](int t) {
+    const bf16 *kb, *vb;
+    int t0, ns;
+    seg_of(t, kb, vb, t0, ns);
 #pragma unroll
     for (int i = 0; i < LPT; ++i) {
       const int c = i * NT + tid;
       if (c < TCH) {
-        const int key = min(t0 + c / CPR, N - 1), d = (c % CPR) * 8;
-        rk[i] = *reinterpret_cast<const u32x4 *>(kg + (size_t)key * DH + d);
+        const int key = min(t0 + c / CPR, ns - 1), d = (c % CPR) * 8;
+        rk[i] = *reinterpret_cast<const u32x4 *>(kb + (size_t)key * DH + d);
       }
     }
 #pragma unroll
@@ -97,9 +117,9 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
       const int c = i * NT + tid;
       if (c < VPCH) {
         const int kp = c / CPR, d = (c % CPR) * 8;
-        const int k0 = min(t0 + 2 * kp, N - 1), k1 = min(t0 + 2 * kp + 1, N - 1);
-        rv0[i] = *reinterpret_cast<const u32x4 *>(vg + (size_t)k0 * DH + d);
-        rv1[i] = *reinterpret_cast<const u32x4 *>(vg + (size_t)k1 * DH + d);
+        const int k0 = min(t0 + 2 * kp, ns - 1), k1 = min(t0 + 2 * kp + 1, ns - 1);
+        rv0[i] = *reinterpret_cast<const u32x4 *>(vb + (size_t)k0 * DH + d);
+        rv1[i] = *reinterpret_cast<const u32x4 *>(vb + (size_t)k1 * DH + d);
       }
     }
   };
@@ -136,14 +156,19 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
 #pragma unroll
   for (int d = 0; d < ODB; ++d) acc[d] = f32x16{};
 
-  const int ntiles = (N + TK - 1) / TK;
+  const int ntiles = nt1 + (SEG2 ? (N2 + TK - 1) / TK : 0);
   gload(0);
   sstore(0);
   __syncthreads();
   for (int t = 0; t < ntiles; ++t) {
-    const int cur = t & 1, t0 = t * TK;
+    const int cur = t & 1;
+    int t0 = t * TK, ns = N;
+    if constexpr (SEG2) {
+      const bf16 *kb, *vb;
+      seg_of(t, kb, vb, t0, ns);
+    }
     const bool more = t + 1 < ntiles;
-    if (more) gload(t0 + TK);
+    if (more) gload(t + 1);
 
     // S^T for two 32-key blocks: lane -> query (lane & 31),
     // register r -> key (r / 4) * 8 + (lane / 32) * 4 + r % 4 of the block.
@@ -159,7 +184,7 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
       }
     }
     float mx = -INFINITY;
-    if (t0 + TK <= N) {  // every key of the tile exists
+    if (t0 + TK <= ns) {  // every key of the tile exists
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -173,7 +198,7 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = t0 + kb * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-          const float v = key < N ? s[kb][r] * sl2 : -INFINITY;
+          const float v = key < ns ? s[kb][r] * sl2 : -INFINITY;
           s[kb][r] = v;
           mx = fmaxf(mx, v);
         }
@@ -233,19 +258,82 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
   }
 }
 
-template <int DH, int NW>
+template <int DH, int NW, bool SEG2>
 static hipError_t run_attn_mfma(const AttnArgs &a, hipStream_t s) {
   const int chunks = (a.a_max + NW * 32 - 1) / (NW * 32);
   const int grid = a.batch * a.n_heads * chunks;
-  attn_mfma_kernel<DH, NW><<<grid, NW * 64, 0, s>>>(a, chunks);
+  attn_mfma_kernel<DH, NW, SEG2><<<grid, NW * 64, 0, s>>>(a, chunks);
   return hipGetLastError();
+}
+
+template <int DH, bool SEG2>
+static hipError_t attn_bf16_nw(const AttnArgs &a, hipStream_t s) {
+  if (a.a_max <= 32) return run_attn_mfma<DH, 1, SEG2>(a, s);
+  if (a.a_max <= 64) return run_attn_mfma<DH, 2, SEG2>(a, s);
+  return run_attn_mfma<DH, 4, SEG2>(a, s);
 }
 
 template <int DH>
 static hipError_t attn_bf16_dispatch(const AttnArgs &a, hipStream_t s) {
-  if (a.a_max <= 32) return run_attn_mfma<DH, 1>(a, s);
-  if (a.a_max <= 64) return run_attn_mfma<DH, 2>(a, s);
-  return run_attn_mfma<DH, 4>(a, s);
+  if (a.k2) return attn_bf16_nw<DH, true>(a, s);
+  return attn_bf16_nw<DH, false>(a, s);
+}
+
+// ------------------------------------------------------------ concatenation
+//
+// The baseline of Appendix B: K and V of the active segment and of the cached
+// segment copied into one buffer per (image, head), active rows first.  Per
+// (image, head) the destination is two contiguous copies, so chunk j (16
+// bytes) of the destination block comes from chunk j of the active block
+// (j < na * cpr) or chunk j - na * cpr of the cached block.  Each thread moves
+// CPT chunks of K and of V, all loads issued before the stores.  Grid:
+// (chunks of a destination block / (256 * CPT), image * head).
+constexpr int CONCAT_CPT = 4;
+
+__global__ __launch_bounds__(256) void concat_kv_kernel(u32x4 *__restrict__ kd, u32x4 *__restrict__ vd,
+                                                        const u32x4 *__restrict__ ka,
+                                                        const u32x4 *__restrict__ va,
+                                                        const u32x4 *__restrict__ kc,
+                                                        const u32x4 *__restrict__ vc, int a_chunks,
+                                                        int c_chunks) {
+  const int per = a_chunks + c_chunks;
+  const size_t bh = blockIdx.y;
+  const int j0 = blockIdx.x * 256 * CONCAT_CPT + threadIdx.x;
+  u32x4 kv[CONCAT_CPT], vv[CONCAT_CPT];
+#pragma unroll
+  for (int u = 0; u < CONCAT_CPT; ++u) {
+    const int j = j0 + u * 256;
+    if (j < per) {
+      const bool act = j < a_chunks;
+      const size_t src = act ? bh * a_chunks + j : bh * c_chunks + (j - a_chunks);
+      kv[u] = act ? ka[src] : kc[src];
+      vv[u] = act ? va[src] : vc[src];
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < CONCAT_CPT; ++u) {
+    const int j = j0 + u * 256;
+    if (j < per) {
+      kd[bh * per + j] = kv[u];
+      vd[bh * per + j] = vv[u];
+    }
+  }
+}
+
+hipError_t launch_concat_kv(DType dt, void *k_dst, void *v_dst, const void *k_a, const void *v_a,
+                            const void *k_c, const void *v_c, int32_t bh, int32_t na, int32_t nc,
+                            int32_t head_dim, hipStream_t s) {
+  const int es = dt == DType::BF16 ? 2 : 4;
+  if ((head_dim * es) % 16 != 0 || bh > 65535) return hipErrorInvalidValue;
+  const int cpr = head_dim * es / 16;
+  const int per = (na + nc) * cpr;
+  if (bh == 0 || per == 0) return hipSuccess;
+  const dim3 grid((per + 256 * CONCAT_CPT - 1) / (256 * CONCAT_CPT), bh);
+  concat_kv_kernel<<<grid, 256, 0, s>>>(
+      static_cast<u32x4 *>(k_dst), static_cast<u32x4 *>(v_dst), static_cast<const u32x4 *>(k_a),
+      static_cast<const u32x4 *>(v_a), static_cast<const u32x4 *>(k_c),
+      static_cast<const u32x4 *>(v_c), na * cpr, nc * cpr);
+  return hipGetLastError();
 }
 
 // fp32 attention: one wavefront per (active row, head).  Logits are formed
@@ -304,6 +392,7 @@ static hipError_t attn_f32_dispatch(const AttnArgs &a, hipStream_t s) {
 
 hipError_t launch_attention(DType dt, const AttnArgs &a, hipStream_t s) {
   if (a.a_total == 0) return hipSuccess;
+  if (a.k2 && dt != DType::BF16) return hipErrorInvalidValue;
   if (dt == DType::BF16) {
     if (a.head_dim == 64) return attn_bf16_dispatch<64>(a, s);
     if (a.head_dim == 80) return attn_bf16_dispatch<80>(a, s);

@@ -86,13 +86,14 @@ marche_status_t check_model(const marche_model_t *m) {
 enum KClass {
   K_ROW_MAP, K_GATHER_LN, K_GEMM_QKV, K_GEMM_QKV_L, K_ATTN_W1, K_ATTN_W2, K_ATTN_W4,
   K_ATTN_SCORES, K_GEMM_O, K_GEMM_O_L, K_GEMM_FC1, K_GEMM_FC1_L, K_GEMM_FC2, K_GEMM_FC2_L,
-  K_SELECT, K_DECODER_INPUT, K_FILL, K_NCLASS
+  K_SELECT, K_DECODER_INPUT, K_FILL, K_ATTN2_W1, K_ATTN2_W2, K_ATTN2_W4, K_CONCAT, K_NCLASS
 };
 const char *const kClassNames[K_NCLASS] = {
     "row_map",       "gather_ln",      "gemm_qkv_t128", "gemm_qkv_t256", "attention_q32",
     "attention_q64", "attention_q128", "attn_scores",   "gemm_o_t128",   "gemm_o_t256",
     "gemm_fc1_t128", "gemm_fc1_t256",  "gemm_fc2_t128", "gemm_fc2_t256", "select_topk",
-    "decoder_input", "fill_zero"};
+    "decoder_input", "fill_zero",      "attention2_q32", "attention2_q64", "attention2_q128",
+    "concat_kv"};
 
 int attn_class(int a_max) { return a_max <= 32 ? K_ATTN_W1 : (a_max <= 64 ? K_ATTN_W2 : K_ATTN_W4); }
 
@@ -364,6 +365,89 @@ marche_status_t select_refresh_ordered(const float *scores, int32_t n_parts,
   LAUNCH(K_SELECT, 0, 4.0 * batch * n_parts * n_tokens,
          launch_select_topk(scores, n_parts, excl_idx, excl_off, batch, n_tokens, k, out_idx,
                             out_off, order == MARCHE_SELECT_LOWEST, stream));
+  return MARCHE_OK;
+}
+
+size_t marche_attention_workspace_bytes(int32_t batch, int32_t n_heads, int32_t head_dim,
+                                         int32_t n_a, int32_t n_c, int32_t dtype, int32_t mode) {
+  if (mode != MARCHE_ATTN_CONCAT || batch <= 0 || n_heads <= 0 || head_dim <= 0 || n_a < 0 ||
+      n_c < 0)
+    return 0;
+  const size_t es = dtype == MARCHE_BF16 ? 2 : 4;
+  const size_t one = (size_t)batch * n_heads * (size_t)(n_a + n_c) * head_dim * es;
+  return 2 * ((one + 255) & ~(size_t)255);
+}
+
+marche_status_t marche_attention_segments(const void *q, void *o, int32_t n_query,
+                                          const void *k_a, const void *v_a, int32_t n_a,
+                                          const void *k_c, const void *v_c, int32_t n_c,
+                                          int32_t batch, int32_t n_heads, int32_t head_dim,
+                                          int32_t dtype, int32_t mode, void *workspace,
+                                          size_t workspace_bytes, marche_stream_t stream_) {
+  if (mode != MARCHE_ATTN_TWO_SEGMENT && mode != MARCHE_ATTN_CONCAT)
+    return fail(MARCHE_ERR_INVALID_ARG, "mode=%d is not TWO_SEGMENT or CONCAT", mode);
+  if (dtype != MARCHE_BF16)
+    return fail(MARCHE_ERR_UNSUPPORTED, "dtype=%d (segment attention is bf16 only)", dtype);
+  if (head_dim != 64 && head_dim != 80)
+    return fail(MARCHE_ERR_UNSUPPORTED, "head_dim=%d (supported: 64, 80)", head_dim);
+  if (batch < 0 || n_heads < 1 || (int64_t)batch * n_heads > 65535)
+    return fail(MARCHE_ERR_INVALID_ARG, "batch=%d / n_heads=%d out of range (batch*n_heads <= 65535)",
+                batch, n_heads);
+  if (n_query < 1 || n_query > 4096)
+    return fail(MARCHE_ERR_INVALID_ARG, "n_query=%d outside [1, 4096]", n_query);
+  if (n_a < 0 || n_c < 0 || n_a + n_c < 1 || n_a + n_c > 65536)
+    return fail(MARCHE_ERR_INVALID_ARG, "segment lengths n_a=%d, n_c=%d (each >= 0, sum in [1, 65536])",
+                n_a, n_c);
+  const int64_t d_model = (int64_t)n_heads * head_dim;
+  if ((int64_t)batch * n_query * d_model >= (1LL << 31) ||
+      (int64_t)batch * n_heads * (n_a + n_c) * head_dim >= (1LL << 31))
+    return fail(MARCHE_ERR_UNSUPPORTED, "buffers reach 2^31 elements");
+  if (batch == 0) return MARCHE_OK;
+  if (!q || !o || (n_a > 0 && (!k_a || !v_a)) || (n_c > 0 && (!k_c || !v_c)))
+    return fail(MARCHE_ERR_INVALID_ARG, "NULL query, output or non-empty segment");
+  for (const void *p : {q, (const void *)o, k_a, v_a, k_c, v_c})
+    if (reinterpret_cast<uintptr_t>(p) & 15)
+      return fail(MARCHE_ERR_INVALID_ARG, "q, o and the segment buffers must be 16-byte aligned");
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  const int cls_w = n_query <= 32 ? 0 : (n_query <= 64 ? 1 : 2);
+  const int32_t nt = n_a + n_c;
+  const double flops = 4.0 * batch * n_query * (double)nt * d_model;
+  // Algorithmic traffic of attention: q, every K/V row of both segments and o once.
+  const double attn_bytes =
+      2.0 * (2.0 * batch * n_query * d_model + 2.0 * batch * (double)nt * d_model);
+  AttnArgs aa{q, k_a, v_a, o, nullptr, nullptr, batch, n_heads, n_a, head_dim,
+              (int32_t)d_model, batch * n_query, n_query};
+  if (mode == MARCHE_ATTN_TWO_SEGMENT) {
+    if (n_a == 0) {  // only the cached segment
+      aa.k_cache = k_c;
+      aa.v_cache = v_c;
+      aa.n_tokens = n_c;
+    } else if (n_c > 0) {
+      aa.k2 = k_c;
+      aa.v2 = v_c;
+      aa.n2 = n_c;
+    }
+    LAUNCH((n_a > 0 && n_c > 0 ? K_ATTN2_W1 : K_ATTN_W1) + cls_w, flops, attn_bytes,
+           launch_attention(DType::BF16, aa, stream));
+    return MARCHE_OK;
+  }
+  const size_t need =
+      marche_attention_workspace_bytes(batch, n_heads, head_dim, n_a, n_c, dtype, mode);
+  if (!workspace || workspace_bytes < need)
+    return fail(MARCHE_ERR_WORKSPACE, "workspace %s: %zu bytes < %zu needed",
+                workspace ? "too small" : "is NULL", workspace_bytes, need);
+  if (reinterpret_cast<uintptr_t>(workspace) & 255)
+    return fail(MARCHE_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  char *kcat = static_cast<char *>(workspace);
+  char *vcat = kcat + need / 2;
+  LAUNCH(K_CONCAT, 0, 2.0 * 2.0 * 2.0 * batch * (double)nt * d_model,
+         launch_concat_kv(DType::BF16, kcat, vcat, n_a ? k_a : k_c, n_a ? v_a : v_c,
+                          n_c ? k_c : k_a, n_c ? v_c : v_a, batch * n_heads, n_a, n_c, head_dim,
+                          stream));
+  aa.k_cache = kcat;
+  aa.v_cache = vcat;
+  aa.n_tokens = nt;
+  LAUNCH(K_ATTN_W1 + cls_w, flops, attn_bytes, launch_attention(DType::BF16, aa, stream));
   return MARCHE_OK;
 }
 

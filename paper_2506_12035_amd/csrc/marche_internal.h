@@ -66,14 +66,24 @@ int device_cu_count();
 // ---- attention (k_attn.hip) ----
 struct AttnArgs {
   const void *q;        // [a_total][D] packed queries
-  const void *k_cache;  // layer base [B][H][N][dh]
+  const void *k_cache;  // layer base [B][H][N][dh] (keys 0..N-1; the first segment)
   const void *v_cache;
   void *o;              // [a_total][D]
-  const int32_t *a_off;
+  const int32_t *a_off; // CSR rows per image; NULL: image b owns rows [b*a_max, (b+1)*a_max)
   const RowMap *map;
   int32_t batch, n_heads, n_tokens, head_dim, d_model, a_total, a_max;
+  // Optional second key/value segment [B][H][n2][dh], attended after the
+  // first in the same online-softmax pass (bf16 attention only).
+  const void *k2 = nullptr;
+  const void *v2 = nullptr;
+  int32_t n2 = 0;
 };
 hipError_t launch_attention(DType dt, const AttnArgs &a, hipStream_t s);
+// dst[b][h] = [a[b][h] (na rows) ; c[b][h] (nc rows)], rows of dh elements, for
+// K and V: the concatenation of the active and cached segments.
+hipError_t launch_concat_kv(DType dt, void *k_dst, void *v_dst, const void *k_a, const void *v_a,
+                            const void *k_c, const void *v_c, int32_t bh, int32_t na, int32_t nc,
+                            int32_t head_dim, hipStream_t s);
 // scores[b][h][j] = sum over the first n_gen[b] active rows i of P_h[i][j]
 hipError_t launch_attn_scores(DType dt, const AttnArgs &a, const int32_t *n_gen, int32_t gen_max,
                               float *scores, hipStream_t s);

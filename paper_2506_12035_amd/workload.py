@@ -250,3 +250,33 @@ def random_refresh(cfg: Config, t: int, candidates: np.ndarray, k: int) -> np.nd
     for b in range(candidates.shape[0]):
         out[b] = np.sort(rng.choice(candidates[b], size=k, replace=False))
     return out
+
+
+@dataclass
+class SegmentCase:
+    """Inputs of the two-segment attention comparison (Appendix B): queries of
+    the active rows and the keys/values of the active and cached segments.
+
+    ``q`` [B][n_active][H*d_h]; ``k_a``/``v_a`` [B][H][n_active][d_h];
+    ``k_c``/``v_c`` [B][H][n_cached][d_h]; all ~ N(0, 1) rounded to bf16.
+    """
+
+    q: np.ndarray
+    k_a: np.ndarray
+    v_a: np.ndarray
+    k_c: np.ndarray
+    v_c: np.ndarray
+
+
+def segment_case(batch: int, n_heads: int, head_dim: int, n_active: int, n_cached: int,
+                 seed: int = SEED_BASE + 100) -> SegmentCase:
+    rng = streams(seed)[STREAM_STATE]
+    D = n_heads * head_dim
+
+    def draw(*shape):
+        return round_to(rng.standard_normal(shape, dtype=np.float32), "bf16")
+
+    return SegmentCase(draw(batch, n_active, D), draw(batch, n_heads, n_active, head_dim),
+                       draw(batch, n_heads, n_active, head_dim),
+                       draw(batch, n_heads, n_cached, head_dim),
+                       draw(batch, n_heads, n_cached, head_dim))

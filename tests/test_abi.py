@@ -148,3 +148,33 @@ def test_profile_entry_bounds():
     binding.profile_reset()
     assert binding.lib().marche_profile_entry(-1, None, None, None, None, None) == binding.MARCHE_ERR_INVALID_ARG
     assert binding.profile_collect() == {}
+
+
+def test_attention_segments_validation_and_workspace():
+    L = binding.lib()
+    bf16, f32 = binding.MARCHE_BF16, binding.MARCHE_F32
+    two, cat = binding.MARCHE_ATTN_TWO_SEGMENT, binding.MARCHE_ATTN_CONCAT
+
+    def call(mode=two, dtype=bf16, head_dim=64, n_query=32, n_a=32, n_c=256, batch=2, ws=None,
+             ws_bytes=0, q=FAKE, k_c=FAKE):
+        return L.marche_attention_segments(q, FAKE, n_query, FAKE, FAKE, n_a, k_c, k_c, n_c, batch,
+                                           16, head_dim, dtype, mode, ws, ws_bytes, None)
+
+    assert call(mode=2) == binding.MARCHE_ERR_INVALID_ARG
+    assert "mode" in binding.last_error()
+    assert call(dtype=f32) == binding.MARCHE_ERR_UNSUPPORTED
+    assert call(head_dim=96) == binding.MARCHE_ERR_UNSUPPORTED
+    assert call(n_query=0) == binding.MARCHE_ERR_INVALID_ARG
+    assert call(n_a=0, n_c=0) == binding.MARCHE_ERR_INVALID_ARG
+    assert call(n_c=-1) == binding.MARCHE_ERR_INVALID_ARG
+    assert call(q=None) == binding.MARCHE_ERR_INVALID_ARG
+    assert call(k_c=None) == binding.MARCHE_ERR_INVALID_ARG
+    assert call(q=FAKE + 8) == binding.MARCHE_ERR_INVALID_ARG
+    assert call(batch=0) == binding.MARCHE_OK
+    need = binding.attention_workspace_bytes(2, 16, 64, 32, 256, bf16, cat)
+    one = 2 * 16 * (32 + 256) * 64 * 2
+    assert need == 2 * ((one + 255) // 256 * 256)
+    assert binding.attention_workspace_bytes(2, 16, 64, 32, 256, bf16, two) == 0
+    assert call(mode=cat) == binding.MARCHE_ERR_WORKSPACE
+    assert call(mode=cat, ws=FAKE, ws_bytes=need - 1) == binding.MARCHE_ERR_WORKSPACE
+    assert call(mode=cat, ws=FAKE + 16, ws_bytes=need) == binding.MARCHE_ERR_INVALID_ARG
