@@ -28,12 +28,10 @@ namespace marche {
 // consecutive columns never straddle a q|k|v third or a head (d_model and
 // head_dim are multiples of 4).
 //
-// The write-back runs in three phases so that no load waits behind a store
-// (on this architecture the vector-memory counter also counts stores):
-//   row(r)            per-row addressing data (may load the row map),
-//   bias(col0)        the bias of four columns,
-//   prior(row, col0)  the value the result is added to (residual epilogues),
-// all issued before the first store(row, r, col0, v), v = acc + bias + prior.
+// The write-back issues every load (row addressing data, biases, residual
+// priors) before the stores it feeds: on this architecture the vector-memory
+// counter also counts stores, so a load issued after a store would wait for
+// the store's acknowledgement.
 
 template <typename T>
 __device__ __forceinline__ void store4(T *p, f32x4 v) {
@@ -49,6 +47,12 @@ __device__ __forceinline__ f32x4 load_bias4(const float *bias, int col0) {
   return *reinterpret_cast<const f32x4 *>(bias + col0);
 }
 
+// Epilogue interface: row(r) per-row addressing data (may load the row map);
+// col(c0) per-column addressing data for the four columns c0..c0+3, computed
+// once per lane where the columns of a lane are fixed; bias4(c0); prior(row,
+// col) the value the result is added to (residual epilogues); store(row, r,
+// col, v) with v = acc + bias + prior.
+
 template <typename T>
 struct EpiQkv {
   static constexpr bool kPrior = false;
@@ -59,23 +63,30 @@ struct EpiQkv {
   const RowMap *map;
   int d_model, head_dim, n_heads, n_tokens;
   using Row = RowMap;
-  __device__ __forceinline__ Row row(int r) const { return map[r]; }
-  __device__ __forceinline__ f32x4 bias4(int col0) const { return load_bias4(bias, col0); }
-  __device__ __forceinline__ f32x4 prior(const Row &, int) const { return f32x4{}; }
   // 32-bit element offsets: the host limits every buffer to < 2^31 elements.
-  __device__ __forceinline__ void store(const Row &m, int r, int col0, f32x4 v) const {
-    if (col0 < d_model) {
-      store4(q + (uint32_t)(r * d_model + col0), v);
-      return;
-    }
-    int c = col0 - d_model;
+  struct Col {
+    T *base;       // q, or the K or V cache of the layer
+    uint32_t off;  // column offset: c0 for q, h*n_tokens*head_dim + d for K/V
+    bool is_q;
+  };
+  __device__ __forceinline__ Row row(int r) const { return map[r]; }
+  __device__ __forceinline__ Col col(int c0) const {
+    if (c0 < d_model) return Col{q, (uint32_t)c0, true};
+    int c = c0 - d_model;
     T *dst = kc;
     if (c >= d_model) {
       c -= d_model;
       dst = vc;
     }
     const int h = c / head_dim, d = c - h * head_dim;
-    store4(dst + (uint32_t)(((m.b * n_heads + h) * n_tokens + m.tok) * head_dim + d), v);
+    return Col{dst, (uint32_t)(h * n_tokens * head_dim + d), false};
+  }
+  __device__ __forceinline__ f32x4 bias4(int c0) const { return load_bias4(bias, c0); }
+  __device__ __forceinline__ f32x4 prior(const Row &, const Col &) const { return f32x4{}; }
+  __device__ __forceinline__ void store(const Row &m, int r, const Col &c, f32x4 v) const {
+    const uint32_t row_off = c.is_q ? (uint32_t)(r * d_model)
+                                    : (uint32_t)((m.b * n_heads * n_tokens + m.tok) * head_dim);
+    store4(c.base + row_off + c.off, v);
   }
 };
 
@@ -89,13 +100,15 @@ struct EpiResid {
   const RowMap *map;
   int n;
   using Row = int32_t;  // element offset of the residual-stream row (< 2^31)
+  using Col = int32_t;
   __device__ __forceinline__ Row row(int r) const { return map[r].x_row * n; }
-  __device__ __forceinline__ f32x4 bias4(int col0) const { return load_bias4(bias, col0); }
-  __device__ __forceinline__ f32x4 prior(const Row &xr, int col0) const {
-    return *reinterpret_cast<const f32x4 *>(x + (uint32_t)(xr + col0));
+  __device__ __forceinline__ Col col(int c0) const { return c0; }
+  __device__ __forceinline__ f32x4 bias4(int c0) const { return load_bias4(bias, c0); }
+  __device__ __forceinline__ f32x4 prior(const Row &xr, const Col &c) const {
+    return *reinterpret_cast<const f32x4 *>(x + (uint32_t)(xr + c));
   }
-  __device__ __forceinline__ void store(const Row &xr, int, int col0, f32x4 v) const {
-    *reinterpret_cast<f32x4 *>(x + (uint32_t)(xr + col0)) = v;
+  __device__ __forceinline__ void store(const Row &xr, int, const Col &c, f32x4 v) const {
+    *reinterpret_cast<f32x4 *>(x + (uint32_t)(xr + c)) = v;
   }
 };
 
@@ -106,12 +119,14 @@ struct EpiGelu {
   const float *bias;
   int n;
   using Row = int32_t;
+  using Col = int32_t;
   __device__ __forceinline__ Row row(int r) const { return r; }
-  __device__ __forceinline__ f32x4 bias4(int col0) const { return load_bias4(bias, col0); }
-  __device__ __forceinline__ f32x4 prior(const Row &, int) const { return f32x4{}; }
-  __device__ __forceinline__ void store(const Row &, int r, int col0, f32x4 v) const {
+  __device__ __forceinline__ Col col(int c0) const { return c0; }
+  __device__ __forceinline__ f32x4 bias4(int c0) const { return load_bias4(bias, c0); }
+  __device__ __forceinline__ f32x4 prior(const Row &, const Col &) const { return f32x4{}; }
+  __device__ __forceinline__ void store(const Row &, int r, const Col &c, f32x4 v) const {
     f32x4 g = {gelu_erf(v[0]), gelu_erf(v[1]), gelu_erf(v[2]), gelu_erf(v[3])};
-    store4(h + (uint32_t)(r * n + col0), g);
+    store4(h + (uint32_t)(r * n + c), g);
   }
 };
 
@@ -147,6 +162,11 @@ __device__ __forceinline__ void write_back(const f32x16 (&acc)[TN][TM], const Ep
 #pragma unroll
       for (int g = 0; g < 4; ++g) b[j][g] = epi.bias4(col_base + j * 32 + g * 8 + (lane >> 5) * 4);
   }
+  typename Epi::Col cinfo[TN][4];
+#pragma unroll
+  for (int j = 0; j < TN; ++j)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) cinfo[j][g] = epi.col(col_base + j * 32 + g * 8 + (lane >> 5) * 4);
   auto bias_of = [&](int j, int g) -> f32x4 {
     if constexpr (BIAS_LDS)
       return *reinterpret_cast<const f32x4 *>(bias_lds + j * 32 + g * 8 + (lane >> 5) * 4);
@@ -166,9 +186,7 @@ __device__ __forceinline__ void write_back(const f32x16 (&acc)[TN][TM], const Ep
       for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int g = 0; g < 4; ++g)
-          dst[ii][j][g] = Epi::kPrior ? epi.prior(rinfo[bi * IB + ii],
-                                                  col_base + j * 32 + g * 8 + (lane >> 5) * 4)
-                                      : f32x4{};
+          dst[ii][j][g] = Epi::kPrior ? epi.prior(rinfo[bi * IB + ii], cinfo[j][g]) : f32x4{};
   };
   load_priors(0, pr[0]);
 #pragma unroll
@@ -194,8 +212,7 @@ __device__ __forceinline__ void write_back(const f32x16 (&acc)[TN][TM], const Ep
         for (int g = 0; g < 4; ++g) {
           const f32x4 a = {acc[j][i][4 * g + 0], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2],
                            acc[j][i][4 * g + 3]};
-          epi.store(rinfo[i], row, col_base + j * 32 + g * 8 + (lane >> 5) * 4,
-                    a + bias_of(j, g) + pr[bi & 1][ii][j][g]);
+          epi.store(rinfo[i], row, cinfo[j][g], a + bias_of(j, g) + pr[bi & 1][ii][j][g]);
         }
     }
   }
@@ -453,11 +470,81 @@ __device__ __forceinline__ void barrier() {
 
 }  // namespace big
 
+// Write-back of the 256x256 tile through LDS (free once the main loop is
+// done).  In the accumulator layout a store instruction would write 16 bytes
+// into each of 32 rows; instead each wavefront writes one 32-row block of its
+// 128x128 accumulators to LDS as fp32 and reads it back row-major, so lane l
+// owns columns 4 (l % 32) .. + 3 of rows l / 32 + 2k: one store instruction
+// then covers two whole 128-column row segments.  Biases and per-row
+// addressing data of the tile were staged in LDS by the caller; residual
+// priors of the next block are loaded before this block's stores.
+namespace big {
+constexpr int kWbStride = 132;  // floats per staged row (128 + 4: no bank conflicts)
+static_assert(4 * 32 * kWbStride * 4 <= 2 * kStage, "staged write-back fits the stages");
+}  // namespace big
+
+// `side` holds the tile's 256 biases (floats [0, 256)) followed by its 256 row
+// records; both were loaded into LDS during the prologue.
+template <class Epi>
+__device__ __forceinline__ void write_back_staged(const f32x16 (&acc)[4][4], const Epi &epi, int m0,
+                                                  int n0, int wm, int wn, int M, int lane, int wave,
+                                                  unsigned char *smem, const unsigned char *side) {
+  using namespace big;
+  using Row = typename Epi::Row;
+  float *st = reinterpret_cast<float *>(smem) + wave * 32 * kWbStride;
+  const Row *rows = reinterpret_cast<const Row *>(side + 1024) + wm * 128;
+  const int c4 = (lane & 31) * 4, half = lane >> 5;
+  const typename Epi::Col col = epi.col(n0 + wn * 128 + c4);
+  const f32x4 b = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(side) +
+                                                    wn * 128 + c4);
+  f32x4 pr[2][16];  // residual priors; zero for epilogues without one
+#pragma unroll
+  for (int k = 0; k < 16; ++k) pr[0][k] = pr[1][k] = f32x4{};
+  auto load_priors = [&](int i, f32x4 (&dst)[16]) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+      dst[k] = Epi::kPrior ? epi.prior(rows[i * 32 + half + 2 * k], col) : f32x4{};
+  };
+  if constexpr (Epi::kPrior) load_priors(0, pr[0]);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    // block row i of the accumulators -> LDS rows 0..31 of this wavefront
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<f32x4 *>(st + (lane & 31) * kWbStride + j * 32 + g * 8 + half * 4) =
+            f32x4{acc[j][i][4 * g + 0], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2],
+                  acc[j][i][4 * g + 3]};
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    f32x4 v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+      v[k] = *reinterpret_cast<const f32x4 *>(st + (half + 2 * k) * kWbStride + c4);
+    if constexpr (Epi::kPrior) {
+      if (i + 1 < 4) load_priors(i + 1, pr[(i + 1) & 1]);
+#pragma unroll
+      for (int k = 0; k < 16; ++k) keep(pr[i & 1][k]);
+    }
+    const int rbase = m0 + wm * 128 + i * 32;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int r = half + 2 * k;
+      if (rbase + r < M) epi.store(rows[i * 32 + r], rbase + r, col, v[k] + b + pr[i & 1][k]);
+    }
+    // this block's reads of the staging rows are done before the next block
+    // overwrites them
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  }
+}
+
 template <class Epi>
 __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, const bf16 *W, int M,
                                                                int N, int K, Epi epi) {
   using namespace big;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * kStage];
+  // biases and row records of the tile for the write-back (5 KB)
+  __shared__ __attribute__((aligned(16))) unsigned char side[1024 + 256 * sizeof(typename Epi::Row)];
   const int tiles_m = (M + 255) / 256, tiles_n = N / 256;
   int tm, tn;
   tile_coords(xcd_remap(blockIdx.x, gridDim.x), tiles_m, tiles_n, tm, tn);
@@ -475,6 +562,10 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
   // k-tile 0 into stage 0; the first quarter of k-tile 1 into stage 1
 #pragma unroll
   for (int p = 0; p < 16; ++p) load_lds(smem, q0 + p, A, W, M, K, m0, n0, 0, lane);
+  // the write-back's biases and row records, loaded while the tile computes
+  if (tid < 64)
+    *reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(side) + tid * 4) = epi.bias4(n0 + tid * 4);
+  reinterpret_cast<typename Epi::Row *>(side + 1024)[tid] = epi.row(min(m0 + tid, M - 1));
   barrier();
   Frag fa, fb;
 #pragma unroll
@@ -543,15 +634,11 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
       }
     }
   }
-  // the last quarter-tile loads (a clamped repeat of the final k-tile) land,
-  // every wavefront is done with the stages; then the tile's 256 biases go
-  // to LDS for the write-back
+  // the last quarter-tile loads (a clamped repeat of the final k-tile) land
+  // and every wavefront is done with the stages before they hold the
+  // write-back's staging rows
   barrier();
-  float *bias_lds = reinterpret_cast<float *>(smem);
-  if (tid < 64)
-    *reinterpret_cast<f32x4 *>(bias_lds + tid * 4) = epi.bias4(n0 + tid * 4);
-  __syncthreads();
-  write_back<4, 4, true>(acc, epi, m0 + wm * 128, n0 + wn * 128, M, lane, bias_lds + wn * 128);
+  write_back_staged(acc, epi, m0, n0, wm, wn, M, lane, wave, smem, side);
 }
 
 // The 256x256 tile is chosen when its tiles fill the compute units in whole
@@ -620,13 +707,14 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float *__restrict__
     __syncthreads();
   }
   const f32x4 b = epi.bias4(n0 + tx * 4);
+  const typename Epi::Col c = epi.col(n0 + tx * 4);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = m0 + ty * 4 + i;
     if (row >= M) continue;
     const typename Epi::Row r = epi.row(row);
     const f32x4 v = {acc[i][0], acc[i][1], acc[i][2], acc[i][3]};
-    epi.store(r, row, n0 + tx * 4, v + b + (Epi::kPrior ? epi.prior(r, n0 + tx * 4) : f32x4{}));
+    epi.store(r, row, c, v + b + (Epi::kPrior ? epi.prior(r, c) : f32x4{}));
   }
 }
 
