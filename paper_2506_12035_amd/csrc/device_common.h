@@ -22,23 +22,24 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-// erf(u) for u >= 0 by the rational approximation of Abramowitz & Stegun
-// 7.1.26 (after Hastings): erf(u) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5))))
-// exp(-u^2) with t = 1 / (1 + p u), absolute error below 1.5e-7 for every
-// u >= 0.  Branch-free: one reciprocal, one exp2, five FMAs.
-__device__ __forceinline__ float erf_nonneg(float u) {
-  constexpr float p = 0.3275911f, a1 = 0.254829592f, a2 = -0.284496736f, a3 = 1.421413741f,
-                  a4 = -1.453152027f, a5 = 1.061405429f;
-  const float t = __builtin_amdgcn_rcpf(fmaf(p, u, 1.0f));
-  const float poly = t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, a5, a4), a3), a2), a1);
-  const float e = __builtin_amdgcn_exp2f(-(u * u) * 1.4426950408889634f);
-  return 1.0f - poly * e;
-}
-
-// Exact-erf GELU: z * Phi(z) = z (1 + erf(z / sqrt 2)) / 2, erf odd.
+// Exact-erf GELU, z * Phi(z), written as max(z, 0) - |z| * Phi(-|z|) (the two
+// agree for either sign of z), with the upper tail of the normal distribution
+// from the rational approximation of Abramowitz & Stegun 7.1.26 (after
+// Hastings): for a >= 0,
+//   Phi(-a) = (1 - erf(a / sqrt 2)) / 2 = t (c1 + t (c2 + t (c3 + t (c4 + t c5)))) exp(-a^2 / 2),
+//   t = 1 / (1 + p a / sqrt 2), c_i = a_i / 2,
+// absolute error of erf below 1.5e-7.  Branch-free: one reciprocal, one exp2,
+// about ten other operations.
 __device__ __forceinline__ float gelu_erf(float z) {
-  const float e = erf_nonneg(fabsf(z) * 0.70710678118654752f);
-  return 0.5f * z * (1.0f + copysignf(e, z));
+  constexpr float p_s = 0.3275911f * 0.70710678118654752f;  // p / sqrt 2
+  constexpr float c1 = 0.5f * 0.254829592f, c2 = 0.5f * -0.284496736f, c3 = 0.5f * 1.421413741f,
+                  c4 = 0.5f * -1.453152027f, c5 = 0.5f * 1.061405429f;
+  constexpr float h = -0.5f * 1.4426950408889634f;  // -log2(e) / 2
+  const float a = fabsf(z);
+  const float t = __builtin_amdgcn_rcpf(fmaf(p_s, a, 1.0f));
+  const float poly = t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, c5, c4), c3), c2), c1);
+  const float e = __builtin_amdgcn_exp2f(a * (a * h));
+  return fmaf(-a, poly * e, fmaxf(z, 0.0f));
 }
 
 template <typename T>

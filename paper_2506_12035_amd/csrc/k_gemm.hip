@@ -527,10 +527,22 @@ __device__ __forceinline__ void write_back_staged(const f32x16 (&acc)[4][4], con
       for (int k = 0; k < 16; ++k) keep(pr[i & 1][k]);
     }
     const int rbase = m0 + wm * 128 + i * 32;
+    auto value = [&](int k) -> f32x4 {
+      if constexpr (Epi::kPrior) return v[k] + b + pr[i & 1][k];
+      else return v[k] + b;
+    };
+    if (rbase + 32 <= M) {  // the whole block exists: no per-row guard
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const int r = half + 2 * k;
-      if (rbase + r < M) epi.store(rows[i * 32 + r], rbase + r, col, v[k] + b + pr[i & 1][k]);
+      for (int k = 0; k < 16; ++k) {
+        const int r = half + 2 * k;
+        epi.store(rows[i * 32 + r], rbase + r, col, value(k));
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const int r = half + 2 * k;
+        if (rbase + r < M) epi.store(rows[i * 32 + r], rbase + r, col, value(k));
+      }
     }
     // this block's reads of the staging rows are done before the next block
     // overwrites them
