@@ -425,7 +425,9 @@ __device__ __forceinline__ int swz(int r, int kc) { return kc ^ ((r >> 1) & 7); 
 // carries activation rows 8q..8q+7, q >= 32 weight rows 8(q-32)..; lane l
 // writes LDS bytes [16 l, 16 l + 16) of the block, i.e. row 8q + l / 8 at
 // physical chunk l % 8, which holds logical chunk swz(row, l % 8).
-__device__ __forceinline__ void load_lds(unsigned char *stage, int q, const bf16 *A, const bf16 *W,
+// `stage` is the LDS byte address of the stage (wave-uniform, so M0 is set
+// from a scalar register).
+__device__ __forceinline__ void load_lds(unsigned stage, int q, const bf16 *A, const bf16 *W,
                                          int M, int K, int m0, int n0, int k0, int lane) {
   const int rr = lane >> 3, pc = lane & 7;
   const bf16 *g;
@@ -436,10 +438,9 @@ __device__ __forceinline__ void load_lds(unsigned char *stage, int q, const bf16
     const int r = (q - 32) * 8 + rr;
     g = W + (size_t)(n0 + r) * K + k0 + swz(r, pc) * 8;
   }
-  const unsigned lds = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void *)(stage + q * 1024);
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
                :
-               : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds))
+               : "v"(g), "s"(__builtin_amdgcn_readfirstlane(stage + q * 1024))
                : "memory", "m0");
 }
 
@@ -561,9 +562,12 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
   int tm, tn;
   tile_coords(xcd_remap(blockIdx.x, gridDim.x), tiles_m, tiles_n, tm, tn);
   const int m0 = tm * 256, n0 = tn * 256;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar address math
   const int wm = wave >> 1, wn = wave & 1;
   const int q0 = wave * 16;  // this wavefront's load instructions q0 .. q0 + 15
+  const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void *)smem;
+  const unsigned lds_stage[2] = {lds0, lds0 + kStage};
   f32x16 acc[4][4];
 #pragma unroll
   for (int j = 0; j < 4; ++j)
@@ -573,7 +577,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
 
   // k-tile 0 into stage 0; the first quarter of k-tile 1 into stage 1
 #pragma unroll
-  for (int p = 0; p < 16; ++p) load_lds(smem, q0 + p, A, W, M, K, m0, n0, 0, lane);
+  for (int p = 0; p < 16; ++p) load_lds(lds_stage[0], q0 + p, A, W, M, K, m0, n0, 0, lane);
   // the write-back's biases and row records, loaded while the tile computes
   if (tid < 64)
     *reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(side) + tid * 4) = epi.bias4(n0 + tid * 4);
@@ -586,7 +590,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
     const int k1 = min(1, nk - 1) * 64;
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
-      load_lds(smem + kStage, q0 + p, A, W, M, K, m0, n0, k1, lane);
+      load_lds(lds_stage[1], q0 + p, A, W, M, K, m0, n0, k1, lane);
       pin();
     }
   }
@@ -594,7 +598,8 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
   for (int kt = 0; kt + 1 < nk; ++kt) {
     const int cur = kt & 1;
     const unsigned char *sc = smem + cur * kStage;
-    unsigned char *sn = smem + (cur ^ 1) * kStage;
+    const unsigned char *sn = smem + (cur ^ 1) * kStage;
+    const unsigned ln = lds_stage[cur ^ 1], lc = lds_stage[cur];
     const int k1 = (kt + 1) * 64, k2 = min(kt + 2, nk - 1) * 64;
     // k16 steps 0..2: fragments of the next step; the rest of k-tile kt+1
 #pragma unroll
@@ -605,8 +610,8 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
       for (int q = 0; q < 16; ++q) {
         mfma(acc, fc, q);
         if (q < 8) read_frag(fn, q, sc, st + 1, wm, wn, lane);
-        else if (st == 0) load_lds(sn, q0 + 4 + (q - 8), A, W, M, K, m0, n0, k1, lane);
-        else if (st == 1 && q < 12) load_lds(sn, q0 + 12 + (q - 8), A, W, M, K, m0, n0, k1, lane);
+        else if (st == 0) load_lds(ln, q0 + 4 + (q - 8), A, W, M, K, m0, n0, k1, lane);
+        else if (st == 1 && q < 12) load_lds(ln, q0 + 12 + (q - 8), A, W, M, K, m0, n0, k1, lane);
         pin();
       }
     }
@@ -628,7 +633,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
 #pragma unroll
     for (int q = 12; q < 16; ++q) {
       mfma(acc, fb, q);
-      load_lds(smem + cur * kStage, q0 + (q - 12), A, W, M, K, m0, n0, k2, lane);
+      load_lds(lc, q0 + (q - 12), A, W, M, K, m0, n0, k2, lane);
       pin();
     }
   }
