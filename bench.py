@@ -86,6 +86,8 @@ def counter_class(name: str):
                          ("EpiResid<0>", "o"), ("EpiGelu", "fc1"), ("EpiQkv", "qkv")):
             if key in name:
                 return f"gemm_{cls}_{tile}"
+    if "attn_resident_kernel" in name:
+        return "attention_res"
     if "attn_mfma_kernel" in name:
         for nw, q in (("4", "q128"), ("2", "q64"), ("1", "q32")):
             if f"ELi{nw}EEEv" in name or f", {nw}>(" in name:

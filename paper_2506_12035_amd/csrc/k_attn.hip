@@ -37,6 +37,100 @@ __device__ __forceinline__ int vperm16(int k) {
   return (k & 3) | (((k >> 3) & 1) << 2) | (((k >> 2) & 1) << 3);
 }
 
+// One 64-key tile of the online softmax for one wavefront's 32 queries.
+// ks: the tile's K rows in LDS (row stride DH + 8); vt: its transposed V
+// (row stride TK + 8, keys of each 16-key group permuted by vperm16); t0: the
+// tile's first key within a segment of ns keys.  Updates the running maximum,
+// sum and the O^T accumulators (log2 domain; sl2 = log2(e) / sqrt(d_h)).
+// Element offsets inside one tile's K and V^T blocks.  Padded layout: rows of
+// DH + 8 (K) and TK + 8 (V^T) elements.  Swizzled layout (DH = 64 only): rows
+// of 64 elements whose 16-byte chunks are permuted by an XOR with the row
+// pair index, so 16 consecutive rows read at one chunk hit distinct banks
+// without padding (8 KB per tile for K and for V^T).
+template <int DH, bool SWZ>
+__device__ __forceinline__ int k_off(int key, int d) {
+  if constexpr (SWZ) return key * 64 + ((((d >> 3) ^ (key >> 1)) & 7) << 3) + (d & 7);
+  else return key * (DH + 8) + d;
+}
+template <int DH, bool SWZ>
+__device__ __forceinline__ int vt_off(int row, int pos) {
+  if constexpr (SWZ) return row * 64 + ((((pos >> 3) ^ (row >> 1)) & 7) << 3) + (pos & 7);
+  else return row * (TK + 8) + pos;
+}
+
+template <int DH, bool SWZ = false>
+__device__ __forceinline__ void attn_tile(const bf16 *ks, const bf16 *vt, const bf16x8 (&qf)[DH / 16],
+                                          f32x16 (&acc)[(DH + 31) / 32], float &m_run, float &l_run,
+                                          int t0, int ns, float sl2, int lane) {
+  static_assert(!SWZ || DH == 64, "swizzled tiles hold 64-element rows");
+  constexpr int QS = DH / 16, ODB = (DH + 31) / 32;
+  // S^T for two 32-key blocks: lane -> query (lane & 31),
+  // register r -> key (r / 4) * 8 + (lane / 32) * 4 + r % 4 of the block.
+  f32x16 s[2];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    s[kb] = f32x16{};
+#pragma unroll
+    for (int st = 0; st < QS; ++st) {
+      const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(
+          &ks[k_off<DH, SWZ>(kb * 32 + (lane & 31), st * 16 + (lane >> 5) * 8)]);
+      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[st], s[kb], 0, 0, 0);
+    }
+  }
+  float mx = -INFINITY;
+  if (t0 + TK <= ns) {  // every key of the tile exists
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        s[kb][r] *= sl2;
+        mx = fmaxf(mx, s[kb][r]);
+      }
+  } else {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = t0 + kb * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        const float v = key < ns ? s[kb][r] * sl2 : -INFINITY;
+        s[kb][r] = v;
+        mx = fmaxf(mx, v);
+      }
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  const float m_new = fmaxf(m_run, mx);
+  const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+  float psum = 0.f;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float p = __builtin_amdgcn_exp2f(s[kb][r] - m_new);
+      s[kb][r] = p;
+      psum += p;
+    }
+  l_run = l_run * alpha + psum;
+  m_run = m_new;
+#pragma unroll
+  for (int d = 0; d < ODB; ++d) acc[d] *= alpha;
+
+  // O^T += V^T P^T over the 64 keys of the tile, 16 keys per MFMA.
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      bf16x8 pb;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pb[e] = (bf16)s[kb][8 * u + e];
+#pragma unroll
+      for (int d = 0; d < ODB; ++d) {
+        const bf16x8 va = *reinterpret_cast<const bf16x8 *>(
+            &vt[vt_off<DH, SWZ>(d * 32 + (lane & 31), kb * 32 + 16 * u + (lane >> 5) * 8)]);
+        acc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, acc[d], 0, 0, 0);
+      }
+    }
+}
+
 template <int DH, int NW, bool SEG2 = false>
 __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chunks) {
   constexpr int NT = NW * 64;
@@ -169,73 +263,7 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
     }
     const bool more = t + 1 < ntiles;
     if (more) gload(t + 1);
-
-    // S^T for two 32-key blocks: lane -> query (lane & 31),
-    // register r -> key (r / 4) * 8 + (lane / 32) * 4 + r % 4 of the block.
-    f32x16 s[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      s[kb] = f32x16{};
-#pragma unroll
-      for (int st = 0; st < QS; ++st) {
-        const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(
-            &Ks[cur][(kb * 32 + (lane & 31)) * KS + st * 16 + (lane >> 5) * 8]);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[st], s[kb], 0, 0, 0);
-      }
-    }
-    float mx = -INFINITY;
-    if (t0 + TK <= ns) {  // every key of the tile exists
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          s[kb][r] *= sl2;
-          mx = fmaxf(mx, s[kb][r]);
-        }
-    } else {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = t0 + kb * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-          const float v = key < ns ? s[kb][r] * sl2 : -INFINITY;
-          s[kb][r] = v;
-          mx = fmaxf(mx, v);
-        }
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    float psum = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = __builtin_amdgcn_exp2f(s[kb][r] - m_new);
-        s[kb][r] = p;
-        psum += p;
-      }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int d = 0; d < ODB; ++d) acc[d] *= alpha;
-
-    // O^T += V^T P^T over the 64 keys of the tile, 16 keys per MFMA.
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        bf16x8 pb;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pb[e] = (bf16)s[kb][8 * u + e];
-#pragma unroll
-        for (int d = 0; d < ODB; ++d) {
-          const bf16x8 va = *reinterpret_cast<const bf16x8 *>(
-              &Vt[cur][(d * 32 + (lane & 31)) * VS + kb * 32 + 16 * u + (lane >> 5) * 8]);
-          acc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, acc[d], 0, 0, 0);
-        }
-      }
-
+    attn_tile<DH>(Ks[cur], Vt[cur], qf, acc, m_run, l_run, t0, ns, sl2, lane);
     if (more) sstore(cur ^ 1);
     __syncthreads();
   }
@@ -258,6 +286,148 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
   }
 }
 
+// Every query of an image in one workgroup and every key resident in LDS
+// (layers where all N <= NTL * 64 tokens are active): one workgroup per
+// (image, head); wavefront w owns the NQB 32-query blocks w, w + NW, ...  All
+// K/V tiles are loaded at once (registers, then LDS: one memory latency per
+// workgroup instead of one per tile) and read once per (image, head), after
+// which each wavefront runs the online softmax over the resident tiles with
+// no further loads or barriers.  With SWZ (head width 64) the tiles take
+// 80 KB, so two workgroups share a CU and one's loads overlap the other's
+// arithmetic.
+template <int DH, int NW, int NTL, int NQB, bool SWZ>
+__global__ __launch_bounds__(NW * 64) void attn_resident_kernel(AttnArgs a) {
+  constexpr int NT = NW * 64;
+  constexpr int ODB = (DH + 31) / 32;
+  constexpr int DHV = ODB * 32;
+  constexpr int KT = SWZ ? TK * 64 : TK * (DH + 8);     // elements per K tile
+  constexpr int VT = SWZ ? DHV * 64 : DHV * (TK + 8);   // elements per V^T tile
+  constexpr int CPR = DH / 8;
+  constexpr int TCH = TK * CPR;
+  constexpr int LPT = (TCH + NT - 1) / NT;
+  constexpr int VPCH = TCH / 2;
+  constexpr int LPV = (VPCH + NT - 1) / NT;
+  constexpr int QS = DH / 16;
+  __shared__ __attribute__((aligned(16))) bf16 Ks[NTL][KT];
+  __shared__ __attribute__((aligned(16))) bf16 Vt[NTL][VT];
+
+  const int bh = xcd_remap(blockIdx.x, gridDim.x);
+  const int b = bh / a.n_heads, h = bh - b * a.n_heads;
+  const int r0 = a.a_off ? a.a_off[b] : b * a.a_max;
+  const int na = a.a_off ? a.a_off[b + 1] - r0 : a.a_max;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int N = a.n_tokens, D = a.d_model;
+  const int ntiles = (N + TK - 1) / TK;  // <= NTL (host-checked)
+  const bf16 *kg = static_cast<const bf16 *>(a.k_cache) + (size_t)(b * a.n_heads + h) * N * DH;
+  const bf16 *vg = static_cast<const bf16 *>(a.v_cache) + (size_t)(b * a.n_heads + h) * N * DH;
+
+  if constexpr (DHV > DH) {  // V^T rows past DH (padding to a multiple of 32) hold zeros
+    for (int i = tid; i < NTL * (DHV - DH) * (TK + 8); i += NT) {
+      const int t = i / ((DHV - DH) * (TK + 8)), rem = i % ((DHV - DH) * (TK + 8));
+      Vt[t][DH * (TK + 8) + rem] = (bf16)0.0f;
+    }
+  }
+  // all tiles' loads first, then all LDS writes
+  u32x4 rk[NTL][LPT], rv0[NTL][LPV], rv1[NTL][LPV];
+#pragma unroll
+  for (int t = 0; t < NTL; ++t) {
+    if (t >= ntiles) break;
+    const int t0 = t * TK;
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+      const int c = i * NT + tid;
+      if (c < TCH) {
+        const int key = min(t0 + c / CPR, N - 1), d = (c % CPR) * 8;
+        rk[t][i] = *reinterpret_cast<const u32x4 *>(kg + (size_t)key * DH + d);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < LPV; ++i) {
+      const int c = i * NT + tid;
+      if (c < VPCH) {
+        const int kp = c / CPR, d = (c % CPR) * 8;
+        const int k0 = min(t0 + 2 * kp, N - 1), k1 = min(t0 + 2 * kp + 1, N - 1);
+        rv0[t][i] = *reinterpret_cast<const u32x4 *>(vg + (size_t)k0 * DH + d);
+        rv1[t][i] = *reinterpret_cast<const u32x4 *>(vg + (size_t)k1 * DH + d);
+      }
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < NTL; ++t) {
+    if (t >= ntiles) break;
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+      const int c = i * NT + tid;
+      if (c < TCH) {
+        const int key = c / CPR, d = (c % CPR) * 8;
+        *reinterpret_cast<u32x4 *>(&Ks[t][k_off<DH, SWZ>(key, d)]) = rk[t][i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < LPV; ++i) {
+      const int c = i * NT + tid;
+      if (c < VPCH) {
+        const int kp = c / CPR, d = (c % CPR) * 8;
+        const int pos = ((2 * kp) & ~15) | vperm16((2 * kp) & 15);  // even: a 32-bit pair
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const unsigned w0 = rv0[t][i][e >> 1], w1 = rv1[t][i][e >> 1];
+          const unsigned lo = (e & 1) ? (w0 >> 16) : (w0 & 0xFFFFu);
+          const unsigned hi = (e & 1) ? (w1 & 0xFFFF0000u) : (w1 << 16);
+          *reinterpret_cast<unsigned *>(&Vt[t][vt_off<DH, SWZ>(d + e, pos)]) = lo | hi;
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  const float sl2 = 1.4426950408889634f / sqrtf((float)DH);
+#pragma unroll 1
+  for (int qb = 0; qb < NQB; ++qb) {
+    const int wq0 = (qb * NW + wave) * 32;
+    if (wq0 >= na) break;  // uniform over the wavefront; no barrier follows
+    const int qi = wq0 + (lane & 31);
+    const bf16 *qrow = static_cast<const bf16 *>(a.q) + (size_t)(r0 + min(qi, na - 1)) * D + h * DH;
+    bf16x8 qf[QS];
+#pragma unroll
+    for (int st = 0; st < QS; ++st)
+      qf[st] = *reinterpret_cast<const bf16x8 *>(qrow + st * 16 + (lane >> 5) * 8);
+    float m_run = -INFINITY, l_run = 0.f;
+    f32x16 acc[ODB];
+#pragma unroll
+    for (int d = 0; d < ODB; ++d) acc[d] = f32x16{};
+    for (int t = 0; t < ntiles; ++t)
+      attn_tile<DH, SWZ>(Ks[t], Vt[t], qf, acc, m_run, l_run, t * TK, N, sl2, lane);
+
+    const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+    const float inv = 1.0f / l_tot;
+    if (qi < na) {
+      bf16 *orow = static_cast<bf16 *>(a.o) + (size_t)(r0 + qi) * D + h * DH;
+#pragma unroll
+      for (int d = 0; d < ODB; ++d)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int dh0 = d * 32 + g * 8 + (lane >> 5) * 4;
+          if (dh0 < DH) {
+            bf16x4 pk = {(bf16)(acc[d][4 * g + 0] * inv), (bf16)(acc[d][4 * g + 1] * inv),
+                         (bf16)(acc[d][4 * g + 2] * inv), (bf16)(acc[d][4 * g + 3] * inv)};
+            *reinterpret_cast<bf16x4 *>(orow + dh0) = pk;
+          }
+        }
+    }
+  }
+}
+
+constexpr int RES_NTL = 5;    // keys resident: 320
+constexpr int RES_QMAX = 320; // queries per workgroup
+
+// Host choice of the resident kernel: more than 64 active queries per image
+// (where the streaming kernel needs several workgroups per (image, head)), all
+// of them and all keys within one workgroup's reach, one key segment.
+bool attn_resident(int32_t a_max, int32_t n_tokens, bool two_segments) {
+  return !two_segments && a_max > 64 && a_max <= RES_QMAX && n_tokens <= RES_NTL * TK;
+}
+
 template <int DH, int NW, bool SEG2>
 static hipError_t run_attn_mfma(const AttnArgs &a, hipStream_t s) {
   const int chunks = (a.a_max + NW * 32 - 1) / (NW * 32);
@@ -276,6 +446,13 @@ static hipError_t attn_bf16_nw(const AttnArgs &a, hipStream_t s) {
 template <int DH>
 static hipError_t attn_bf16_dispatch(const AttnArgs &a, hipStream_t s) {
   if (a.k2) return attn_bf16_nw<DH, true>(a, s);
+  if (attn_resident(a.a_max, a.n_tokens, a.k2 != nullptr)) {
+    if constexpr (DH == 64)  // 80 KB of swizzled tiles: two workgroups per CU
+      attn_resident_kernel<DH, 4, RES_NTL, 3, true><<<a.batch * a.n_heads, 4 * 64, 0, s>>>(a);
+    else
+      attn_resident_kernel<DH, 10, RES_NTL, 1, false><<<a.batch * a.n_heads, 10 * 64, 0, s>>>(a);
+    return hipGetLastError();
+  }
   return attn_bf16_nw<DH, false>(a, s);
 }
 

@@ -86,16 +86,20 @@ marche_status_t check_model(const marche_model_t *m) {
 enum KClass {
   K_ROW_MAP, K_GATHER_LN, K_GEMM_QKV, K_GEMM_QKV_L, K_ATTN_W1, K_ATTN_W2, K_ATTN_W4,
   K_ATTN_SCORES, K_GEMM_O, K_GEMM_O_L, K_GEMM_FC1, K_GEMM_FC1_L, K_GEMM_FC2, K_GEMM_FC2_L,
-  K_SELECT, K_DECODER_INPUT, K_FILL, K_ATTN2_W1, K_ATTN2_W2, K_ATTN2_W4, K_CONCAT, K_NCLASS
+  K_SELECT, K_DECODER_INPUT, K_FILL, K_ATTN2_W1, K_ATTN2_W2, K_ATTN2_W4, K_CONCAT, K_ATTN_RES,
+  K_NCLASS
 };
 const char *const kClassNames[K_NCLASS] = {
     "row_map",       "gather_ln",      "gemm_qkv_t128", "gemm_qkv_t256", "attention_q32",
     "attention_q64", "attention_q128", "attn_scores",   "gemm_o_t128",   "gemm_o_t256",
     "gemm_fc1_t128", "gemm_fc1_t256",  "gemm_fc2_t128", "gemm_fc2_t256", "select_topk",
     "decoder_input", "fill_zero",      "attention2_q32", "attention2_q64", "attention2_q128",
-    "concat_kv"};
+    "concat_kv",     "attention_res"};
 
-int attn_class(int a_max) { return a_max <= 32 ? K_ATTN_W1 : (a_max <= 64 ? K_ATTN_W2 : K_ATTN_W4); }
+int attn_class(DType dt, int a_max, int n_tokens) {
+  if (dt == DType::BF16 && attn_resident(a_max, n_tokens, false)) return K_ATTN_RES;
+  return a_max <= 32 ? K_ATTN_W1 : (a_max <= 64 ? K_ATTN_W2 : K_ATTN_W4);
+}
 
 struct Pending {
   int cls;
@@ -311,7 +315,7 @@ marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layer
     AttnArgs aa{buf1, kc, vc, buf0, a_off, map, batch, H, N, dh, D, M, a_max};
     // Algorithmic traffic: every cached K/V element of the batch read once,
     // plus the queries read and the outputs written.
-    LAUNCH(attn_class(a_max), 4.0 * M * N * D, es * (2.0 * batch * N * D + 2.0 * M * D),
+    LAUNCH(attn_class(dt, a_max, N), 4.0 * M * N * D, es * (2.0 * batch * N * D + 2.0 * M * D),
            launch_attention(dt, aa, stream));
     if (want_scores && l == score_layer) {
       LAUNCH(K_ATTN_SCORES, 2.0 * batch * gen_max * N * D,
@@ -427,8 +431,9 @@ marche_status_t marche_attention_segments(const void *q, void *o, int32_t n_quer
       aa.v2 = v_c;
       aa.n2 = n_c;
     }
-    LAUNCH((n_a > 0 && n_c > 0 ? K_ATTN2_W1 : K_ATTN_W1) + cls_w, flops, attn_bytes,
-           launch_attention(DType::BF16, aa, stream));
+    const int cls = (n_a > 0 && n_c > 0) ? K_ATTN2_W1 + cls_w
+                                         : attn_class(DType::BF16, n_query, aa.n_tokens);
+    LAUNCH(cls, flops, attn_bytes, launch_attention(DType::BF16, aa, stream));
     return MARCHE_OK;
   }
   const size_t need =
@@ -447,7 +452,8 @@ marche_status_t marche_attention_segments(const void *q, void *o, int32_t n_quer
   aa.k_cache = kcat;
   aa.v_cache = vcat;
   aa.n_tokens = nt;
-  LAUNCH(K_ATTN_W1 + cls_w, flops, attn_bytes, launch_attention(DType::BF16, aa, stream));
+  LAUNCH(attn_class(DType::BF16, n_query, nt), flops, attn_bytes,
+         launch_attention(DType::BF16, aa, stream));
   return MARCHE_OK;
 }
 

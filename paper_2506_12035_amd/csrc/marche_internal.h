@@ -79,6 +79,9 @@ struct AttnArgs {
   int32_t n2 = 0;
 };
 hipError_t launch_attention(DType dt, const AttnArgs &a, hipStream_t s);
+// Whether bf16 attention with these sizes runs the resident-K/V kernel (one
+// workgroup per (image, head)).
+bool attn_resident(int32_t a_max, int32_t n_tokens, bool two_segments);
 // dst[b][h] = [a[b][h] (na rows) ; c[b][h] (nc rows)], rows of dh elements, for
 // K and V: the concatenation of the active and cached segments.
 hipError_t launch_concat_kv(DType dt, void *k_dst, void *v_dst, const void *k_a, const void *v_a,
