@@ -80,7 +80,7 @@ def traffic_for(kernel: str, workload: str):
 
 def counter_class(name: str):
     """Timing class of a kernel symbol as rocprofv3 prints it (mangled or not)."""
-    tile = "t256" if "gemm_bf16_big_kernel" in name else "t128"
+    tile = "t256" if "gemm_bf16_big_kernel" in name else "t128x256"
     if "gemm_bf16" in name:
         for key, cls in (("EpiResidILi1E", "fc2"), ("EpiResid<1>", "fc2"), ("EpiResidILi0E", "o"),
                          ("EpiResid<0>", "o"), ("EpiGelu", "fc1"), ("EpiQkv", "qkv")):

@@ -9,12 +9,11 @@
 //   - adds into the float32 residual stream row     (output projection, fc2)
 //   - applies exact GELU and stores the hidden row  (fc1)
 //
-// bf16 path: workgroup tile BM x BN x BK, a grid of wavefronts each owning a
-// block of 32x32 MFMA tiles (v_mfma_f32_32x32x16_bf16, fp32 accumulators).
-// Tiles are staged global -> registers -> LDS (double-buffered LDS, one or
-// two k-tiles of register prefetch).  LDS rows are padded by 16 bytes, which
-// makes the 16-byte MFMA operand reads (32 rows at one k offset) bank-conflict
-// free.
+// bf16 path (v_mfma_f32_32x32x16_bf16, fp32 accumulators): a 256x256 tile on
+// four wavefronts (one workgroup per CU) for shapes that fill the chip in
+// whole waves, else a 128x256 tile of which two workgroups share a CU.  Both
+// load operands straight from global memory into XOR-swizzled LDS stages and
+// write back through LDS in row-major order.
 //
 // fp32 path: plain FMA, 64x64 tiles, 4x4 outputs per thread.
 #include "device_common.h"
@@ -138,86 +137,6 @@ __device__ __forceinline__ void keep(const RowMap &m) {
   asm volatile("" ::"v"(m.x_row), "v"(m.b), "v"(m.tok));
 }
 
-// Write-back of one wavefront's TM x TN block of 32x32 accumulators (C^T
-// layout: lane l owns output row l & 31 of each block and, in register group g,
-// columns g * 8 + (l / 32) * 4 .. + 3).  Rows at or beyond M are clamped for
-// the loads and skipped for the stores.  Residual priors are loaded for IB
-// block rows at a time (at most 16 four-column groups, 64 registers), each
-// batch's loads issued before the previous batch's stores.
-//
-// With BIAS_LDS, the biases of the block's columns come from LDS
-// (bias_lds[c - col_base] for column c; the caller staged them there), which
-// keeps them out of registers and off the vector-memory counter.
-template <int TM, int TN, bool BIAS_LDS = false, class Epi>
-__device__ __forceinline__ void write_back(const f32x16 (&acc)[TN][TM], const Epi &epi, int row0,
-                                           int col_base, int M, int lane,
-                                           const float *bias_lds = nullptr) {
-  typename Epi::Row rinfo[TM];
-#pragma unroll
-  for (int i = 0; i < TM; ++i) rinfo[i] = epi.row(min(row0 + i * 32 + (lane & 31), M - 1));
-  f32x4 b[BIAS_LDS ? 1 : TN][4];
-  if constexpr (!BIAS_LDS) {
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) b[j][g] = epi.bias4(col_base + j * 32 + g * 8 + (lane >> 5) * 4);
-  }
-  typename Epi::Col cinfo[TN][4];
-#pragma unroll
-  for (int j = 0; j < TN; ++j)
-#pragma unroll
-    for (int g = 0; g < 4; ++g) cinfo[j][g] = epi.col(col_base + j * 32 + g * 8 + (lane >> 5) * 4);
-  auto bias_of = [&](int j, int g) -> f32x4 {
-    if constexpr (BIAS_LDS)
-      return *reinterpret_cast<const f32x4 *>(bias_lds + j * 32 + g * 8 + (lane >> 5) * 4);
-    else
-      return b[j][g];
-  };
-#pragma unroll
-  for (int i = 0; i < TM; ++i) keep(rinfo[i]);
-  constexpr int IB = (16 / (TN * 4)) < 1 ? 1 : ((16 / (TN * 4)) > TM ? TM : 16 / (TN * 4));
-  constexpr int NB = TM / IB;
-  static_assert(TM % IB == 0, "prior batches");
-  f32x4 pr[2][IB][TN][4];
-  auto load_priors = [&](int bi, f32x4 (&dst)[IB][TN][4]) {
-#pragma unroll
-    for (int ii = 0; ii < IB; ++ii)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int g = 0; g < 4; ++g)
-          dst[ii][j][g] = Epi::kPrior ? epi.prior(rinfo[bi * IB + ii], cinfo[j][g]) : f32x4{};
-  };
-  load_priors(0, pr[0]);
-#pragma unroll
-  for (int bi = 0; bi < NB; ++bi) {
-    // the next batch's loads go out before this batch's stores
-    if (bi + 1 < NB) load_priors(bi + 1, pr[(bi + 1) & 1]);
-    if constexpr (Epi::kPrior) {
-#pragma unroll
-      for (int ii = 0; ii < IB; ++ii)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-          for (int g = 0; g < 4; ++g) keep(pr[bi & 1][ii][j][g]);
-    }
-#pragma unroll
-    for (int ii = 0; ii < IB; ++ii) {
-      const int i = bi * IB + ii;
-      const int row = row0 + i * 32 + (lane & 31);
-      if (row >= M) continue;
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x4 a = {acc[j][i][4 * g + 0], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2],
-                           acc[j][i][4 * g + 3]};
-          epi.store(rinfo[i], row, cinfo[j][g], a + bias_of(j, g) + pr[bi & 1][ii][j][g]);
-        }
-    }
-  }
-}
-
 // ------------------------------------------------------------------ bf16 MFMA
 //
 // The MFMA A operand is a 32-row slice of W (output columns) and the B
@@ -226,23 +145,6 @@ __device__ __forceinline__ void write_back(const f32x16 (&acc)[TN][TM], const Ep
 // register r, output column (r / 4) * 8 + (l / 32) * 4 + r % 4 -- four
 // consecutive columns per group of four registers, which the epilogue stores
 // together.
-
-template <int BM_, int BN_, int BK_, int WGM_, int WGN_, int PF_, int MINB_>
-struct TileCfg {
-  static constexpr int BM = BM_, BN = BN_, BK = BK_;
-  static constexpr int WGM = WGM_, WGN = WGN_;  // wavefront grid
-  static constexpr int PF = PF_;                // k-tiles staged in registers ahead
-  static constexpr int MINB = MINB_;            // workgroups per CU to budget registers for
-  static constexpr int NT = WGM * WGN * 64;
-  static constexpr int WM = BM / WGM, WN = BN / WGN;
-  static constexpr int TM = WM / 32, TN = WN / 32;
-  static constexpr int LS = BK + 8;             // LDS row stride (elements): +16 bytes
-  static constexpr int CPR = BK / 8;            // 16-byte chunks per tile row
-  static constexpr int A_CHUNKS = BM * CPR / NT;
-  static constexpr int B_CHUNKS = BN * CPR / NT;
-  static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile not divisible");
-  static_assert(2 * (BM + BN) * LS * 2 <= 160 * 1024, "LDS budget");
-};
 
 // Grouped tile order: GROUP consecutive tile rows sweep all tile columns
 // together, so concurrently running workgroups share A rows and W columns.
@@ -255,144 +157,6 @@ __device__ __forceinline__ void tile_coords(int id, int tiles_m, int tiles_n, in
   const int in = id - g * per_group;
   tm = first_m + in % gm;
   tn = in / gm;
-}
-
-template <class C>
-struct Stage {
-  u32x4 a[C::A_CHUNKS];
-  u32x4 b[C::B_CHUNKS];
-};
-
-template <class C>
-__device__ __forceinline__ void stage_load(Stage<C> &st, const bf16 *__restrict__ A,
-                                           const bf16 *__restrict__ W, int M, int K, int m0,
-                                           int n0, int k0, int tid) {
-#pragma unroll
-  for (int i = 0; i < C::A_CHUNKS; ++i) {
-    const int c = i * C::NT + tid, row = c / C::CPR, col = (c % C::CPR) * 8;
-    st.a[i] = *reinterpret_cast<const u32x4 *>(A + (size_t)min(m0 + row, M - 1) * K + k0 + col);
-  }
-#pragma unroll
-  for (int i = 0; i < C::B_CHUNKS; ++i) {
-    const int c = i * C::NT + tid, row = c / C::CPR, col = (c % C::CPR) * 8;
-    st.b[i] = *reinterpret_cast<const u32x4 *>(W + (size_t)(n0 + row) * K + k0 + col);
-  }
-}
-
-template <class C>
-__device__ __forceinline__ void stage_store(const Stage<C> &st, bf16 *As, bf16 *Bs, int tid) {
-#pragma unroll
-  for (int i = 0; i < C::A_CHUNKS; ++i) {
-    const int c = i * C::NT + tid, row = c / C::CPR, col = (c % C::CPR) * 8;
-    *reinterpret_cast<u32x4 *>(&As[row * C::LS + col]) = st.a[i];
-  }
-#pragma unroll
-  for (int i = 0; i < C::B_CHUNKS; ++i) {
-    const int c = i * C::NT + tid, row = c / C::CPR, col = (c % C::CPR) * 8;
-    *reinterpret_cast<u32x4 *>(&Bs[row * C::LS + col]) = st.b[i];
-  }
-}
-
-// One BK-deep slab of MFMAs for this wavefront's block of 32x32 tiles.
-template <class C>
-__device__ __forceinline__ void tile_mfma(f32x16 (&acc)[C::TN][C::TM], const bf16 *As,
-                                          const bf16 *Bs, int wm, int wn, int lane) {
-  const int lrow = lane & 31, lk = (lane >> 5) * 8;
-#pragma unroll
-  for (int kk = 0; kk < C::BK; kk += 16) {
-    bf16x8 af[C::TM], bw[C::TN];
-#pragma unroll
-    for (int i = 0; i < C::TM; ++i)
-      af[i] = *reinterpret_cast<const bf16x8 *>(&As[(wm * C::WM + i * 32 + lrow) * C::LS + kk + lk]);
-#pragma unroll
-    for (int j = 0; j < C::TN; ++j)
-      bw[j] = *reinterpret_cast<const bf16x8 *>(&Bs[(wn * C::WN + j * 32 + lrow) * C::LS + kk + lk]);
-#pragma unroll
-    for (int j = 0; j < C::TN; ++j)
-#pragma unroll
-      for (int i = 0; i < C::TM; ++i)
-        acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bw[j], af[i], acc[j][i], 0, 0, 0);
-  }
-}
-
-template <class C, class Epi>
-__global__ __launch_bounds__(C::NT, C::MINB) void gemm_bf16_kernel(const bf16 *__restrict__ A,
-                                                                   const bf16 *__restrict__ W,
-                                                                   int M, int N, int K, Epi epi) {
-  __shared__ __attribute__((aligned(16))) bf16 As[2][C::BM * C::LS];
-  __shared__ __attribute__((aligned(16))) bf16 Bs[2][C::BN * C::LS];
-  const int tiles_m = (M + C::BM - 1) / C::BM, tiles_n = N / C::BN;
-  int tm, tn;
-  tile_coords(xcd_remap(blockIdx.x, gridDim.x), tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * C::BM, n0 = tn * C::BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / C::WGN, wn = wave % C::WGN;
-  f32x16 acc[C::TN][C::TM];
-#pragma unroll
-  for (int j = 0; j < C::TN; ++j)
-#pragma unroll
-    for (int i = 0; i < C::TM; ++i) acc[j][i] = f32x16{};
-
-  const int nk = K / C::BK;
-  if constexpr (C::PF == 1) {
-    // k-tile t+1 is loaded into registers while k-tile t is multiplied, then
-    // written to the other LDS buffer.
-    Stage<C> st;
-    stage_load<C>(st, A, W, M, K, m0, n0, 0, tid);
-    stage_store<C>(st, As[0], Bs[0], tid);
-    __syncthreads();
-    for (int kt = 0; kt + 1 < nk; ++kt) {
-      const int cur = kt & 1;
-      stage_load<C>(st, A, W, M, K, m0, n0, (kt + 1) * C::BK, tid);
-      tile_mfma<C>(acc, As[cur], Bs[cur], wm, wn, lane);
-      stage_store<C>(st, As[cur ^ 1], Bs[cur ^ 1], tid);
-      __syncthreads();
-    }
-    tile_mfma<C>(acc, As[(nk - 1) & 1], Bs[(nk - 1) & 1], wm, wn, lane);
-  } else {
-    // Two register stages: k-tile t+2 is loaded while k-tile t is multiplied
-    // and k-tile t+1 (loaded one iteration earlier) goes to LDS after it, so
-    // every load has two iterations to land.
-    Stage<C> s0, s1;
-    stage_load<C>(s0, A, W, M, K, m0, n0, 0, tid);
-    if (nk > 1) stage_load<C>(s1, A, W, M, K, m0, n0, C::BK, tid);
-    stage_store<C>(s0, As[0], Bs[0], tid);
-    __syncthreads();
-    int kt = 0;
-    for (; kt + 2 < nk; kt += 2) {
-      stage_load<C>(s0, A, W, M, K, m0, n0, (kt + 2) * C::BK, tid);
-      tile_mfma<C>(acc, As[0], Bs[0], wm, wn, lane);
-      stage_store<C>(s1, As[1], Bs[1], tid);
-      __syncthreads();
-      if (kt + 3 < nk) stage_load<C>(s1, A, W, M, K, m0, n0, (kt + 3) * C::BK, tid);
-      tile_mfma<C>(acc, As[1], Bs[1], wm, wn, lane);
-      stage_store<C>(s0, As[0], Bs[0], tid);
-      __syncthreads();
-    }
-    if (kt + 1 < nk) {  // two k-tiles left: buffer 0 holds kt, s1 holds kt + 1
-      tile_mfma<C>(acc, As[0], Bs[0], wm, wn, lane);
-      stage_store<C>(s1, As[1], Bs[1], tid);
-      __syncthreads();
-      tile_mfma<C>(acc, As[1], Bs[1], wm, wn, lane);
-    } else {
-      tile_mfma<C>(acc, As[0], Bs[0], wm, wn, lane);
-    }
-  }
-
-  write_back<C::TM, C::TN>(acc, epi, m0 + wm * C::WM, n0 + wn * C::WN, M, lane);
-}
-
-// 128x128 tile, 2x2 wavefronts of 64x64, two register stages, registers
-// budgeted for two workgroups per CU.
-using TileS = TileCfg<128, 128, 64, 2, 2, 2, 2>;
-
-template <class C, class Epi>
-static hipError_t launch_tile(const void *a, const void *w, int m, int n, int k, const Epi &epi,
-                              hipStream_t s) {
-  const int grid = ((m + C::BM - 1) / C::BM) * (n / C::BN);
-  gemm_bf16_kernel<C, Epi><<<grid, C::NT, 0, s>>>(static_cast<const bf16 *>(a),
-                                                  static_cast<const bf16 *>(w), m, n, k, epi);
-  return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ 256x256 tile
@@ -471,44 +235,47 @@ __device__ __forceinline__ void barrier() {
 
 }  // namespace big
 
-// Write-back of the 256x256 tile through LDS (free once the main loop is
-// done).  In the accumulator layout a store instruction would write 16 bytes
-// into each of 32 rows; instead each wavefront writes one 32-row block of its
-// 128x128 accumulators to LDS as fp32 and reads it back row-major, so lane l
+// Write-back through LDS (free once the main loop is done).  In the
+// accumulator layout a store instruction would write 16 bytes into each of
+// 32 rows; instead each wavefront writes one 32-row block of its accumulators
+// (128 columns wide) to LDS as fp32 and reads it back row-major, so lane l
 // owns columns 4 (l % 32) .. + 3 of rows l / 32 + 2k: one store instruction
-// then covers two whole 128-column row segments.  Biases and per-row
-// addressing data of the tile were staged in LDS by the caller; residual
-// priors of the next block are loaded before this block's stores.
+// then covers two whole 128-column row segments.  Per-row addressing data of
+// the tile were staged in LDS by the caller; residual priors of the next
+// batch of rows are loaded before this batch's stores.
 namespace big {
 constexpr int kWbStride = 132;  // floats per staged row (128 + 4: no bank conflicts)
 static_assert(4 * 32 * kWbStride * 4 <= 2 * kStage, "staged write-back fits the stages");
 }  // namespace big
 
-// `side` holds the tile's 256 biases (floats [0, 256)) followed by its 256 row
-// records; both were loaded into LDS during the prologue.
-template <class Epi>
-__device__ __forceinline__ void write_back_staged(const f32x16 (&acc)[4][4], const Epi &epi, int m0,
-                                                  int n0, int wm, int wn, int M, int lane, int wave,
-                                                  unsigned char *smem, const unsigned char *side) {
+// One wavefront's TM 32-row blocks of 128 columns (accumulators acc[j][i]:
+// column block j, row block i) starting at output row row0 and column col0.
+// `st` is this wavefront's staging area (32 rows of kWbStride floats), `rows`
+// the row records of rows row0.. (in LDS), `b` the bias of this lane's four
+// columns col0 + 4 (lane % 32) .. + 3.  Residual priors are loaded PB rows at
+// a time, each batch before the stores of the previous one.
+template <int TM, int PB, class Epi>
+__device__ __forceinline__ void write_back_staged(const f32x16 (&acc)[4][TM], const Epi &epi,
+                                                  int row0, int col0, int M, int lane, float *st,
+                                                  const typename Epi::Row *rows, f32x4 b) {
   using namespace big;
-  using Row = typename Epi::Row;
-  float *st = reinterpret_cast<float *>(smem) + wave * 32 * kWbStride;
-  const Row *rows = reinterpret_cast<const Row *>(side + 1024) + wm * 128;
+  static_assert(16 % PB == 0, "prior batches");
+  constexpr int NB = 16 / PB;  // batches per 32-row block
   const int c4 = (lane & 31) * 4, half = lane >> 5;
-  const typename Epi::Col col = epi.col(n0 + wn * 128 + c4);
-  const f32x4 b = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(side) +
-                                                    wn * 128 + c4);
-  f32x4 pr[2][16];  // residual priors; zero for epilogues without one
+  const typename Epi::Col col = epi.col(col0 + c4);
+  f32x4 pr[2][PB];  // residual priors; zero for epilogues without one
 #pragma unroll
-  for (int k = 0; k < 16; ++k) pr[0][k] = pr[1][k] = f32x4{};
-  auto load_priors = [&](int i, f32x4 (&dst)[16]) {
+  for (int k = 0; k < PB; ++k) pr[0][k] = pr[1][k] = f32x4{};
+  // batch u: block u / NB, rows half + 2 k for k in [(u % NB) PB, + PB)
+  auto load_priors = [&](int u, f32x4 (&dst)[PB]) {
+    const int i = u / NB, k0 = (u % NB) * PB;
 #pragma unroll
-    for (int k = 0; k < 16; ++k)
-      dst[k] = Epi::kPrior ? epi.prior(rows[i * 32 + half + 2 * k], col) : f32x4{};
+    for (int k = 0; k < PB; ++k)
+      dst[k] = Epi::kPrior ? epi.prior(rows[i * 32 + half + 2 * (k0 + k)], col) : f32x4{};
   };
   if constexpr (Epi::kPrior) load_priors(0, pr[0]);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < TM; ++i) {
     // block row i of the accumulators -> LDS rows 0..31 of this wavefront
 #pragma unroll
     for (int j = 0; j < 4; ++j)
@@ -518,31 +285,36 @@ __device__ __forceinline__ void write_back_staged(const f32x16 (&acc)[4][4], con
             f32x4{acc[j][i][4 * g + 0], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2],
                   acc[j][i][4 * g + 3]};
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    f32x4 v[16];
+    const int rbase = row0 + i * 32;
+    const bool full = rbase + 32 <= M;  // the whole block exists: no per-row guard
 #pragma unroll
-    for (int k = 0; k < 16; ++k)
-      v[k] = *reinterpret_cast<const f32x4 *>(st + (half + 2 * k) * kWbStride + c4);
-    if constexpr (Epi::kPrior) {
-      if (i + 1 < 4) load_priors(i + 1, pr[(i + 1) & 1]);
+    for (int nb = 0; nb < NB; ++nb) {
+      const int u = i * NB + nb;
+      f32x4 v[PB];
 #pragma unroll
-      for (int k = 0; k < 16; ++k) keep(pr[i & 1][k]);
-    }
-    const int rbase = m0 + wm * 128 + i * 32;
-    auto value = [&](int k) -> f32x4 {
-      if constexpr (Epi::kPrior) return v[k] + b + pr[i & 1][k];
-      else return v[k] + b;
-    };
-    if (rbase + 32 <= M) {  // the whole block exists: no per-row guard
+      for (int k = 0; k < PB; ++k)
+        v[k] = *reinterpret_cast<const f32x4 *>(st + (half + 2 * (nb * PB + k)) * kWbStride + c4);
+      if constexpr (Epi::kPrior) {
+        if (u + 1 < TM * NB) load_priors(u + 1, pr[(u + 1) & 1]);
 #pragma unroll
-      for (int k = 0; k < 16; ++k) {
-        const int r = half + 2 * k;
-        epi.store(rows[i * 32 + r], rbase + r, col, value(k));
+        for (int k = 0; k < PB; ++k) keep(pr[u & 1][k]);
       }
-    } else {
+      auto value = [&](int k) -> f32x4 {
+        if constexpr (Epi::kPrior) return v[k] + b + pr[u & 1][k];
+        else return v[k] + b;
+      };
+      if (full) {
 #pragma unroll
-      for (int k = 0; k < 16; ++k) {
-        const int r = half + 2 * k;
-        if (rbase + r < M) epi.store(rows[i * 32 + r], rbase + r, col, value(k));
+        for (int k = 0; k < PB; ++k) {
+          const int r = half + 2 * (nb * PB + k);
+          epi.store(rows[i * 32 + r], rbase + r, col, value(k));
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < PB; ++k) {
+          const int r = half + 2 * (nb * PB + k);
+          if (rbase + r < M) epi.store(rows[i * 32 + r], rbase + r, col, value(k));
+        }
       }
     }
     // this block's reads of the staging rows are done before the next block
@@ -655,37 +427,230 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
   // and every wavefront is done with the stages before they hold the
   // write-back's staging rows
   barrier();
-  write_back_staged(acc, epi, m0, n0, wm, wn, M, lane, wave, smem, side);
+  const f32x4 b = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(side) +
+                                                    wn * 128 + (lane & 31) * 4);
+  write_back_staged<4, 16>(acc, epi, m0 + wm * 128, n0 + wn * 128, M, lane,
+                           reinterpret_cast<float *>(smem) + wave * 32 * kWbStride,
+                           reinterpret_cast<const typename Epi::Row *>(side + 1024) + wm * 128, b);
 }
 
-// The 256x256 tile is chosen when its tiles fill the compute units in whole
-// waves well enough: at least 90% of the last wave, or 80% when K >= 2048
-// (the longer main loop amortises the tile's fixed start and write-back).
-// Otherwise the 128x128 tile, two workgroups per CU, fills the chip in finer
-// steps.  Measured at MAR-L sizes: full-step QKV, fc1 and fc2 and
-// cache-aware QKV take the large tile; the output projection and the other
-// cache-aware GEMMs the small one.
-bool gemm_large_tile(DType dt, int32_t m, int32_t n, int32_t k) {
-  if (dt != DType::BF16 || n % 256 != 0 || m <= 0) return false;
+// ------------------------------------------------------------------ 128x256 tile, two per CU
+//
+// A 128x256x32 workgroup tile on four wavefronts of 64x128 (8 accumulators,
+// 128 registers), budgeted so that two workgroups share a CU: while one
+// writes its tile back (bias, GELU, residual read-modify-write, KV-cache
+// scatter) the other keeps the matrix cores busy.  Three 24 KB stages of
+// 64-byte rows (16-byte chunks permuted by an XOR with bits 2..3 of the row,
+// so the 16 rows one fragment read touches per chunk hit 16 distinct bank
+// groups), loaded straight from global memory; the loads of k-tile t+3 go out
+// as soon as every wavefront is done with k-tile t, two k-tiles ahead of use.
+namespace pair {
+
+constexpr int kBM = 128, kBN = 256, kBK = 32;
+constexpr int kWOff = kBM * kBK * 2;             // weight rows start 8 KB into a stage
+constexpr int kStage = (kBM + kBN) * kBK * 2;    // 24 KB
+constexpr int kLoads = kStage / 1024 / 4;        // load instructions per wavefront per k-tile
+static_assert(kLoads == 6, "load schedule assumes six loads per wavefront");
+
+__device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 2) & 3); }
+
+struct Frag {
+  bf16x8 x[2];  // activation rows (MFMA B operand)
+  bf16x8 w[4];  // weight rows (MFMA A operand)
+};
+
+// Load instruction q (0..23 per k-tile) moves 1 KB: q < 8 carries activation
+// rows 16q..16q+15, q >= 8 weight rows 16(q-8)..; lane l writes LDS bytes
+// [16 l, 16 l + 16) of the block: row 16 q' + l / 4 at physical chunk l % 4.
+__device__ __forceinline__ void load_lds(unsigned stage, int q, const bf16 *A, const bf16 *W,
+                                         int M, int K, int m0, int n0, int k0, int lane) {
+  const int rr = lane >> 2, pc = lane & 3;
+  const bf16 *g;
+  if (q < 8) {
+    const int r = q * 16 + rr;
+    g = A + (size_t)min(m0 + r, M - 1) * K + k0 + swz(r, pc) * 8;
+  } else {
+    const int r = (q - 8) * 16 + rr;
+    g = W + (size_t)(n0 + r) * K + k0 + swz(r, pc) * 8;
+  }
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(g), "s"(__builtin_amdgcn_readfirstlane(stage + q * 1024))
+               : "memory", "m0");
+}
+
+// Fragment r of k16 step s (0 or 1), in the order the MFMAs need them: x0 w0 x1 w1 w2 w3.
+__device__ __forceinline__ void read_frag(Frag &f, int r, const unsigned char *stage, int s, int wm,
+                                          int wn, int lane) {
+  const int c = 2 * s + (lane >> 5);
+  if (r == 0 || r == 2) {
+    const int row = wm * 64 + (r >> 1) * 32 + (lane & 31);
+    f.x[r >> 1] = *reinterpret_cast<const bf16x8 *>(stage + row * 64 + swz(row, c) * 16);
+  } else {
+    const int j = r == 1 ? 0 : r - 2;
+    const int row = wn * 128 + j * 32 + (lane & 31);
+    f.w[j] = *reinterpret_cast<const bf16x8 *>(stage + kWOff + row * 64 + swz(row, c) * 16);
+  }
+}
+
+__device__ __forceinline__ void mfma(f32x16 (&acc)[4][2], const Frag &f, int q) {
+  const int j = q >> 1, i = q & 1;
+  acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.w[j], f.x[i], acc[j][i], 0, 0, 0);
+}
+
+// Wait until at most VM of this wavefront's loads are in flight and its LDS
+// reads are done, then the workgroup barrier.
+template <int VM>
+__device__ __forceinline__ void barrier_vm() {
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(VM) : "memory");
+}
+
+}  // namespace pair
+
+template <class Epi>
+__global__ __launch_bounds__(256, 2) void gemm_bf16_pair_kernel(const bf16 *A, const bf16 *W,
+                                                                int M, int N, int K, Epi epi) {
+  using namespace pair;
+  using big::pin;
+  using Row = typename Epi::Row;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[3 * kStage];
+  __shared__ __attribute__((aligned(16))) Row rows_lds[kBM];
+  static_assert(4 * 32 * big::kWbStride * 4 <= 3 * kStage, "staged write-back fits the stages");
+  const int tiles_m = (M + kBM - 1) / kBM, tiles_n = N / kBN;
+  int tm, tn;
+  tile_coords(xcd_remap(blockIdx.x, gridDim.x), tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * kBM, n0 = tn * kBN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int q0 = wave * kLoads;
+  const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void *)smem;
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) acc[j][i] = f32x16{};
+  const int nk = K / kBK;
+
+  // The write-back's row record (threads < 128) and bias (each lane's four
+  // columns), loaded before the tile loads and kept in registers: they reach
+  // LDS only after the main loop, so no wait on them holds up the pipeline.
+  Row rec{};
+  if (tid < kBM) rec = epi.row(min(m0 + tid, M - 1));
+  const f32x4 bias = epi.bias4(n0 + wn * 128 + (lane & 31) * 4);
+
+  // k-tiles 0 and 1 and the first half of k-tile 2
+  unsigned s0 = lds0, s1 = lds0 + kStage, s2 = lds0 + 2 * kStage;
+#pragma unroll
+  for (int p = 0; p < kLoads; ++p) load_lds(s0, q0 + p, A, W, M, K, m0, n0, 0, lane);
+  if (nk > 1) {
+#pragma unroll
+    for (int p = 0; p < kLoads; ++p) load_lds(s1, q0 + p, A, W, M, K, m0, n0, kBK, lane);
+  }
+  if (nk > 2) {
+#pragma unroll
+    for (int p = 0; p < 3; ++p) load_lds(s2, q0 + p, A, W, M, K, m0, n0, 2 * kBK, lane);
+  }
+  if (nk > 2) barrier_vm<9>();
+  else if (nk > 1) barrier_vm<6>();
+  else barrier_vm<0>();
+  Frag fa, fb;
+  const unsigned char *smem_u = smem;
+#pragma unroll
+  for (int r = 0; r < 6; ++r) read_frag(fa, r, smem_u + (s0 - lds0), 0, wm, wn, lane);
+
+  for (int t = 0; t + 1 < nk; ++t) {
+    // s0: k-tile t; s1: k-tile t+1; s2: k-tile t+2 (its first half in flight)
+    const bool has2 = t + 2 < nk, has3 = t + 3 < nk;
+    const int k2 = (t + 2) * kBK, k3 = (t + 3) * kBK;
+    const unsigned char *sc = smem_u + (s0 - lds0), *sn = smem_u + (s1 - lds0);
+    // k16 step 0: step-1 fragments; second half of k-tile t+2
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      mfma(acc, fa, q);
+      if (q < 6) read_frag(fb, q, sc, 1, wm, wn, lane);
+      else if (has2) load_lds(s2, q0 + 3 + (q - 6), A, W, M, K, m0, n0, k2, lane);
+      pin();
+    }
+    // k16 step 1: last load of k-tile t+2; barrier (k-tile t+1 complete,
+    // k-tile t read by all); step-0 fragments of k-tile t+1; first half of
+    // k-tile t+3 into the stage k-tile t leaves
+    mfma(acc, fb, 0);
+    if (has2) load_lds(s2, q0 + 5, A, W, M, K, m0, n0, k2, lane);
+    pin();
+    mfma(acc, fb, 1);
+    pin();
+    if (has2) barrier_vm<6>();
+    else barrier_vm<0>();
+    pin();
+#pragma unroll
+    for (int q = 2; q < 8; ++q) {
+      mfma(acc, fb, q);
+      read_frag(fa, q - 2, sn, 0, wm, wn, lane);
+      if (q >= 5 && has3) load_lds(s0, q0 + (q - 5), A, W, M, K, m0, n0, k3, lane);
+      pin();
+    }
+    const unsigned s_old = s0;
+    s0 = s1;
+    s1 = s2;
+    s2 = s_old;
+  }
+  {  // last k-tile
+    const unsigned char *sc = smem_u + (s0 - lds0);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      mfma(acc, fa, q);
+      if (q < 6) read_frag(fb, q, sc, 1, wm, wn, lane);
+      pin();
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      mfma(acc, fb, q);
+      pin();
+    }
+  }
+  if (tid < kBM) rows_lds[tid] = rec;
+  // every wavefront is done with the stages before they hold the write-back's
+  // staging rows, and the row records are in LDS
+  barrier_vm<0>();
+  write_back_staged<2, 8>(acc, epi, m0 + wm * 64, n0 + wn * 128, M, lane,
+                          reinterpret_cast<float *>(smem) + wave * 32 * big::kWbStride,
+                          rows_lds + wm * 64, bias);
+}
+
+// Tile choice.  The 256x256 tile (one workgroup per CU) when its tiles fill
+// the compute units in whole waves well enough: at least 90% of the last
+// wave, or 80% when K >= 2048 (the longer main loop amortises the tile's
+// fixed start and write-back).  Otherwise the 128x256 tile, two workgroups
+// per CU, whose write-backs overlap the other workgroup's main loop and whose
+// finer steps fill the chip better.  Measured at MAR-L sizes: full-step QKV,
+// fc1 and fc2 and cache-aware QKV take the 256x256 tile, the output
+// projection and the other cache-aware GEMMs the 128x256 one.  Under
+// sustained load the 128x256 tile runs at a lower clock (more operand traffic
+// per flop), which is why it does not replace the large tile outright.
+int gemm_tile_kind(DType dt, int32_t m, int32_t n, int32_t k) {
+  if (dt != DType::BF16 || m <= 0) return GEMM_TILE_128x256;
   const long tiles = (long)((m + 255) / 256) * (n / 256);
   const long cus = device_cu_count();
   const long waves = (tiles + cus - 1) / cus;
   const double fill = (double)tiles / (double)(waves * cus);
-  return fill >= 0.9 || (fill >= 0.8 && k >= 2048);
+  return (fill >= 0.9 || (fill >= 0.8 && k >= 2048)) ? GEMM_TILE_256 : GEMM_TILE_128x256;
 }
 
+// N a multiple of 256 and K of 64 (the host limits d_model and d_mlp to
+// multiples of 256).
 template <class Epi>
 static hipError_t run_bf16(const void *a, const void *w, int m, int n, int k, const Epi &epi,
                            hipStream_t s) {
   if (m == 0) return hipSuccess;
-  if (n % TileS::BN != 0 || k % TileS::BK != 0) return hipErrorInvalidValue;
-  if (gemm_large_tile(DType::BF16, m, n, k)) {
-    const int grid = ((m + 255) / 256) * (n / 256);
-    gemm_bf16_big_kernel<Epi><<<grid, 256, 0, s>>>(static_cast<const bf16 *>(a),
-                                                    static_cast<const bf16 *>(w), m, n, k, epi);
-    return hipGetLastError();
-  }
-  return launch_tile<TileS>(a, w, m, n, k, epi, s);
+  if (n % 256 != 0 || k % 64 != 0) return hipErrorInvalidValue;
+  const bf16 *A = static_cast<const bf16 *>(a), *W = static_cast<const bf16 *>(w);
+  if (gemm_tile_kind(DType::BF16, m, n, k) == GEMM_TILE_256)
+    gemm_bf16_big_kernel<Epi><<<((m + 255) / 256) * (n / 256), 256, 0, s>>>(A, W, m, n, k, epi);
+  else
+    gemm_bf16_pair_kernel<Epi>
+        <<<((m + pair::kBM - 1) / pair::kBM) * (n / pair::kBN), 256, 0, s>>>(A, W, m, n, k, epi);
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ fp32 FMA

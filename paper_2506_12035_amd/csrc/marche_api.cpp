@@ -81,8 +81,9 @@ marche_status_t check_model(const marche_model_t *m) {
 
 // One class per kernel symbol.  The attention kernel is instantiated per
 // query-chunk width (1, 2 or 4 wavefronts of 32 queries), chosen from the
-// largest active set of the call; each GEMM has a 128x128 and a 256x256 tile
-// instantiation (class + 1), chosen from its shape.
+// largest active set of the call; each bf16 GEMM has a 128x256 and a 256x256
+// (class + 1) tile instantiation, chosen from its shape (fp32 GEMMs are timed
+// under the first).
 enum KClass {
   K_ROW_MAP, K_GATHER_LN, K_GEMM_QKV, K_GEMM_QKV_L, K_ATTN_W1, K_ATTN_W2, K_ATTN_W4,
   K_ATTN_SCORES, K_GEMM_O, K_GEMM_O_L, K_GEMM_FC1, K_GEMM_FC1_L, K_GEMM_FC2, K_GEMM_FC2_L,
@@ -90,11 +91,17 @@ enum KClass {
   K_NCLASS
 };
 const char *const kClassNames[K_NCLASS] = {
-    "row_map",       "gather_ln",      "gemm_qkv_t128", "gemm_qkv_t256", "attention_q32",
-    "attention_q64", "attention_q128", "attn_scores",   "gemm_o_t128",   "gemm_o_t256",
-    "gemm_fc1_t128", "gemm_fc1_t256",  "gemm_fc2_t128", "gemm_fc2_t256", "select_topk",
-    "decoder_input", "fill_zero",      "attention2_q32", "attention2_q64", "attention2_q128",
-    "concat_kv",     "attention_res"};
+    "row_map",           "gather_ln",      "gemm_qkv_t128x256", "gemm_qkv_t256",
+    "attention_q32",     "attention_q64",  "attention_q128",    "attn_scores",
+    "gemm_o_t128x256",   "gemm_o_t256",    "gemm_fc1_t128x256", "gemm_fc1_t256",
+    "gemm_fc2_t128x256", "gemm_fc2_t256",  "select_topk",       "decoder_input",
+    "fill_zero",         "attention2_q32", "attention2_q64",    "attention2_q128",
+    "concat_kv",         "attention_res"};
+
+// Timing class of a GEMM launch: base is the projection's 128x256 class.
+int gemm_class(int base, DType dt, int32_t m, int32_t n, int32_t k) {
+  return base + (gemm_tile_kind(dt, m, n, k) == GEMM_TILE_256 ? 1 : 0);
+}
 
 int attn_class(DType dt, int a_max, int n_tokens) {
   if (dt == DType::BF16 && attn_resident(a_max, n_tokens, false)) return K_ATTN_RES;
@@ -308,7 +315,7 @@ marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layer
            launch_gather_ln(dt, buf0, x, map, static_cast<const float *>(L.ln1_g),
                             static_cast<const float *>(L.ln1_b), M, D, m->ln_eps, stream));
     QkvOut qo{buf1, kc, vc, D, dh, H, N};
-    LAUNCH(K_GEMM_QKV + gemm_large_tile(dt, M, 3 * D, D), 2.0 * M * 3 * D * D,
+    LAUNCH(gemm_class(K_GEMM_QKV, dt, M, 3 * D, D), 2.0 * M * 3 * D * D,
            gemm_bytes_act * ((double)M * D + 3.0 * D * D + 3.0 * M * D),
            launch_gemm_qkv(dt, buf0, L.w_qkv, static_cast<const float *>(L.b_qkv), M, 3 * D, D,
                            map, qo, stream));
@@ -322,17 +329,17 @@ marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layer
              es * (double)batch * N * D + 4.0 * batch * H * N,
              launch_attn_scores(dt, aa, n_gen, gen_max, scores, stream));
     }
-    LAUNCH(K_GEMM_O + gemm_large_tile(dt, M, D, D), 2.0 * M * D * D, gemm_bytes_act * ((double)M * D + (double)D * D) + 8.0 * M * D,
+    LAUNCH(gemm_class(K_GEMM_O, dt, M, D, D), 2.0 * M * D * D, gemm_bytes_act * ((double)M * D + (double)D * D) + 8.0 * M * D,
            launch_gemm_resid(dt, buf0, L.w_o, static_cast<const float *>(L.b_o), M, D, D, map, x,
                              0, stream));
     LAUNCH(K_GATHER_LN, 0, (double)M * D * (4 + es),
            launch_gather_ln(dt, buf1, x, map, static_cast<const float *>(L.ln2_g),
                             static_cast<const float *>(L.ln2_b), M, D, m->ln_eps, stream));
-    LAUNCH(K_GEMM_FC1 + gemm_large_tile(dt, M, F, D), 2.0 * M * F * D,
+    LAUNCH(gemm_class(K_GEMM_FC1, dt, M, F, D), 2.0 * M * F * D,
            gemm_bytes_act * ((double)M * D + (double)F * D + (double)M * F),
            launch_gemm_gelu(dt, buf1, L.w_1, static_cast<const float *>(L.b_1), M, F, D, hid,
                             stream));
-    LAUNCH(K_GEMM_FC2 + gemm_large_tile(dt, M, D, F), 2.0 * M * D * F,
+    LAUNCH(gemm_class(K_GEMM_FC2, dt, M, D, F), 2.0 * M * D * F,
            gemm_bytes_act * ((double)M * F + (double)D * F) + 8.0 * M * D,
            launch_gemm_resid(dt, hid, L.w_2, static_cast<const float *>(L.b_2), M, D, F, map, x,
                              1, stream));

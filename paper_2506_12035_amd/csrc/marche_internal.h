@@ -59,7 +59,10 @@ hipError_t launch_gemm_gelu(DType dt, const void *a, const void *w, const float 
                             int32_t n, int32_t k, void *h, hipStream_t s);
 // Whether a bf16 GEMM of this shape runs on the 256x256 tile (else 128x128);
 // each tile is its own kernel symbol.
-bool gemm_large_tile(DType dt, int32_t m, int32_t n, int32_t k);
+// bf16 GEMM workgroup tile for an M x N x K product: 128x256 (two workgroups
+// per CU) or 256x256 (one per CU).
+enum GemmTile { GEMM_TILE_128x256 = 0, GEMM_TILE_256 = 1 };
+int gemm_tile_kind(DType dt, int32_t m, int32_t n, int32_t k);
 // Compute units of the current device (queried once per device, then cached).
 int device_cu_count();
 

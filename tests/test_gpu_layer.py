@@ -165,7 +165,7 @@ def _ragged_case(cfg, B, sizes, gens, seed):
 @pytest.mark.parametrize("shape", list(BF16_SHAPES))
 def test_bf16_layer_ragged(shape):
     spec = BF16_SHAPES[shape]
-    cfg = workload.CONFIGS[spec["cid"]].with_(n_tokens=spec["n_tokens"])
+    cfg = workload.CONFIGS[spec["cid"]].with_(**{k: v for k, v in spec.items() if k != "cid"})
     N = cfg.n_tokens
     # ragged active sets: a single token, a typical cache-aware set, a set that
     # spans two query chunks, and every token (a full layer)
