@@ -222,6 +222,100 @@ marche_status_t marche_attention_segments(const void *q, void *o, int32_t n_quer
                                           int32_t dtype, int32_t mode, void *workspace,
                                           size_t workspace_bytes, marche_stream_t stream);
 
+/* ---- The rest of a MAR step: encoder input, decoder input, sampler ----
+ * These calls surround marche_step to make a whole generation step of the
+ * masked autoregressive model: the encoder over the known tokens (Eq. 1), the
+ * decoder input built from its output (Eq. 2), and the sampler that draws
+ * the generating tokens' values from the decoder output (Eq. 3).  The encoder
+ * blocks themselves are marche_step over a model whose n_tokens is the
+ * encoder's row count n_buf + n_known, with every row active; its cache is
+ * scratch that every layer overwrites before reading, so the caller may
+ * describe it with a marche_kv_cache_t filled directly (no kv_cache_init).
+ * Image tokens are numbered p in [0, n_img); sequence position of image
+ * token p is n_buf + p, the n_buf buffer rows come first.  Known tokens are
+ * those with rank[b][p] < n_known, rank being the position of p in image b's
+ * generation order. */
+
+/* Encoder input rows (Eq. 1), x_enc [batch][n_buf + n_known][d_model] float32:
+ *   row i < n_buf:  cls[b] + pe_enc[i]                      (buffer rows)
+ *   row n_buf + r:  w_z . tok[b][p] + b_z + pe_enc[n_buf + p],  p = known[b][r]
+ * cls [batch][d_model]; tok [batch][n_img][c_tok]; w_z [d_model][c_tok];
+ * b_z [d_model]; pe_enc [n_buf + n_img][d_model]; known [batch][n_known]
+ * int32 image tokens (device; any order, ascending is the encoder's usual
+ * order).  All float32.  d_model a multiple of 256, <= 4096; 1 <= c_tok <= 64. */
+marche_status_t marche_encoder_input(float *x_enc, const float *cls, const float *tok,
+                                     const float *w_z, const float *b_z, const float *pe_enc,
+                                     const int32_t *known, int32_t batch, int32_t n_buf,
+                                     int32_t n_img, int32_t n_known, int32_t d_model,
+                                     int32_t c_tok, marche_stream_t stream);
+
+/* Decoder input from the encoder output (Eq. 2), x_dec [batch][n_buf + n_img][d_model]
+ * float32, every row written:
+ *   u = LN(x_enc) * ln_g + ln_b;  v = u . w_de^T + b_de   (per encoder row)
+ *   x_dec[b][j] = v[encoder row of j] + pe_dec[j]  for buffer rows j < n_buf and
+ *                 known tokens j = n_buf + known[b][r] (encoder row n_buf + r);
+ *   x_dec[b][n_buf + p] = mask + pe_dec[n_buf + p]  for rank[b][p] >= n_known.
+ * x_enc [batch][n_buf + n_known][d_model] float32; w_de [d_model][d_model] in
+ * `dtype` (u is rounded to it); ln_g, ln_b, b_de, mask [d_model] and pe_dec
+ * [n_buf + n_img][d_model] float32; known [batch][n_known], rank [batch][n_img]
+ * int32 (device).  workspace: marche_encoder_to_decoder_workspace_bytes, 256-byte
+ * aligned.  d_model a multiple of 256, <= 4096. */
+size_t marche_encoder_to_decoder_workspace_bytes(int32_t batch, int32_t n_buf, int32_t n_known,
+                                                 int32_t d_model, int32_t dtype);
+marche_status_t marche_encoder_to_decoder(float *x_dec, const float *x_enc, const float *ln_g,
+                                          const float *ln_b, float ln_eps, const void *w_de,
+                                          const float *b_de, const float *mask,
+                                          const float *pe_dec, const int32_t *known,
+                                          const int32_t *rank, int32_t batch, int32_t n_buf,
+                                          int32_t n_img, int32_t n_known, int32_t d_model,
+                                          int32_t dtype, void *workspace, size_t workspace_bytes,
+                                          marche_stream_t stream);
+
+/* Sampler of Eq. 3: x_i ~ p(x_i | z_i; tau) for n_rows generating tokens.
+ * Condition z_i = LN(x_dec[row_i]) * dec_ln_g + dec_ln_b + pe_diff[p_i]
+ * (row_i = rows[i] = b * n_tokens + n_buf + p_i).  Denoiser eps(x, t, z), W = width:
+ *   c = W_t2 SiLU(W_t1 sinus(t) + b_t1) + b_t2 + W_c z + b_c,  s = SiLU(c)
+ *   [shift_k | scale_k | gate_k] = rows [3kW, 3kW + 3W) of W_ada s + b_ada,
+ *   [shift_f | scale_f] = rows [3nW, 3nW + 2W)            (n = n_blocks)
+ *   h = W_in x + b_in;  for k < n: h += gate_k * (W_2k SiLU(W_1k (LN(h)(1 + scale_k) + shift_k) + b_1k) + b_2k)
+ *   eps = W_out (LN(h)(1 + scale_f) + shift_f) + b_out
+ * with LN without affine (eps head->ln_eps) and sinus(t) = [cos(t w_j) | sin(t w_j)],
+ * w_j = 10000^(-j / (t_freq/2)).  DDPM ancestral sampling over n_steps steps of
+ * the cosine schedule (alpha_bar(u) = cos^2((u + 0.008)/1.008 pi/2) normalised,
+ * betas clipped at 0.999): x = noise[n_steps]; for i = n_steps-1 .. 0:
+ *   x0 = (x - sqrt(1 - ab_i) eps(x, i, z)) / sqrt(ab_i),
+ *   x = posterior mean(x0, x) + temperature * sqrt(posterior variance) * noise[i]
+ * (no noise at i = 0); the final x goes to tok_out[out_rows[i]] (c_tok floats).
+ * noise [n_steps + 1][n_rows][c_tok] float32 (caller-drawn, device);
+ * rows, out_rows [n_rows] int32 (device).
+ * Weights: w_t1 [W][t_freq], w_t2 [W][W], w_c [W][d_cond], w_ada [(3n+2)W][W],
+ * w_1, w_2 [n][W][W] in head->dtype; w_in [W][c_tok], w_out [c_tok][W] and
+ * every bias float32.  Supported: width and d_cond multiples of 256 (<= 4096),
+ * t_freq a multiple of 64 (<= 4096), 1 <= n_blocks <= 64, 1 <= c_tok <= 64,
+ * 1 <= n_steps <= 10000; n_rows * (3n+2) * width < 2^31.  workspace:
+ * marche_diffusion_workspace_bytes, 256-byte aligned. */
+typedef struct {
+  int32_t width, n_blocks, c_tok, d_cond, t_freq;
+  marche_dtype_t dtype;
+  float ln_eps;
+} marche_head_t;
+
+typedef struct {
+  const void *w_t1, *b_t1, *w_t2, *b_t2, *w_c, *b_c, *w_in, *b_in, *w_ada, *b_ada, *w_1, *b_1,
+      *w_2, *b_2, *w_out, *b_out;
+} marche_head_weights_t;
+
+size_t marche_diffusion_workspace_bytes(const marche_head_t *head, int32_t n_rows,
+                                        int32_t n_steps);
+marche_status_t marche_diffusion_sample(const marche_head_t *head, const marche_head_weights_t *w,
+                                        const float *x_dec, int32_t n_tokens, int32_t n_buf,
+                                        const float *dec_ln_g, const float *dec_ln_b,
+                                        float dec_ln_eps, const float *pe_diff,
+                                        const int32_t *rows, const int32_t *out_rows,
+                                        int32_t n_rows, const float *noise, int32_t n_steps,
+                                        float temperature, float *tok_out, void *workspace,
+                                        size_t workspace_bytes, marche_stream_t stream);
+
 /* Name of a status code (static string). */
 const char *marche_status_string(marche_status_t s);
 

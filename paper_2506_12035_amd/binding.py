@@ -25,6 +25,8 @@ EXPORTED = (
     "kv_cache_init", "marche_step_workspace_bytes", "marche_step", "select_refresh",
     "select_refresh_ordered",
     "marche_decoder_input", "marche_attention_workspace_bytes", "marche_attention_segments",
+    "marche_encoder_input", "marche_encoder_to_decoder_workspace_bytes",
+    "marche_encoder_to_decoder", "marche_diffusion_workspace_bytes", "marche_diffusion_sample",
     "marche_status_string", "marche_last_error",
     "marche_profile_enable", "marche_profile_collect", "marche_profile_entry",
     "marche_profile_reset",
@@ -46,6 +48,18 @@ class KVCache(C.Structure):
     _fields_ = [("k", C.c_void_p), ("v", C.c_void_p), ("n_layers", C.c_int32),
                 ("batch", C.c_int32), ("n_heads", C.c_int32), ("n_tokens", C.c_int32),
                 ("head_dim", C.c_int32), ("dtype", C.c_int32)]
+
+
+class Head(C.Structure):
+    _fields_ = [("width", C.c_int32), ("n_blocks", C.c_int32), ("c_tok", C.c_int32),
+                ("d_cond", C.c_int32), ("t_freq", C.c_int32), ("dtype", C.c_int32),
+                ("ln_eps", C.c_float)]
+
+
+class HeadWeights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("w_t1", "b_t1", "w_t2", "b_t2", "w_c", "b_c", "w_in",
+                                          "b_in", "w_ada", "b_ada", "w_1", "b_1", "w_2", "b_2",
+                                          "w_out", "b_out")]
 
 
 class MarcheError(RuntimeError):
@@ -76,6 +90,17 @@ def lib() -> C.CDLL:
         L.marche_attention_workspace_bytes.restype = sz
         L.marche_attention_segments.argtypes = [vp, vp, i32, vp, vp, i32, vp, vp, i32, i32, i32,
                                                 i32, i32, i32, vp, sz, vp]
+        L.marche_encoder_input.argtypes = [vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32,
+                                           i32, vp]
+        L.marche_encoder_to_decoder_workspace_bytes.argtypes = [i32, i32, i32, i32, i32]
+        L.marche_encoder_to_decoder_workspace_bytes.restype = sz
+        L.marche_encoder_to_decoder.argtypes = [vp, vp, vp, vp, C.c_float, vp, vp, vp, vp, vp, vp,
+                                                i32, i32, i32, i32, i32, i32, vp, sz, vp]
+        L.marche_diffusion_workspace_bytes.argtypes = [C.POINTER(Head), i32, i32]
+        L.marche_diffusion_workspace_bytes.restype = sz
+        L.marche_diffusion_sample.argtypes = [C.POINTER(Head), C.POINTER(HeadWeights), vp, i32,
+                                              i32, vp, vp, C.c_float, vp, vp, vp, i32, vp, i32,
+                                              C.c_float, vp, vp, sz, vp]
         L.marche_status_string.argtypes = [C.c_int]
         L.marche_status_string.restype = C.c_char_p
         L.marche_last_error.argtypes = []
@@ -90,7 +115,8 @@ def lib() -> C.CDLL:
         L.marche_profile_reset.restype = None
         for name in ("kv_cache_init", "marche_step", "select_refresh", "select_refresh_ordered",
                      "marche_decoder_input", "marche_attention_segments",
-                     "marche_profile_enable", "marche_profile_entry"):
+                     "marche_encoder_input", "marche_encoder_to_decoder",
+                     "marche_diffusion_sample", "marche_profile_enable", "marche_profile_entry"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -187,6 +213,54 @@ def attention_segments(q, o, n_query: int, k_a, v_a, n_a: int, k_c, v_c, n_c: in
                                            _ptr(k_c), _ptr(v_c), n_c, batch, n_heads, head_dim,
                                            dtype, mode, _ptr(workspace), workspace_bytes,
                                            _stream(stream)))
+
+
+def encoder_input(x_enc, cls, tok, w_z, b_z, pe_enc, known, batch: int, n_buf: int, n_img: int,
+                  n_known: int, d_model: int, c_tok: int, stream=None) -> None:
+    _check(lib().marche_encoder_input(_ptr(x_enc), _ptr(cls), _ptr(tok), _ptr(w_z), _ptr(b_z),
+                                      _ptr(pe_enc), _ptr(known), batch, n_buf, n_img, n_known,
+                                      d_model, c_tok, _stream(stream)))
+
+
+def encoder_to_decoder_workspace_bytes(batch: int, n_buf: int, n_known: int, d_model: int,
+                                       dtype: int) -> int:
+    return lib().marche_encoder_to_decoder_workspace_bytes(batch, n_buf, n_known, d_model, dtype)
+
+
+def encoder_to_decoder(x_dec, x_enc, ln_g, ln_b, ln_eps: float, w_de, b_de, mask, pe_dec, known,
+                       rank, batch: int, n_buf: int, n_img: int, n_known: int, d_model: int,
+                       dtype: int, workspace=None, workspace_bytes: int = 0, stream=None) -> None:
+    _check(lib().marche_encoder_to_decoder(_ptr(x_dec), _ptr(x_enc), _ptr(ln_g), _ptr(ln_b), ln_eps,
+                                           _ptr(w_de), _ptr(b_de), _ptr(mask), _ptr(pe_dec),
+                                           _ptr(known), _ptr(rank), batch, n_buf, n_img, n_known,
+                                           d_model, dtype, _ptr(workspace), workspace_bytes,
+                                           _stream(stream)))
+
+
+def make_head(width, n_blocks, c_tok, d_cond, t_freq, dtype, ln_eps) -> Head:
+    return Head(width, n_blocks, c_tok, d_cond, t_freq, dtype, ln_eps)
+
+
+def make_head_weights(p: dict) -> HeadWeights:
+    w = HeadWeights()
+    for name, _ in HeadWeights._fields_:
+        setattr(w, name, _ptr(p[name]))
+    return w
+
+
+def diffusion_workspace_bytes(head: Head, n_rows: int, n_steps: int) -> int:
+    return lib().marche_diffusion_workspace_bytes(C.byref(head), n_rows, n_steps)
+
+
+def diffusion_sample(head: Head, weights: HeadWeights, x_dec, n_tokens: int, n_buf: int, dec_ln_g,
+                     dec_ln_b, dec_ln_eps: float, pe_diff, rows, out_rows, n_rows: int, noise,
+                     n_steps: int, temperature: float, tok_out, workspace=None,
+                     workspace_bytes: int = 0, stream=None) -> None:
+    _check(lib().marche_diffusion_sample(C.byref(head), C.byref(weights), _ptr(x_dec), n_tokens,
+                                         n_buf, _ptr(dec_ln_g), _ptr(dec_ln_b), dec_ln_eps,
+                                         _ptr(pe_diff), _ptr(rows), _ptr(out_rows), n_rows,
+                                         _ptr(noise), n_steps, temperature, _ptr(tok_out),
+                                         _ptr(workspace), workspace_bytes, _stream(stream)))
 
 
 def profile_enable(on: bool) -> None:

@@ -42,6 +42,12 @@ __device__ __forceinline__ float gelu_erf(float z) {
   return fmaf(-a, poly * e, fmaxf(z, 0.0f));
 }
 
+// SiLU z * sigmoid(z) = z / (1 + 2^(-z log2 e)); for z -> -inf the power
+// overflows to +inf and the reciprocal to 0.
+__device__ __forceinline__ float silu(float z) {
+  return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * z));
+}
+
 template <typename T>
 __device__ __forceinline__ T from_f32(float v);
 template <>

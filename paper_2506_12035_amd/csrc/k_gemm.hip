@@ -129,6 +129,58 @@ struct EpiGelu {
   }
 };
 
+// Plain epilogue of the sampler's GEMMs: out[r][c] = act(C + bias) stored
+// row-major as T (ld = n), act the identity or SiLU.
+template <typename T, bool SILU>
+struct EpiPlain {
+  static constexpr bool kPrior = false;
+  T *out;
+  const float *bias;
+  int n;
+  using Row = int32_t;  // element offset of the output row (< 2^31, host-checked)
+  using Col = int32_t;
+  __device__ __forceinline__ Row row(int r) const { return r * n; }
+  __device__ __forceinline__ Col col(int c0) const { return c0; }
+  __device__ __forceinline__ f32x4 bias4(int c0) const { return load_bias4(bias, c0); }
+  __device__ __forceinline__ f32x4 prior(const Row &, const Col &) const { return f32x4{}; }
+  __device__ __forceinline__ void store(const Row &ro, int, const Col &c, f32x4 v) const {
+    if constexpr (SILU) v = f32x4{silu(v[0]), silu(v[1]), silu(v[2]), silu(v[3])};
+    store4(out + (uint32_t)(ro + c), v);
+  }
+};
+
+// Decoder embedding of the encoder rows (Eq. 2): encoder row r of image
+// b = r / n_enc holds buffer token i = r % n_enc (i < n_buf) or the known
+// image token known[b][i - n_buf]; its result goes to that token's sequence
+// position j in the float32 decoder input x [batch][n_tokens][n], plus the
+// decoder's positional embedding pe[j].
+struct EpiEmbed {
+  static constexpr bool kPrior = true;
+  float *x;
+  const float *bias;
+  const float *pe;
+  const int32_t *known;
+  int n, n_enc, n_buf, n_known, n_tokens;
+  struct Row {
+    int32_t x_off;   // (b * n_tokens + j) * n
+    int32_t pe_off;  // j * n
+  };
+  using Col = int32_t;
+  __device__ __forceinline__ Row row(int r) const {
+    const int b = r / n_enc, i = r - b * n_enc;
+    const int j = i < n_buf ? i : n_buf + known[b * n_known + (i - n_buf)];
+    return Row{(b * n_tokens + j) * n, j * n};
+  }
+  __device__ __forceinline__ Col col(int c0) const { return c0; }
+  __device__ __forceinline__ f32x4 bias4(int c0) const { return load_bias4(bias, c0); }
+  __device__ __forceinline__ f32x4 prior(const Row &ro, const Col &c) const {
+    return *reinterpret_cast<const f32x4 *>(pe + (uint32_t)(ro.pe_off + c));
+  }
+  __device__ __forceinline__ void store(const Row &ro, int, const Col &c, f32x4 v) const {
+    *reinterpret_cast<f32x4 *>(x + (uint32_t)(ro.x_off + c)) = v;
+  }
+};
+
 // Empty uses that pin loaded values to this point: without them the compiler
 // sinks the loads into the row-guarded store blocks, one wait per block.
 __device__ __forceinline__ void keep(const f32x4 &v) { asm volatile("" ::"v"(v)); }
@@ -746,6 +798,34 @@ hipError_t launch_gemm_gelu(DType dt, const void *a, const void *w, const float 
   }
   EpiGelu<bf16> e{static_cast<bf16 *>(h), bias, n};
   return run_bf16(a, w, m, n, k, e, s);
+}
+
+}  // namespace marche
+
+namespace marche {
+
+hipError_t launch_gemm_plain(DType dt, const void *a, const void *w, const float *bias, int32_t m,
+                             int32_t n, int32_t k, void *out, DType out_dt, bool silu_act,
+                             hipStream_t s) {
+  if (dt == DType::F32) {
+    if (out_dt != DType::F32) return hipErrorInvalidValue;
+    if (silu_act) return run_f32(a, w, m, n, k, EpiPlain<float, true>{static_cast<float *>(out), bias, n}, s);
+    return run_f32(a, w, m, n, k, EpiPlain<float, false>{static_cast<float *>(out), bias, n}, s);
+  }
+  if (out_dt == DType::F32) {
+    if (silu_act) return hipErrorInvalidValue;
+    return run_bf16(a, w, m, n, k, EpiPlain<float, false>{static_cast<float *>(out), bias, n}, s);
+  }
+  if (silu_act) return run_bf16(a, w, m, n, k, EpiPlain<bf16, true>{static_cast<bf16 *>(out), bias, n}, s);
+  return run_bf16(a, w, m, n, k, EpiPlain<bf16, false>{static_cast<bf16 *>(out), bias, n}, s);
+}
+
+hipError_t launch_gemm_embed(DType dt, const void *a, const void *w, const float *bias, int32_t m,
+                             int32_t n, int32_t k, float *x, const float *pe, const int32_t *known,
+                             int32_t n_enc, int32_t n_buf, int32_t n_known, int32_t n_tokens,
+                             hipStream_t s) {
+  EpiEmbed e{x, bias, pe, known, n, n_enc, n_buf, n_known, n_tokens};
+  return dt == DType::F32 ? run_f32(a, w, m, n, k, e, s) : run_bf16(a, w, m, n, k, e, s);
 }
 
 }  // namespace marche

@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -88,6 +89,9 @@ enum KClass {
   K_ROW_MAP, K_GATHER_LN, K_GEMM_QKV, K_GEMM_QKV_L, K_ATTN_W1, K_ATTN_W2, K_ATTN_W4,
   K_ATTN_SCORES, K_GEMM_O, K_GEMM_O_L, K_GEMM_FC1, K_GEMM_FC1_L, K_GEMM_FC2, K_GEMM_FC2_L,
   K_SELECT, K_DECODER_INPUT, K_FILL, K_ATTN2_W1, K_ATTN2_W2, K_ATTN2_W4, K_CONCAT, K_ATTN_RES,
+  K_ENC_INPUT, K_MASK_FILL, K_LN_ROWS, K_GEMM_EMBED, K_GEMM_EMBED_L, K_TIME_SINUS, K_GEMM_HEAD,
+  K_GEMM_HEAD_L, K_GEMM_HEAD_SILU, K_GEMM_HEAD_SILU_L, K_HEAD_SILU_COND, K_HEAD_IN_MOD,
+  K_HEAD_GATE_MOD, K_HEAD_OUT_STEP,
   K_NCLASS
 };
 const char *const kClassNames[K_NCLASS] = {
@@ -96,7 +100,10 @@ const char *const kClassNames[K_NCLASS] = {
     "gemm_o_t128x256",   "gemm_o_t256",    "gemm_fc1_t128x256", "gemm_fc1_t256",
     "gemm_fc2_t128x256", "gemm_fc2_t256",  "select_topk",       "decoder_input",
     "fill_zero",         "attention2_q32", "attention2_q64",    "attention2_q128",
-    "concat_kv",         "attention_res"};
+    "concat_kv",         "attention_res",  "encoder_input",     "mask_fill",
+    "ln_rows",           "gemm_embed_t128x256", "gemm_embed_t256", "time_sinus",
+    "gemm_head_t128x256", "gemm_head_t256", "gemm_head_silu_t128x256", "gemm_head_silu_t256",
+    "head_silu_cond",    "head_in_mod",    "head_gate_mod",     "head_out_step"};
 
 // Timing class of a GEMM launch: base is the projection's 128x256 class.
 int gemm_class(int base, DType dt, int32_t m, int32_t n, int32_t k) {
@@ -486,6 +493,274 @@ marche_status_t marche_decoder_input(float *x, const float *cls, const float *va
          4.0 * d_model * ((double)batch * n_tokens + (double)batch * n_known + batch + n_tokens + 1),
          launch_decoder_input(x, cls, value, mask, pos, rank, batch, n_tokens, n_buf, d_model,
                               n_known, stream));
+  return MARCHE_OK;
+}
+
+// ------------------------------------------------------------------ rest of a MAR step
+
+marche_status_t marche_encoder_input(float *x_enc, const float *cls, const float *tok,
+                                     const float *w_z, const float *b_z, const float *pe_enc,
+                                     const int32_t *known, int32_t batch, int32_t n_buf,
+                                     int32_t n_img, int32_t n_known, int32_t d_model,
+                                     int32_t c_tok, marche_stream_t stream_) {
+  if (batch < 0 || n_buf < 0 || n_img < 0 || n_known < 0 || n_known > n_img)
+    return fail(MARCHE_ERR_INVALID_ARG, "batch=%d n_buf=%d n_img=%d n_known=%d inconsistent", batch,
+                n_buf, n_img, n_known);
+  if (d_model < 256 || d_model % 256 != 0 || d_model > 4096)
+    return fail(MARCHE_ERR_UNSUPPORTED, "d_model=%d (must be a multiple of 256, <= 4096)", d_model);
+  if (c_tok < 1 || c_tok > 64)
+    return fail(MARCHE_ERR_UNSUPPORTED, "c_tok=%d (supported: 1..64)", c_tok);
+  const int64_t rows = (int64_t)batch * (n_buf + n_known);
+  if (rows * d_model >= (1LL << 31)) return fail(MARCHE_ERR_UNSUPPORTED, "x_enc reaches 2^31 elements");
+  if (rows == 0) return MARCHE_OK;
+  if (!x_enc || !cls || !pe_enc || (n_known > 0 && (!tok || !w_z || !b_z || !known)))
+    return fail(MARCHE_ERR_INVALID_ARG, "NULL input to marche_encoder_input");
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  // Algorithmic traffic: x_enc written; class, token and positional rows read once.
+  LAUNCH(K_ENC_INPUT, 2.0 * batch * n_known * (double)d_model * c_tok,
+         4.0 * ((double)rows * d_model + (double)batch * d_model + (double)batch * n_known * c_tok +
+                (double)(n_buf + n_img) * d_model + (double)d_model * c_tok),
+         launch_encoder_input(x_enc, cls, tok, w_z, b_z, pe_enc, known, batch, n_buf, n_img, n_known,
+                              d_model, c_tok, stream));
+  return MARCHE_OK;
+}
+
+size_t marche_encoder_to_decoder_workspace_bytes(int32_t batch, int32_t n_buf, int32_t n_known,
+                                                 int32_t d_model, int32_t dtype) {
+  if (batch < 0 || n_buf < 0 || n_known < 0 || d_model < 0) return 0;
+  return align256((size_t)batch * (n_buf + n_known) * d_model * elem_size(dtype));
+}
+
+marche_status_t marche_encoder_to_decoder(float *x_dec, const float *x_enc, const float *ln_g,
+                                          const float *ln_b, float ln_eps, const void *w_de,
+                                          const float *b_de, const float *mask,
+                                          const float *pe_dec, const int32_t *known,
+                                          const int32_t *rank, int32_t batch, int32_t n_buf,
+                                          int32_t n_img, int32_t n_known, int32_t d_model,
+                                          int32_t dtype, void *workspace, size_t workspace_bytes,
+                                          marche_stream_t stream_) {
+  if (dtype != MARCHE_F32 && dtype != MARCHE_BF16)
+    return fail(MARCHE_ERR_UNSUPPORTED, "dtype=%d is not F32 or BF16", dtype);
+  if (batch < 0 || n_buf < 0 || n_img < 0 || n_buf + n_img < 1 || n_known < 0 || n_known > n_img)
+    return fail(MARCHE_ERR_INVALID_ARG, "batch=%d n_buf=%d n_img=%d n_known=%d inconsistent", batch,
+                n_buf, n_img, n_known);
+  if (d_model < 256 || d_model % 256 != 0 || d_model > 4096)
+    return fail(MARCHE_ERR_UNSUPPORTED, "d_model=%d (must be a multiple of 256, <= 4096)", d_model);
+  if (!(ln_eps > 0.0f)) return fail(MARCHE_ERR_INVALID_ARG, "ln_eps must be > 0");
+  const int32_t n_enc = n_buf + n_known, n_tokens = n_buf + n_img;
+  // the embedding epilogue addresses x_dec and pe_dec with 32-bit offsets
+  if ((int64_t)batch * n_tokens * d_model >= (1LL << 31))
+    return fail(MARCHE_ERR_UNSUPPORTED, "x_dec reaches 2^31 elements");
+  if (batch == 0) return MARCHE_OK;
+  if (!x_dec || !x_enc || !ln_g || !ln_b || !w_de || !b_de || !mask || !pe_dec ||
+      (n_img > 0 && !rank) || (n_known > 0 && !known))
+    return fail(MARCHE_ERR_INVALID_ARG, "NULL input to marche_encoder_to_decoder");
+  const size_t need = marche_encoder_to_decoder_workspace_bytes(batch, n_buf, n_known, d_model, dtype);
+  if (need > 0 && (!workspace || workspace_bytes < need))
+    return fail(MARCHE_ERR_WORKSPACE, "workspace %s: %zu bytes < %zu needed",
+                workspace ? "too small" : "is NULL", workspace_bytes, need);
+  if (reinterpret_cast<uintptr_t>(workspace) & 255)
+    return fail(MARCHE_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  const DType dt = dtype == MARCHE_BF16 ? DType::BF16 : DType::F32;
+  const size_t es = elem_size(dtype);
+  const int M = batch * n_enc, D = d_model;
+  if (M > 0) {
+    LAUNCH(K_LN_ROWS, 0, (double)M * D * (4 + es),
+           launch_ln_rows(dt, workspace, x_enc, nullptr, ln_g, ln_b, nullptr, M, 1, 0, D, ln_eps,
+                          stream));
+    LAUNCH(gemm_class(K_GEMM_EMBED, dt, M, D, D), 2.0 * M * (double)D * D,
+           es * ((double)M * D + (double)D * D) + 4.0 * (double)M * D + 4.0 * (double)n_tokens * D,
+           launch_gemm_embed(dt, workspace, w_de, b_de, M, D, D, x_dec, pe_dec, known, n_enc, n_buf,
+                             n_known, n_tokens, stream));
+  }
+  LAUNCH(K_MASK_FILL, 0, 4.0 * D * (2.0 * batch * (n_img - n_known) + 1) + 4.0 * batch * n_img,
+         launch_mask_fill(x_dec, mask, pe_dec, rank, batch, n_tokens, n_buf, n_known, D, stream));
+  return MARCHE_OK;
+}
+
+namespace {
+
+marche_status_t check_head(const marche_head_t *h) {
+  if (!h) return fail(MARCHE_ERR_INVALID_ARG, "head is NULL");
+  if (h->dtype != MARCHE_F32 && h->dtype != MARCHE_BF16)
+    return fail(MARCHE_ERR_UNSUPPORTED, "head.dtype=%d is not F32 or BF16", h->dtype);
+  if (h->width < 256 || h->width % 256 != 0 || h->width > 4096)
+    return fail(MARCHE_ERR_UNSUPPORTED, "head.width=%d (must be a multiple of 256, <= 4096)", h->width);
+  if (h->d_cond < 256 || h->d_cond % 256 != 0 || h->d_cond > 4096)
+    return fail(MARCHE_ERR_UNSUPPORTED, "head.d_cond=%d (must be a multiple of 256, <= 4096)", h->d_cond);
+  if (h->t_freq < 64 || h->t_freq % 64 != 0 || h->t_freq > 4096)
+    return fail(MARCHE_ERR_UNSUPPORTED, "head.t_freq=%d (must be a multiple of 64, <= 4096)", h->t_freq);
+  if (h->n_blocks < 1 || h->n_blocks > 64)
+    return fail(MARCHE_ERR_UNSUPPORTED, "head.n_blocks=%d (supported: 1..64)", h->n_blocks);
+  if (h->c_tok < 1 || h->c_tok > 64)
+    return fail(MARCHE_ERR_UNSUPPORTED, "head.c_tok=%d (supported: 1..64)", h->c_tok);
+  if (!(h->ln_eps > 0.0f)) return fail(MARCHE_ERR_INVALID_ARG, "head.ln_eps must be > 0");
+  return MARCHE_OK;
+}
+
+// Workspace of the sampler, in carve order.
+struct HeadWs {
+  size_t z, cond, sinus, h1, temb, sc, mod, h, a, y, t, x, total;
+};
+
+HeadWs head_ws(const marche_head_t *hd, int32_t n_rows, int32_t n_steps) {
+  const size_t es = elem_size(hd->dtype), M = (size_t)n_rows, T = (size_t)n_steps;
+  const size_t W = hd->width, nb = hd->n_blocks;
+  HeadWs w{};
+  w.z = align256(M * hd->d_cond * es);
+  w.cond = align256(M * W * 4);
+  w.sinus = align256(T * hd->t_freq * es);
+  w.h1 = align256(T * W * es);
+  w.temb = align256(T * W * 4);
+  w.sc = align256(M * W * es);
+  w.mod = align256(M * (3 * nb + 2) * W * es);
+  w.h = align256(M * W * 4);
+  w.a = align256(M * W * es);
+  w.y = align256(M * W * es);
+  w.t = align256(M * W * 4);
+  w.x = align256(M * hd->c_tok * 4);
+  w.total = w.z + w.cond + w.sinus + w.h1 + w.temb + w.sc + w.mod + w.h + w.a + w.y + w.t + w.x;
+  return w;
+}
+
+}  // namespace
+
+size_t marche_diffusion_workspace_bytes(const marche_head_t *head, int32_t n_rows, int32_t n_steps) {
+  if (check_head(head) != MARCHE_OK || n_rows < 0 || n_steps < 1) return 0;
+  return head_ws(head, n_rows, n_steps).total;
+}
+
+marche_status_t marche_diffusion_sample(const marche_head_t *hd, const marche_head_weights_t *w,
+                                        const float *x_dec, int32_t n_tokens, int32_t n_buf,
+                                        const float *dec_ln_g, const float *dec_ln_b,
+                                        float dec_ln_eps, const float *pe_diff,
+                                        const int32_t *rows, const int32_t *out_rows,
+                                        int32_t n_rows, const float *noise, int32_t n_steps,
+                                        float temperature, float *tok_out, void *workspace,
+                                        size_t workspace_bytes, marche_stream_t stream_) {
+  marche_status_t st = check_head(hd);
+  if (st != MARCHE_OK) return st;
+  if (!w) return fail(MARCHE_ERR_INVALID_ARG, "weights are NULL");
+  if (n_rows < 0) return fail(MARCHE_ERR_INVALID_ARG, "n_rows=%d < 0", n_rows);
+  if (n_steps < 1 || n_steps > 10000)
+    return fail(MARCHE_ERR_INVALID_ARG, "n_steps=%d outside [1, 10000]", n_steps);
+  if (n_tokens < 1 || n_buf < 0 || n_buf >= n_tokens)
+    return fail(MARCHE_ERR_INVALID_ARG, "n_tokens=%d n_buf=%d inconsistent", n_tokens, n_buf);
+  if (!(dec_ln_eps > 0.0f)) return fail(MARCHE_ERR_INVALID_ARG, "dec_ln_eps must be > 0");
+  if (!(temperature >= 0.0f) || temperature > 1e30f)
+    return fail(MARCHE_ERR_INVALID_ARG, "temperature must be finite and >= 0");
+  const int W = hd->width, nb = hd->n_blocks, C = hd->c_tok, D = hd->d_cond, F = hd->t_freq;
+  const int ML = (3 * nb + 2) * W;
+  // GEMM epilogues use 32-bit element offsets
+  if ((int64_t)n_rows * ML >= (1LL << 31) || (int64_t)n_rows * D >= (1LL << 31) ||
+      (int64_t)n_steps * std::max(W, F) >= (1LL << 31))
+    return fail(MARCHE_ERR_UNSUPPORTED, "sampler buffers reach 2^31 elements");
+  if (n_rows == 0) return MARCHE_OK;
+  const void *wp[] = {w->w_t1, w->b_t1, w->w_t2, w->b_t2, w->w_c, w->b_c, w->w_in, w->b_in,
+                      w->w_ada, w->b_ada, w->w_1, w->b_1, w->w_2, w->b_2, w->w_out, w->b_out};
+  for (const void *q : wp)
+    if (!q) return fail(MARCHE_ERR_INVALID_ARG, "a head weight is NULL");
+  if (!x_dec || !dec_ln_g || !dec_ln_b || !pe_diff || !rows || !out_rows || !noise || !tok_out)
+    return fail(MARCHE_ERR_INVALID_ARG, "NULL input to marche_diffusion_sample");
+  const HeadWs L = head_ws(hd, n_rows, n_steps);
+  if (!workspace || workspace_bytes < L.total)
+    return fail(MARCHE_ERR_WORKSPACE, "workspace %s: %zu bytes < %zu needed",
+                workspace ? "too small" : "is NULL", workspace_bytes, L.total);
+  if (reinterpret_cast<uintptr_t>(workspace) & 255)
+    return fail(MARCHE_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  const DType dt = hd->dtype == MARCHE_BF16 ? DType::BF16 : DType::F32;
+  const size_t es = elem_size(hd->dtype);
+  const int M = n_rows, T = n_steps;
+  char *p = static_cast<char *>(workspace);
+  auto take = [&](size_t n) { char *q = p; p += n; return q; };
+  void *z = take(L.z);
+  float *cond = reinterpret_cast<float *>(take(L.cond));
+  void *sinus = take(L.sinus);
+  void *h1 = take(L.h1);
+  float *temb = reinterpret_cast<float *>(take(L.temb));
+  void *sc = take(L.sc);
+  void *mod = take(L.mod);
+  float *hbuf = reinterpret_cast<float *>(take(L.h));
+  void *abuf = take(L.a);
+  void *ybuf = take(L.y);
+  float *tbuf = reinterpret_cast<float *>(take(L.t));
+  float *xs = reinterpret_cast<float *>(take(L.x));
+  auto fp = [](const void *q) { return static_cast<const float *>(q); };
+
+  // condition rows and the time-embedding table (all timesteps)
+  LAUNCH(K_LN_ROWS, 0, (double)M * D * (4 + es) + 4.0 * M * D,
+         launch_ln_rows(dt, z, x_dec, rows, dec_ln_g, dec_ln_b, pe_diff, M, n_tokens, n_buf, D,
+                        dec_ln_eps, stream));
+  LAUNCH(gemm_class(K_GEMM_HEAD, dt, M, W, D), 2.0 * M * (double)W * D,
+         es * ((double)M * D + (double)W * D) + 4.0 * M * W,
+         launch_gemm_plain(dt, z, w->w_c, fp(w->b_c), M, W, D, cond, DType::F32, false, stream));
+  LAUNCH(K_TIME_SINUS, 0, es * (double)T * F, launch_time_sinus(dt, sinus, T, F, stream));
+  LAUNCH(gemm_class(K_GEMM_HEAD_SILU, dt, T, W, F), 2.0 * T * (double)W * F,
+         es * ((double)T * F + (double)W * F + (double)T * W),
+         launch_gemm_plain(dt, sinus, w->w_t1, fp(w->b_t1), T, W, F, h1, dt, true, stream));
+  LAUNCH(gemm_class(K_GEMM_HEAD, dt, T, W, W), 2.0 * T * (double)W * W,
+         es * ((double)T * W + (double)W * W) + 4.0 * T * W,
+         launch_gemm_plain(dt, h1, w->w_t2, fp(w->b_t2), T, W, W, temb, DType::F32, false, stream));
+
+  // cosine schedule (double precision on the host)
+  std::vector<double> betas(T), abar(T);
+  {
+    auto g = [](double u) {
+      const double c = std::cos((u + 0.008) / 1.008 * 1.5707963267948966);
+      return c * c;
+    };
+    double prod = 1.0;
+    for (int i = 0; i < T; ++i) {
+      betas[i] = std::min(1.0 - g((double)(i + 1) / T) / g((double)i / T), 0.999);
+      prod *= 1.0 - betas[i];
+      abar[i] = prod;
+    }
+  }
+  const float *x_init = noise + (size_t)T * M * C;
+  for (int i = T - 1; i >= 0; --i) {
+    const float *xc = i == T - 1 ? x_init : xs;
+    LAUNCH(K_HEAD_SILU_COND, 0, 4.0 * M * W + es * (double)M * W,
+           launch_silu_cond(dt, sc, cond, temb + (size_t)i * W, M, W, stream));
+    LAUNCH(gemm_class(K_GEMM_HEAD, dt, M, ML, W), 2.0 * M * (double)ML * W,
+           es * ((double)M * W + (double)ML * W + (double)M * ML),
+           launch_gemm_plain(dt, sc, w->w_ada, fp(w->b_ada), M, ML, W, mod, dt, false, stream));
+    LAUNCH(K_HEAD_IN_MOD, 2.0 * M * (double)W * C,
+           4.0 * M * C + 4.0 * M * W + es * 3.0 * M * W,
+           launch_head_in_mod(dt, abuf, hbuf, xc, fp(w->w_in), fp(w->b_in), mod, ML, M, W, C,
+                              hd->ln_eps, stream));
+    for (int k = 0; k < nb; ++k) {
+      const char *w1 = static_cast<const char *>(w->w_1) + (size_t)k * W * W * es;
+      const char *w2 = static_cast<const char *>(w->w_2) + (size_t)k * W * W * es;
+      LAUNCH(gemm_class(K_GEMM_HEAD_SILU, dt, M, W, W), 2.0 * M * (double)W * W,
+             es * (2.0 * M * W + (double)W * W),
+             launch_gemm_plain(dt, abuf, w1, fp(w->b_1) + (size_t)k * W, M, W, W, ybuf, dt, true,
+                               stream));
+      LAUNCH(gemm_class(K_GEMM_HEAD, dt, M, W, W), 2.0 * M * (double)W * W,
+             es * ((double)M * W + (double)W * W) + 4.0 * M * W,
+             launch_gemm_plain(dt, ybuf, w2, fp(w->b_2) + (size_t)k * W, M, W, W, tbuf,
+                               DType::F32, false, stream));
+      // the next modulated norm: block k + 1's, or the final layer's
+      const int nxt = 3 * (k + 1) * W;
+      LAUNCH(K_HEAD_GATE_MOD, 0, 4.0 * 3.0 * M * W + es * 4.0 * M * W,
+             launch_head_gate_mod(dt, abuf, hbuf, tbuf, mod, ML, 3 * k * W + 2 * W, nxt, nxt + W,
+                                  M, W, hd->ln_eps, stream));
+    }
+    const double ab = abar[i], abp = i > 0 ? abar[i - 1] : 1.0, b = betas[i];
+    HeadStep hs;
+    hs.sra = (float)(1.0 / std::sqrt(ab));
+    hs.srm1 = (float)std::sqrt(1.0 / ab - 1.0);
+    hs.c1 = (float)(b * std::sqrt(abp) / (1.0 - ab));
+    hs.c2 = (float)((1.0 - abp) * std::sqrt(1.0 - b) / (1.0 - ab));
+    hs.sigma = i > 0 ? (float)(temperature * std::sqrt(b * (1.0 - abp) / (1.0 - ab))) : 0.0f;
+    LAUNCH(K_HEAD_OUT_STEP, 2.0 * M * (double)W * C,
+           es * (double)M * W + 4.0 * ((double)C * W + 3.0 * M * C),
+           launch_head_out_step(dt, xs, i == 0 ? tok_out : nullptr, abuf, fp(w->w_out),
+                                fp(w->b_out), xc, noise + (size_t)i * M * C, out_rows, M, W, C,
+                                hs, stream));
+  }
   return MARCHE_OK;
 }
 

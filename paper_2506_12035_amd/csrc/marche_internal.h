@@ -37,6 +37,44 @@ hipError_t launch_decoder_input(float *x, const float *cls, const float *value, 
                                 hipStream_t s);
 hipError_t launch_fill_zero(void *dst, size_t bytes, hipStream_t s);
 
+// ---- the rest of a MAR step (k_mar.hip) ----
+// Encoder input rows [batch][n_buf + n_known][d_model] (Eq. 1).
+hipError_t launch_encoder_input(float *x, const float *cls, const float *tok, const float *w_z,
+                                const float *b_z, const float *pe, const int32_t *known,
+                                int32_t batch, int32_t n_buf, int32_t n_img, int32_t n_known,
+                                int32_t d_model, int32_t c_tok, hipStream_t s);
+// Masked rows of the decoder input (Eq. 2).
+hipError_t launch_mask_fill(float *x, const float *mask, const float *pe, const int32_t *rank,
+                           int32_t batch, int32_t n_tokens, int32_t n_buf, int32_t n_known,
+                           int32_t d_model, hipStream_t s);
+// out[r] = LN(x[rows ? rows[r] : r]) * g + b (+ add[src % n_tokens - n_buf]).
+hipError_t launch_ln_rows(DType dt, void *out, const float *x, const int32_t *rows_idx,
+                          const float *g, const float *b, const float *add, int32_t rows,
+                          int32_t n_tokens, int32_t n_buf, int32_t d_model, float eps,
+                          hipStream_t s);
+// Sinusoidal time embedding table [n_steps][freq].
+hipError_t launch_time_sinus(DType dt, void *out, int32_t n_steps, int32_t freq, hipStream_t s);
+// sc = SiLU(cond + temb_row), [rows][width].
+hipError_t launch_silu_cond(DType dt, void *sc, const float *cond, const float *temb, int32_t rows,
+                            int32_t width, hipStream_t s);
+// h = w_in x + b_in; a = LN(h) (1 + scale) + shift with block 0's modulation.
+hipError_t launch_head_in_mod(DType dt, void *a, float *h, const float *x, const float *w_in,
+                              const float *b_in, const void *mod, int32_t mod_ld, int32_t rows,
+                              int32_t width, int32_t c_tok, float eps, hipStream_t s);
+// h += gate t; a = LN(h) (1 + scale) + shift (slices of mod at the offsets).
+hipError_t launch_head_gate_mod(DType dt, void *a, float *h, const float *t, const void *mod,
+                                int32_t mod_ld, int32_t gate_off, int32_t shift_off,
+                                int32_t scale_off, int32_t rows, int32_t width, float eps,
+                                hipStream_t s);
+// Coefficients of one DDPM step (see head_out_step_kernel).
+struct HeadStep {
+  float sra, srm1, c1, c2, sigma;
+};
+hipError_t launch_head_out_step(DType dt, float *x_next, float *tok_out, const void *a,
+                                const float *w_out, const float *b_out, const float *x_cur,
+                                const float *noise, const int32_t *out_rows, int32_t rows,
+                                int32_t width, int32_t c_tok, const HeadStep &st, hipStream_t s);
+
 // ---- GEMMs with fused epilogues (k_gemm.hip) ----
 // C[M][N] = A[M][K] . W[N][K]^T (+ bias) followed by one epilogue:
 //   qkv:   columns [0,D) -> q [M][D]; [D,2D) -> K cache, [2D,3D) -> V cache
@@ -59,6 +97,18 @@ hipError_t launch_gemm_gelu(DType dt, const void *a, const void *w, const float 
                             int32_t n, int32_t k, void *h, hipStream_t s);
 // Whether a bf16 GEMM of this shape runs on the 256x256 tile (else 128x128);
 // each tile is its own kernel symbol.
+// Sampler GEMMs: out[r][c] = act(C + bias) as out_dt (row-major, ld = n), act
+// SiLU or the identity; a float32 GEMM writes float32 only.
+hipError_t launch_gemm_plain(DType dt, const void *a, const void *w, const float *bias, int32_t m,
+                             int32_t n, int32_t k, void *out, DType out_dt, bool silu_act,
+                             hipStream_t s);
+// Decoder embedding of the encoder rows scattered to their sequence positions
+// (n = d_model): x[b][j][c] = C + bias + pe[j][c], j the position encoder row
+// r = b * n_enc + i holds (i < n_buf: i; else n_buf + known[b][i - n_buf]).
+hipError_t launch_gemm_embed(DType dt, const void *a, const void *w, const float *bias, int32_t m,
+                             int32_t n, int32_t k, float *x, const float *pe, const int32_t *known,
+                             int32_t n_enc, int32_t n_buf, int32_t n_known, int32_t n_tokens,
+                             hipStream_t s);
 // bf16 GEMM workgroup tile for an M x N x K product: 128x256 (two workgroups
 // per CU) or 256x256 (one per CU).
 enum GemmTile { GEMM_TILE_128x256 = 0, GEMM_TILE_256 = 1 };

@@ -280,3 +280,104 @@ def segment_case(batch: int, n_heads: int, head_dim: int, n_active: int, n_cache
                        draw(batch, n_heads, n_active, head_dim),
                        draw(batch, n_heads, n_cached, head_dim),
                        draw(batch, n_heads, n_cached, head_dim))
+
+
+# ------------------------------------------------------------------ the rest of a MAR step
+
+@dataclass(frozen=True)
+class MarConfig:
+    """A whole MAR model around the cache-aware decoder (latency workloads):
+    the encoder stack over the known tokens (Eq. 1), the decoder stack
+    ``dec`` (Eq. 2, the cache-aware step), and the sampler head of Eq. 3
+    (``head_blocks`` modulated residual MLP blocks of width ``head_width`` over
+    ``c_tok``-channel token values, ``sample_steps`` DDPM steps)."""
+
+    name: str
+    dec: Config
+    enc_layers: int
+    head_width: int
+    head_blocks: int
+    c_tok: int = 16
+    t_freq: int = 256
+    sample_steps: int = 100
+    temperature: float = 1.0
+    head_eps: float = 1e-6
+    head_std: float = 0.02
+
+    @property
+    def enc(self) -> Config:
+        """The encoder stack: the decoder's block shape, its own depth and weights."""
+        return self.dec.with_(n_layers=self.enc_layers, seed=self.dec.seed_value + 7919)
+
+
+# MAR-L end to end (the scales the paper adopts from MAR: 16 encoder and 16
+# decoder blocks of width 1024, a head of 8 blocks of width 1280, 16-channel
+# tokens, 100 sampling steps), and a tiny case for parity tests.
+MAR_CONFIGS: Dict[str, MarConfig] = {
+    "mar-l-e2e": MarConfig("mar-l-e2e-enc16-dec16-head8x1280-B128",
+                           CONFIGS[3].with_(n_layers=16, name="mar-l-dec16-B128"),
+                           enc_layers=16, head_width=1280, head_blocks=8),
+    "tiny": MarConfig("tiny-e2e", Config(90, "tiny-dec", 2, 256, 4, 64, 1024, 36, 4, 3, "bf16",
+                                         n_steps=6),
+                      enc_layers=2, head_width=256, head_blocks=2, sample_steps=8,
+                      head_std=0.08),
+}
+
+
+def mar_embeddings(mc: MarConfig, batch: Optional[int] = None) -> Dict[str, np.ndarray]:
+    """Embeddings and the two LayerNorms around the stacks (float32; ``w_de``
+    rounded to the model dtype): cls [B][D], w_z [D][C], b_z [D], pe_enc and
+    pe_dec [N][D], enc_ln_g/b, w_de [D][D], b_de, mask [D], dec_ln_g/b,
+    pe_diff [N_img][D]."""
+    cfg = mc.dec
+    B = cfg.batch if batch is None else batch
+    ss = np.random.SeedSequence([cfg.seed_value, 31])
+    rng = np.random.Generator(np.random.PCG64(ss))
+    D, N, C = cfg.d_model, cfg.n_tokens, mc.c_tok
+    s = cfg.weight_std
+    out = {
+        "cls": rng.standard_normal((cfg.batch, D), dtype=np.float32)[:B].copy(),
+        "w_z": _normal(rng, (D, C), 0.25),
+        "b_z": _normal(rng, (D,), s),
+        "pe_enc": rng.standard_normal((N, D), dtype=np.float32),
+        "enc_ln_g": 1.0 + _normal(rng, (D,), s),
+        "enc_ln_b": _normal(rng, (D,), s),
+        "w_de": round_to(_normal(rng, (D, D), s), cfg.dtype),
+        "b_de": _normal(rng, (D,), s),
+        "mask": rng.standard_normal((D,), dtype=np.float32),
+        "pe_dec": rng.standard_normal((N, D), dtype=np.float32),
+        "dec_ln_g": 1.0 + _normal(rng, (D,), s),
+        "dec_ln_b": _normal(rng, (D,), s),
+        "pe_diff": rng.standard_normal((cfg.n_img, D), dtype=np.float32),
+    }
+    return out
+
+
+def head_weights(mc: MarConfig) -> Dict[str, np.ndarray]:
+    """Sampler head parameters (nn.Linear layout): the GEMM weights w_t1, w_t2,
+    w_c, w_ada [(3n+2)W][W], w_1 and w_2 [n][W][W] rounded to the model dtype;
+    w_in [W][C], w_out [C][W] and all biases float32."""
+    cfg = mc.dec
+    ss = np.random.SeedSequence([cfg.seed_value, 37])
+    rng = np.random.Generator(np.random.PCG64(ss))
+    W, n, C, D, Ft, s = mc.head_width, mc.head_blocks, mc.c_tok, cfg.d_model, mc.t_freq, mc.head_std
+    r = lambda a: round_to(a, cfg.dtype)
+    return {
+        "w_t1": r(_normal(rng, (W, Ft), s)), "b_t1": _normal(rng, (W,), s),
+        "w_t2": r(_normal(rng, (W, W), s)), "b_t2": _normal(rng, (W,), s),
+        "w_c": r(_normal(rng, (W, D), s)), "b_c": _normal(rng, (W,), s),
+        "w_in": _normal(rng, (W, C), 0.25), "b_in": _normal(rng, (W,), s),
+        "w_ada": r(_normal(rng, ((3 * n + 2) * W, W), s)), "b_ada": _normal(rng, ((3 * n + 2) * W,), s),
+        "w_1": r(_normal(rng, (n, W, W), s)), "b_1": _normal(rng, (n, W), s),
+        "w_2": r(_normal(rng, (n, W, W), s)), "b_2": _normal(rng, (n, W), s),
+        "w_out": _normal(rng, (C, W), s), "b_out": _normal(rng, (C,), s),
+    }
+
+
+def head_noise(mc: MarConfig, t: int, n_rows: int) -> np.ndarray:
+    """The sampler's draws for decoding step ``t``: [sample_steps + 1][n_rows][C]
+    standard normal (index sample_steps is the initial x, index i the noise of
+    sampling step i)."""
+    ss = np.random.SeedSequence([mc.dec.seed_value, 41, t])
+    rng = np.random.Generator(np.random.PCG64(ss))
+    return rng.standard_normal((mc.sample_steps + 1, n_rows, mc.c_tok), dtype=np.float32)

@@ -178,3 +178,79 @@ def test_attention_segments_validation_and_workspace():
     assert call(mode=cat) == binding.MARCHE_ERR_WORKSPACE
     assert call(mode=cat, ws=FAKE, ws_bytes=need - 1) == binding.MARCHE_ERR_WORKSPACE
     assert call(mode=cat, ws=FAKE + 16, ws_bytes=need) == binding.MARCHE_ERR_INVALID_ARG
+
+
+def test_encoder_and_decoder_input_validation():
+    L = binding.lib()
+    f32, bf16 = binding.MARCHE_F32, binding.MARCHE_BF16
+
+    def enc(batch=2, n_buf=4, n_img=32, n_known=8, d=256, c=16, x=FAKE, known=FAKE):
+        return L.marche_encoder_input(x, FAKE, FAKE, FAKE, FAKE, FAKE, known, batch, n_buf, n_img,
+                                      n_known, d, c, None)
+
+    assert enc(n_known=33) == binding.MARCHE_ERR_INVALID_ARG
+    assert enc(d=320) == binding.MARCHE_ERR_UNSUPPORTED
+    assert enc(c=65) == binding.MARCHE_ERR_UNSUPPORTED
+    assert enc(x=None) == binding.MARCHE_ERR_INVALID_ARG
+    assert enc(known=None) == binding.MARCHE_ERR_INVALID_ARG
+    assert enc(batch=0) == binding.MARCHE_OK  # nothing to do: no HIP call
+
+    def e2d(dtype=bf16, n_known=8, d=256, ws=FAKE, ws_bytes=1 << 20, eps=1e-6, batch=2, rank=FAKE):
+        return L.marche_encoder_to_decoder(FAKE, FAKE, FAKE, FAKE, eps, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                           rank, batch, 4, 32, n_known, d, dtype, ws, ws_bytes, None)
+
+    assert e2d(dtype=5) == binding.MARCHE_ERR_UNSUPPORTED
+    assert e2d(n_known=-1) == binding.MARCHE_ERR_INVALID_ARG
+    assert e2d(d=100) == binding.MARCHE_ERR_UNSUPPORTED
+    assert e2d(eps=0.0) == binding.MARCHE_ERR_INVALID_ARG
+    assert e2d(rank=None) == binding.MARCHE_ERR_INVALID_ARG
+    need = binding.encoder_to_decoder_workspace_bytes(2, 4, 8, 256, bf16)
+    assert need == (2 * 12 * 256 * 2 + 255) // 256 * 256
+    assert binding.encoder_to_decoder_workspace_bytes(2, 4, 8, 256, f32) == 2 * 12 * 256 * 4
+    assert e2d(ws=None) == binding.MARCHE_ERR_WORKSPACE
+    assert e2d(ws_bytes=need - 1) == binding.MARCHE_ERR_WORKSPACE
+    assert e2d(ws=FAKE + 16) == binding.MARCHE_ERR_INVALID_ARG
+    assert e2d(batch=0) == binding.MARCHE_OK
+
+
+def test_diffusion_sample_validation_and_workspace():
+    L = binding.lib()
+    bf16 = binding.MARCHE_BF16
+    wts = binding.HeadWeights(*([FAKE] * 16))
+
+    def call(head=None, n_rows=10, n_steps=8, ws=FAKE, ws_bytes=1 << 30, tau=1.0, weights=wts,
+             noise=FAKE, n_tokens=36, n_buf=4):
+        hd = head or binding.make_head(256, 2, 16, 256, 256, bf16, 1e-6)
+        return L.marche_diffusion_sample(C.byref(hd), C.byref(weights), FAKE, n_tokens, n_buf, FAKE,
+                                         FAKE, 1e-6, FAKE, FAKE, FAKE, n_rows, noise, n_steps, tau,
+                                         FAKE, ws, ws_bytes, None)
+
+    for kw, status in [(dict(width=300), binding.MARCHE_ERR_UNSUPPORTED),
+                       (dict(n_blocks=0), binding.MARCHE_ERR_UNSUPPORTED),
+                       (dict(c_tok=65), binding.MARCHE_ERR_UNSUPPORTED),
+                       (dict(d_cond=128), binding.MARCHE_ERR_UNSUPPORTED),
+                       (dict(t_freq=96), binding.MARCHE_ERR_UNSUPPORTED),
+                       (dict(dtype=7), binding.MARCHE_ERR_UNSUPPORTED),
+                       (dict(ln_eps=0.0), binding.MARCHE_ERR_INVALID_ARG)]:
+        h = dict(width=256, n_blocks=2, c_tok=16, d_cond=256, t_freq=256, dtype=bf16, ln_eps=1e-6)
+        h.update(kw)
+        assert call(head=binding.make_head(**h)) == status, kw
+    assert call(n_steps=0) == binding.MARCHE_ERR_INVALID_ARG
+    assert call(n_steps=10001) == binding.MARCHE_ERR_INVALID_ARG
+    assert call(n_rows=-1) == binding.MARCHE_ERR_INVALID_ARG
+    assert call(tau=-1.0) == binding.MARCHE_ERR_INVALID_ARG
+    assert call(tau=float("nan")) == binding.MARCHE_ERR_INVALID_ARG
+    assert call(n_buf=36) == binding.MARCHE_ERR_INVALID_ARG
+    assert call(noise=None) == binding.MARCHE_ERR_INVALID_ARG
+    assert call(weights=binding.HeadWeights(*([FAKE] * 15 + [None]))) == binding.MARCHE_ERR_INVALID_ARG
+    assert call(n_rows=0) == binding.MARCHE_OK
+    hd = binding.make_head(256, 2, 16, 256, 256, bf16, 1e-6)
+    need = binding.diffusion_workspace_bytes(hd, 10, 8)
+    a = lambda v: (v + 255) // 256 * 256
+    W, M, T = 256, 10, 8
+    assert need == (a(M * 256 * 2) + a(M * W * 4) + a(T * 256 * 2) + a(T * W * 2) + a(T * W * 4) +
+                    a(M * W * 2) + a(M * 8 * W * 2) + a(M * W * 4) + 2 * a(M * W * 2) + a(M * W * 4) +
+                    a(M * 16 * 4))
+    assert call(ws=None) == binding.MARCHE_ERR_WORKSPACE
+    assert call(ws_bytes=need - 1) == binding.MARCHE_ERR_WORKSPACE
+    assert call(ws=FAKE + 64) == binding.MARCHE_ERR_INVALID_ARG
