@@ -80,7 +80,8 @@ def traffic_for(kernel: str, workload: str):
 
 def counter_class(name: str):
     """Timing class of a kernel symbol as rocprofv3 prints it (mangled or not)."""
-    tile = "t256" if "gemm_bf16_big_kernel" in name else "t128x256"
+    tile = ("t256" if "gemm_bf16_big_kernel" in name else
+            "t64x128" if "gemm_bf16_small_kernel" in name else "t128x256")
     if "gemm_bf16" in name:
         for key, cls in (("EpiResidILi1E", "fc2"), ("EpiResid<1>", "fc2"), ("EpiResidILi0E", "o"),
                          ("EpiResid<0>", "o"), ("EpiGelu", "fc1"), ("EpiQkv", "qkv")):
@@ -317,6 +318,81 @@ def appb_main(args) -> int:
     return 0
 
 
+def e2e_main(args) -> int:
+    """Whole MAR generations (encoder, cache-aware decoder, sampler) at MAR-L
+    sizes: seconds per image for the paper's schedule and for full recompute of
+    the decoder with the same encoder and sampler, with a per-phase split."""
+    import torch
+
+    from paper_2506_12035_amd import binding, driver, workload
+
+    mc = workload.MAR_CONFIGS[args.e2e_config]
+    log(f"[e2e] {mc.name}: building the engine")
+    eng = driver.MarEngine(mc)
+    B, T = eng.B, mc.dec.n_steps
+
+    def generation():
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        eng.generate()
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0
+
+    def phases():
+        ev = {k: [] for k in ("encoder", "decoder", "sampler")}
+        eng.tok.zero_()
+        for t in eng.steps:
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            e[0].record()
+            eng.encode(t)
+            e[1].record()
+            eng.dec.step(t, build_input=False)
+            e[2].record()
+            eng.sample(t)
+            e[3].record()
+            for i, k in enumerate(ev):
+                ev[k].append((e[i], e[i + 1]))
+        torch.cuda.synchronize()
+        return {k: sum(a.elapsed_time(b) for a, b in v) for k, v in ev.items()}
+
+    log("[e2e] warmup generation")
+    generation()
+    log("[e2e] timed generation")
+    wall = generation()
+    split = phases()
+    log(f"[e2e] {wall / B * 1e3:.2f} ms/image; per generation (ms): {split}")
+    binding.profile_reset()
+    binding.profile_enable(True)
+    eng.generate()
+    prof = binding.profile_collect()
+    binding.profile_enable(False)
+    rates = kernel_rates(prof, mc.dec.dtype)
+
+    eng.dec.set_schedule(1, "ratio", 10000)
+    generation()
+    fwall = generation()
+    fsplit = phases()
+    eng.dec.set_schedule(mc.dec.full_every, "ratio", mc.dec.ratio_bp)
+    log(f"[e2e] full recompute: {fwall / B * 1e3:.2f} ms/image -> speedup {fwall / wall:.3f}")
+    out = {
+        "metric": "MAR end-to-end generation latency (encoder + decoder + sampler), s/image",
+        "value": wall / B, "unit": "s/image", "higher_is_better": False, "n_gpus": 1,
+        "images_per_s": B / wall, "dtype": mc.dec.dtype, "data": "synthetic",
+        "config": {"workload": mc.name, "batch": B, "decode_steps": T,
+                   "encoder_layers": mc.enc_layers, "decoder_layers": mc.dec.n_layers,
+                   "d_model": mc.dec.d_model, "head_blocks": mc.head_blocks,
+                   "head_width": mc.head_width, "token_channels": mc.c_tok,
+                   "sampling_steps": mc.sample_steps, "refresh_ratio": mc.dec.ratio_bp / 10000,
+                   "full_every": mc.dec.full_every, "sel_layer": mc.dec.sel_layer},
+        "phase_ms_per_generation": split,
+        "full_recompute": {"s_per_image": fwall / B, "phase_ms_per_generation": fsplit},
+        "speedup_vs_full_recompute": fwall / wall,
+        "kernels": rates,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def ingest_main(args) -> int:
     from paper_2506_12035_amd import schedule, workload
 
@@ -374,6 +450,11 @@ def main() -> int:
                     help="only run Appendix B's comparison: attention over an active and a cached "
                          "segment, concatenate-then-attend vs the two-segment pass vs one resident "
                          "buffer, MAR-L heads at batch 128, over a sweep of segment lengths")
+    ap.add_argument("--e2e", action="store_true",
+                    help="only time whole MAR generations: encoder over the known tokens, the "
+                         "cache-aware decoder and the sampler (s/image), against full recompute "
+                         "of the decoder with the same encoder and sampler")
+    ap.add_argument("--e2e-config", default="mar-l-e2e", help="whole-model workload name")
     ap.add_argument("--ingest-counters", nargs=5, default=None,
                     metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV", "BENCH_JSON"),
                     help="write profiles/traffic.json from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE "
@@ -404,6 +485,8 @@ def main() -> int:
         return 1
     if args.appb:
         return appb_main(args)
+    if args.e2e:
+        return e2e_main(args)
     if args.calibrate_copy:
         n = args.calibrate_copy * (1 << 20) // 4
         src = torch.arange(n, dtype=torch.float32, device="cuda")

@@ -290,50 +290,54 @@ __device__ __forceinline__ void barrier() {
 // Write-back through LDS (free once the main loop is done).  In the
 // accumulator layout a store instruction would write 16 bytes into each of
 // 32 rows; instead each wavefront writes one 32-row block of its accumulators
-// (128 columns wide) to LDS as fp32 and reads it back row-major, so lane l
-// owns columns 4 (l % 32) .. + 3 of rows l / 32 + 2k: one store instruction
-// then covers two whole 128-column row segments.  Per-row addressing data of
-// the tile were staged in LDS by the caller; residual priors of the next
-// batch of rows are loaded before this batch's stores.
+// to LDS as fp32 and reads it back row-major, so one store instruction covers
+// whole row segments (two rows of 128 columns, or four of 64).  Per-row
+// addressing data of the tile were staged in LDS by the caller; residual
+// priors of the next batch of rows are loaded before this batch's stores.
 namespace big {
 constexpr int kWbStride = 132;  // floats per staged row (128 + 4: no bank conflicts)
 static_assert(4 * 32 * kWbStride * 4 <= 2 * kStage, "staged write-back fits the stages");
 }  // namespace big
 
-// One wavefront's TM 32-row blocks of 128 columns (accumulators acc[j][i]:
+// One wavefront's TM 32-row blocks of TN * 32 columns (accumulators acc[j][i]:
 // column block j, row block i) starting at output row row0 and column col0.
-// `st` is this wavefront's staging area (32 rows of kWbStride floats), `rows`
-// the row records of rows row0.. (in LDS), `b` the bias of this lane's four
-// columns col0 + 4 (lane % 32) .. + 3.  Residual priors are loaded PB rows at
-// a time, each batch before the stores of the previous one.
-template <int TM, int PB, class Epi>
-__device__ __forceinline__ void write_back_staged(const f32x16 (&acc)[4][TM], const Epi &epi,
+// Each block goes through the wavefront's staging area `st` (32 rows of
+// TN * 32 + 4 floats) and is read back with TN * 8 lanes per row, so lane l
+// owns columns 4 (l % (8 TN)) .. + 3 of rows l / (8 TN) + (64 / (8 TN)) k.
+// `rows` are the row records of rows row0.. (in LDS), `b` the bias of this
+// lane's four columns.  Residual priors are loaded PB rows at a time, each
+// batch before the stores of the previous one.
+template <int TN, int TM, int PB, class Epi>
+__device__ __forceinline__ void write_back_staged(const f32x16 (&acc)[TN][TM], const Epi &epi,
                                                   int row0, int col0, int M, int lane, float *st,
                                                   const typename Epi::Row *rows, f32x4 b) {
-  using namespace big;
-  static_assert(16 % PB == 0, "prior batches");
-  constexpr int NB = 16 / PB;  // batches per 32-row block
-  const int c4 = (lane & 31) * 4, half = lane >> 5;
+  constexpr int LPR = TN * 8;      // lanes per output row
+  constexpr int RPP = 64 / LPR;    // rows per store instruction
+  constexpr int KP = 32 / RPP;     // store instructions per 32-row block
+  constexpr int STR = TN * 32 + 4; // staged row stride (floats): no bank conflicts
+  static_assert(KP % PB == 0, "prior batches");
+  constexpr int NB = KP / PB;      // batches per 32-row block
+  const int c4 = (lane % LPR) * 4, rsub = lane / LPR, half = lane >> 5;
   const typename Epi::Col col = epi.col(col0 + c4);
   f32x4 pr[2][PB];  // residual priors; zero for epilogues without one
 #pragma unroll
   for (int k = 0; k < PB; ++k) pr[0][k] = pr[1][k] = f32x4{};
-  // batch u: block u / NB, rows half + 2 k for k in [(u % NB) PB, + PB)
+  // batch u: block u / NB, rows rsub + RPP k for k in [(u % NB) PB, + PB)
   auto load_priors = [&](int u, f32x4 (&dst)[PB]) {
     const int i = u / NB, k0 = (u % NB) * PB;
 #pragma unroll
     for (int k = 0; k < PB; ++k)
-      dst[k] = Epi::kPrior ? epi.prior(rows[i * 32 + half + 2 * (k0 + k)], col) : f32x4{};
+      dst[k] = Epi::kPrior ? epi.prior(rows[i * 32 + rsub + RPP * (k0 + k)], col) : f32x4{};
   };
   if constexpr (Epi::kPrior) load_priors(0, pr[0]);
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     // block row i of the accumulators -> LDS rows 0..31 of this wavefront
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int g = 0; g < 4; ++g)
-        *reinterpret_cast<f32x4 *>(st + (lane & 31) * kWbStride + j * 32 + g * 8 + half * 4) =
+        *reinterpret_cast<f32x4 *>(st + (lane & 31) * STR + j * 32 + g * 8 + half * 4) =
             f32x4{acc[j][i][4 * g + 0], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2],
                   acc[j][i][4 * g + 3]};
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -345,7 +349,7 @@ __device__ __forceinline__ void write_back_staged(const f32x16 (&acc)[4][TM], co
       f32x4 v[PB];
 #pragma unroll
       for (int k = 0; k < PB; ++k)
-        v[k] = *reinterpret_cast<const f32x4 *>(st + (half + 2 * (nb * PB + k)) * kWbStride + c4);
+        v[k] = *reinterpret_cast<const f32x4 *>(st + (rsub + RPP * (nb * PB + k)) * STR + c4);
       if constexpr (Epi::kPrior) {
         if (u + 1 < TM * NB) load_priors(u + 1, pr[(u + 1) & 1]);
 #pragma unroll
@@ -358,13 +362,13 @@ __device__ __forceinline__ void write_back_staged(const f32x16 (&acc)[4][TM], co
       if (full) {
 #pragma unroll
         for (int k = 0; k < PB; ++k) {
-          const int r = half + 2 * (nb * PB + k);
+          const int r = rsub + RPP * (nb * PB + k);
           epi.store(rows[i * 32 + r], rbase + r, col, value(k));
         }
       } else {
 #pragma unroll
         for (int k = 0; k < PB; ++k) {
-          const int r = half + 2 * (nb * PB + k);
+          const int r = rsub + RPP * (nb * PB + k);
           if (rbase + r < M) epi.store(rows[i * 32 + r], rbase + r, col, value(k));
         }
       }
@@ -481,7 +485,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
   barrier();
   const f32x4 b = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(side) +
                                                     wn * 128 + (lane & 31) * 4);
-  write_back_staged<4, 16>(acc, epi, m0 + wm * 128, n0 + wn * 128, M, lane,
+  write_back_staged<4, 4, 16>(acc, epi, m0 + wm * 128, n0 + wn * 128, M, lane,
                            reinterpret_cast<float *>(smem) + wave * 32 * kWbStride,
                            reinterpret_cast<const typename Epi::Row *>(side + 1024) + wm * 128, b);
 }
@@ -665,9 +669,154 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_pair_kernel(const bf16 *A, c
   // every wavefront is done with the stages before they hold the write-back's
   // staging rows, and the row records are in LDS
   barrier_vm<0>();
-  write_back_staged<2, 8>(acc, epi, m0 + wm * 64, n0 + wn * 128, M, lane,
+  write_back_staged<4, 2, 8>(acc, epi, m0 + wm * 64, n0 + wn * 128, M, lane,
                           reinterpret_cast<float *>(smem) + wave * 32 * big::kWbStride,
                           rows_lds + wm * 64, bias);
+}
+
+// ------------------------------------------------------------------ 64x128 tile
+//
+// For products too small to spread 128x256 tiles over the chip (the sampler's
+// MLP on a few hundred rows, a shard of a few images): a 64x128x128 tile on
+// four wavefronts of 32x64 (2 accumulator blocks).  With so little work per
+// workgroup its time is the serial chain of k-tiles (barrier, LDS round trip,
+// dependent MFMAs), not bandwidth, so the k-tile is long: three 48 KB stages
+// of 256-byte rows (16-byte chunks XOR-permuted by the row's low four bits,
+// so 16 rows read at one chunk hit 16 distinct bank groups), one barrier per
+// 128 of K, the next k16 step's fragments read while the current one's MFMAs
+// run, and the loads of k-tile t+3 issued once every wavefront is done with
+// k-tile t.
+namespace small {
+
+constexpr int kBM = 64, kBN = 128, kBK = 128;
+constexpr int kRow = kBK * 2;                  // 256-byte rows
+constexpr int kWOff = kBM * kRow;              // weight rows start 16 KB into a stage
+constexpr int kStage = (kBM + kBN) * kRow;     // 48 KB
+constexpr int kLoads = kStage / 1024 / 4;      // load instructions per wavefront per k-tile
+static_assert(kLoads == 12, "load count per wavefront");
+
+__device__ __forceinline__ int swz(int r, int c) { return c ^ (r & 15); }
+
+struct Frag {
+  bf16x8 x;     // activation rows (MFMA B operand)
+  bf16x8 w[2];  // weight rows (MFMA A operand)
+};
+
+// Load instruction q (0..47 per k-tile) moves 1 KB = four 256-byte rows:
+// q < 16 carries activation rows 4q..4q+3, q >= 16 weight rows 4(q-16)..;
+// lane l writes LDS bytes [16 l, 16 l + 16): row 4 q' + l / 16 at physical
+// chunk l % 16.
+__device__ __forceinline__ void load_lds(unsigned stage, int q, const bf16 *A, const bf16 *W,
+                                         int M, int K, int m0, int n0, int k0, int lane) {
+  const int rr = lane >> 4, pc = lane & 15;
+  const bf16 *g;
+  if (q < 16) {
+    const int r = q * 4 + rr;
+    g = A + (size_t)min(m0 + r, M - 1) * K + k0 + swz(r, pc) * 8;
+  } else {
+    const int r = (q - 16) * 4 + rr;
+    g = W + (size_t)(n0 + r) * K + k0 + swz(r, pc) * 8;
+  }
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(g), "s"(__builtin_amdgcn_readfirstlane(stage + q * 1024))
+               : "memory", "m0");
+}
+
+// Fragments of k16 step s (0..7) of a stage.
+__device__ __forceinline__ void read_frags(Frag &f, const unsigned char *stage, int s, int wm,
+                                           int wn, int lane) {
+  const int c = 2 * s + (lane >> 5);
+  const int xr = wm * 32 + (lane & 31);
+  f.x = *reinterpret_cast<const bf16x8 *>(stage + xr * kRow + swz(xr, c) * 16);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int wr = wn * 64 + j * 32 + (lane & 31);
+    f.w[j] = *reinterpret_cast<const bf16x8 *>(stage + kWOff + wr * kRow + swz(wr, c) * 16);
+  }
+}
+
+__device__ __forceinline__ void mfma(f32x16 (&acc)[2][1], const Frag &f) {
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+    acc[j][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.w[j], f.x, acc[j][0], 0, 0, 0);
+}
+
+}  // namespace small
+
+template <class Epi>
+__global__ __launch_bounds__(256) void gemm_bf16_small_kernel(const bf16 *A, const bf16 *W, int M,
+                                                              int N, int K, Epi epi) {
+  using namespace small;
+  using pair::barrier_vm;
+  using big::pin;
+  using Row = typename Epi::Row;
+  constexpr int kStr = 2 * 32 + 4;  // staged write-back row (floats)
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[3 * kStage];
+  __shared__ __attribute__((aligned(16))) Row rows_lds[kBM];
+  static_assert(4 * 32 * kStr * 4 <= 3 * kStage, "staged write-back fits the stages");
+  const int tiles_m = (M + kBM - 1) / kBM, tiles_n = N / kBN;
+  int tm, tn;
+  tile_coords(xcd_remap(blockIdx.x, gridDim.x), tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * kBM, n0 = tn * kBN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int q0 = wave * kLoads;
+  const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void *)smem;
+  const unsigned char *smem_u = smem;
+  f32x16 acc[2][1] = {{f32x16{}}, {f32x16{}}};
+  const int nk = K / kBK;
+  auto load_tile = [&](unsigned st, int t) {
+#pragma unroll
+    for (int p = 0; p < kLoads; ++p) load_lds(st, q0 + p, A, W, M, K, m0, n0, t * kBK, lane);
+  };
+
+  // the write-back's row record (threads < 64) and this lane's bias, kept in
+  // registers until after the main loop
+  Row rec{};
+  if (tid < kBM) rec = epi.row(min(m0 + tid, M - 1));
+  const f32x4 bias = epi.bias4(n0 + wn * 64 + (lane & 15) * 4);
+
+  // k-tiles 0, 1 and 2 (as far as they exist)
+  unsigned s0 = lds0, s1 = lds0 + kStage, s2 = lds0 + 2 * kStage;
+  load_tile(s0, 0);
+  if (nk > 1) load_tile(s1, 1);
+  if (nk > 2) load_tile(s2, 2);
+  if (nk > 2) barrier_vm<2 * kLoads>();
+  else if (nk > 1) barrier_vm<kLoads>();
+  else barrier_vm<0>();
+  Frag f[2];
+  read_frags(f[0], smem_u + (s0 - lds0), 0, wm, wn, lane);
+
+  for (int t = 0; t < nk; ++t) {
+    // s0: k-tile t (f[0] holds its step-0 fragments); s1, s2: k-tiles t+1, t+2
+    const unsigned char *sc = smem_u + (s0 - lds0);
+#pragma unroll
+    for (int st = 0; st < 7; ++st) {
+      read_frags(f[(st + 1) & 1], sc, st + 1, wm, wn, lane);
+      mfma(acc, f[st & 1]);
+      pin();
+    }
+    if (t + 1 < nk) {
+      // k-tile t+1 complete (k-tile t+2 may still be in flight) and k-tile t
+      // read by every wavefront
+      if (t + 2 < nk) barrier_vm<kLoads>();
+      else barrier_vm<0>();
+      read_frags(f[0], smem_u + (s1 - lds0), 0, wm, wn, lane);
+    }
+    mfma(acc, f[1]);
+    if (t + 3 < nk) load_tile(s0, t + 3);  // into the stage k-tile t left
+    const unsigned s_old = s0;
+    s0 = s1;
+    s1 = s2;
+    s2 = s_old;
+  }
+  if (tid < kBM) rows_lds[tid] = rec;
+  barrier_vm<0>();
+  write_back_staged<2, 1, 8>(acc, epi, m0 + wm * 32, n0 + wn * 64, M, lane,
+                             reinterpret_cast<float *>(smem) + wave * 32 * kStr,
+                             rows_lds + wm * 32, bias);
 }
 
 // Tile choice.  The 256x256 tile (one workgroup per CU) when its tiles fill
@@ -675,18 +824,23 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_pair_kernel(const bf16 *A, c
 // wave, or 80% when K >= 2048 (the longer main loop amortises the tile's
 // fixed start and write-back).  Otherwise the 128x256 tile, two workgroups
 // per CU, whose write-backs overlap the other workgroup's main loop and whose
-// finer steps fill the chip better.  Measured at MAR-L sizes: full-step QKV,
-// fc1 and fc2 and cache-aware QKV take the 256x256 tile, the output
-// projection and the other cache-aware GEMMs the 128x256 one.  Under
-// sustained load the 128x256 tile runs at a lower clock (more operand traffic
-// per flop), which is why it does not replace the large tile outright.
+// finer steps fill the chip better; and when even 128x256 tiles would occupy
+// fewer than half the compute units, the 64x128 tile (K a multiple of 128).  Measured at MAR-L
+// sizes: full-step QKV, fc1 and fc2 and cache-aware QKV take the 256x256
+// tile, the output projection and the other cache-aware GEMMs the 128x256
+// one, the sampler's per-block GEMMs (a few hundred rows) the 64x128 one.
+// Under sustained load the 128x256 tile runs at a lower clock (more operand
+// traffic per flop), which is why it does not replace the large tile
+// outright.
 int gemm_tile_kind(DType dt, int32_t m, int32_t n, int32_t k) {
   if (dt != DType::BF16 || m <= 0) return GEMM_TILE_128x256;
-  const long tiles = (long)((m + 255) / 256) * (n / 256);
   const long cus = device_cu_count();
+  const long tiles = (long)((m + 255) / 256) * (n / 256);
   const long waves = (tiles + cus - 1) / cus;
   const double fill = (double)tiles / (double)(waves * cus);
-  return (fill >= 0.9 || (fill >= 0.8 && k >= 2048)) ? GEMM_TILE_256 : GEMM_TILE_128x256;
+  if (fill >= 0.9 || (fill >= 0.8 && k >= 2048)) return GEMM_TILE_256;
+  if (k % small::kBK == 0 && (long)((m + 127) / 128) * (n / 256) * 2 < cus) return GEMM_TILE_64x128;
+  return GEMM_TILE_128x256;
 }
 
 // N a multiple of 256 and K of 64 (the host limits d_model and d_mlp to
@@ -697,11 +851,18 @@ static hipError_t run_bf16(const void *a, const void *w, int m, int n, int k, co
   if (m == 0) return hipSuccess;
   if (n % 256 != 0 || k % 64 != 0) return hipErrorInvalidValue;
   const bf16 *A = static_cast<const bf16 *>(a), *W = static_cast<const bf16 *>(w);
-  if (gemm_tile_kind(DType::BF16, m, n, k) == GEMM_TILE_256)
-    gemm_bf16_big_kernel<Epi><<<((m + 255) / 256) * (n / 256), 256, 0, s>>>(A, W, m, n, k, epi);
-  else
-    gemm_bf16_pair_kernel<Epi>
-        <<<((m + pair::kBM - 1) / pair::kBM) * (n / pair::kBN), 256, 0, s>>>(A, W, m, n, k, epi);
+  switch (gemm_tile_kind(DType::BF16, m, n, k)) {
+    case GEMM_TILE_256:
+      gemm_bf16_big_kernel<Epi><<<((m + 255) / 256) * (n / 256), 256, 0, s>>>(A, W, m, n, k, epi);
+      break;
+    case GEMM_TILE_64x128:
+      gemm_bf16_small_kernel<Epi>
+          <<<((m + small::kBM - 1) / small::kBM) * (n / small::kBN), 256, 0, s>>>(A, W, m, n, k, epi);
+      break;
+    default:
+      gemm_bf16_pair_kernel<Epi>
+          <<<((m + pair::kBM - 1) / pair::kBM) * (n / pair::kBN), 256, 0, s>>>(A, W, m, n, k, epi);
+  }
   return hipGetLastError();
 }
 

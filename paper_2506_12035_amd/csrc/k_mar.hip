@@ -55,14 +55,14 @@ __device__ __forceinline__ float centre_rstd(float4 (&v)[NV], float eps) {
 // ---- Eq. 1: encoder input rows -------------------------------------------
 // Row i of image b (b = row / n_enc): i < n_buf -> cls[b] + pe[i]; else the
 // known image token p = known[b][i - n_buf]: w_z . tok[b][p] + b_z + pe[n_buf + p].
-template <int NV>
+template <int NV, int CM>
 __global__ __launch_bounds__(256) void encoder_input_kernel(
     float *__restrict__ x, const float *__restrict__ cls, const float *__restrict__ tok,
     const float *__restrict__ w_z, const float *__restrict__ b_z, const float *__restrict__ pe,
     const int32_t *__restrict__ known, int rows, int n_enc, int n_buf, int n_img, int n_known,
     int C) {
   constexpr int D = NV * 256;
-  __shared__ float tv[4][64];
+  __shared__ float tv[4][CM];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int row = blockIdx.x * 4 + w;
   if (row >= rows) return;  // no barrier below
@@ -79,9 +79,10 @@ __global__ __launch_bounds__(256) void encoder_input_kernel(
     return;
   }
   const int p = known[(size_t)b * n_known + (i - n_buf)];
-  if (lane < C) tv[w][lane] = tok[((size_t)b * n_img + p) * C + lane];
-  // the wavefront's own LDS writes are visible to its later reads once they
-  // have completed; no other wavefront touches tv[w]
+  // token value, zero-padded to CM channels
+  if (lane < CM) tv[w][lane] = lane < C ? tok[((size_t)b * n_img + p) * C + lane] : 0.f;
+  // the wavefront's own LDS writes are complete before its reads; no other
+  // wavefront touches tv[w]
   __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
   __builtin_amdgcn_wave_barrier();
   const float4 *p4 = reinterpret_cast<const float4 *>(pe + (size_t)(n_buf + p) * D);
@@ -94,7 +95,8 @@ __global__ __launch_bounds__(256) void encoder_input_kernel(
     for (int e = 0; e < 4; ++e) {
       const float *wr = w_z + (size_t)(d0 + e) * C;
       float s = 0.f;
-      for (int c = 0; c < C; ++c) s = fmaf(wr[c], tv[w][c], s);
+#pragma unroll
+      for (int c = 0; c < CM; ++c) s = fmaf(wr[min(c, C - 1)], tv[w][c], s);
       acc[e] = s;
     }
     const float4 q = p4[lane + 64 * k], bb = bz[lane + 64 * k];
@@ -201,40 +203,53 @@ __global__ __launch_bounds__(256) void silu_cond_kernel(OutT *__restrict__ sc,
              silu(a.w + t.w));
 }
 
+// w_t[c][d] = w[d][c] for a [rows][cols] float32 matrix (the input
+// projection, so that lanes over d read it coalesced).
+__global__ __launch_bounds__(256) void transpose_f32_kernel(float *__restrict__ w_t,
+                                                            const float *__restrict__ w, int rows,
+                                                            int cols) {
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= rows * cols) return;
+  const int d = idx / cols, c = idx - d * cols;
+  w_t[(size_t)c * rows + d] = w[idx];
+}
+
 // Input projection of the noisy token and the first block's modulated norm:
 // h[r] = w_in x[r] + b_in;  a[r] = LN(h[r]) * (1 + scale) + shift with
-// (shift, scale) = mod[r][0 .. 2W) (block 0).
-template <typename T, int NV>
+// (shift, scale) = mod[r][0 .. 2W) (block 0).  The projection is given
+// transposed, w_in_t [C][W].
+template <typename T, int NV, int CM>
 __global__ __launch_bounds__(256) void head_in_mod_kernel(T *__restrict__ a_out,
                                                           float *__restrict__ h,
                                                           const float *__restrict__ x,
-                                                          const float *__restrict__ w_in,
+                                                          const float *__restrict__ w_in_t,
                                                           const float *__restrict__ b_in,
                                                           const T *__restrict__ mod, int mod_ld,
                                                           int rows, int C, float eps) {
   constexpr int W = NV * 256;
-  __shared__ float tv[4][64];
+  __shared__ float tv[4][CM];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int r = blockIdx.x * 4 + w;
   if (r >= rows) return;
-  if (lane < C) tv[w][lane] = x[(size_t)r * C + lane];
+  if (lane < CM) tv[w][lane] = lane < C ? x[(size_t)r * C + lane] : 0.f;
   __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): own LDS writes done
   __builtin_amdgcn_wave_barrier();
   float4 v[NV];
   const float4 *bi = reinterpret_cast<const float4 *>(b_in);
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
-    const int d0 = 4 * (lane + 64 * k);
-    float acc[4];
+    const int c4 = lane + 64 * k;
+    float4 acc = bi[c4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float *wr = w_in + (size_t)(d0 + e) * C;
-      float s = 0.f;
-      for (int c = 0; c < C; ++c) s = fmaf(wr[c], tv[w][c], s);
-      acc[e] = s;
+    for (int c = 0; c < CM; ++c) {  // channels past C have tv = 0 and repeat row C - 1
+      const float4 wv = reinterpret_cast<const float4 *>(w_in_t + (size_t)min(c, C - 1) * W)[c4];
+      const float xc = tv[w][c];
+      acc.x = fmaf(wv.x, xc, acc.x);
+      acc.y = fmaf(wv.y, xc, acc.y);
+      acc.z = fmaf(wv.z, xc, acc.z);
+      acc.w = fmaf(wv.w, xc, acc.w);
     }
-    const float4 bb = bi[lane + 64 * k];
-    v[k] = make_float4(acc[0] + bb.x, acc[1] + bb.y, acc[2] + bb.z, acc[3] + bb.w);
+    v[k] = acc;
     reinterpret_cast<float4 *>(h + (size_t)r * W)[lane + 64 * k] = v[k];
   }
   const float rstd = centre_rstd<NV>(v, eps);
@@ -292,37 +307,34 @@ __global__ __launch_bounds__(256) void head_gate_mod_kernel(T *__restrict__ a_ou
 // (0 at the last step).  x_next may alias x_cur (each lane reads its own
 // element before writing it).  On the last step the result also goes to
 // tok_out[out_rows[r]].
-template <typename T>
+template <typename T, int CM>
 __global__ __launch_bounds__(256) void head_out_step_kernel(
     float *x_next, float *__restrict__ tok_out, const T *__restrict__ a,
     const float *__restrict__ w_out, const float *__restrict__ b_out, const float *x_cur,
     const float *__restrict__ noise, const int32_t *__restrict__ out_rows, int rows, int W, int C,
     float sra, float srm1, float c1, float c2, float sigma) {
-  constexpr int CMAX = 64;
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= rows) return;
-  float acc[CMAX];
+  float acc[CM];
 #pragma unroll
-  for (int c = 0; c < CMAX; ++c) acc[c] = 0.f;
+  for (int c = 0; c < CM; ++c) acc[c] = 0.f;
   const T *ar = a + (size_t)r * W;
   for (int k0 = 4 * lane; k0 < W; k0 += 256) {
     const float4 av = load_row4(ar + k0);
+    float4 wv[CM];  // all loads of this chunk first (rows past C repeat the last one)
 #pragma unroll
-    for (int c = 0; c < CMAX; ++c) {
-      if (c < C) {
-        const float4 wv = *reinterpret_cast<const float4 *>(w_out + (size_t)c * W + k0);
-        acc[c] = fmaf(av.x, wv.x, fmaf(av.y, wv.y, fmaf(av.z, wv.z, fmaf(av.w, wv.w, acc[c]))));
-      }
-    }
+    for (int c = 0; c < CM; ++c)
+      wv[c] = *reinterpret_cast<const float4 *>(w_out + (size_t)min(c, C - 1) * W + k0);
+#pragma unroll
+    for (int c = 0; c < CM; ++c)
+      acc[c] = fmaf(av.x, wv[c].x, fmaf(av.y, wv[c].y, fmaf(av.z, wv[c].z, fmaf(av.w, wv[c].w, acc[c]))));
   }
   float e = 0.f;
 #pragma unroll
-  for (int c = 0; c < CMAX; ++c) {
-    if (c < C) {
-      const float s = wave_sum(acc[c]);
-      if (lane == c) e = s;
-    }
+  for (int c = 0; c < CM; ++c) {
+    const float s = wave_sum(acc[c]);
+    if (lane == c) e = s;
   }
   if (lane < C) {
     const size_t idx = (size_t)r * C + lane;
@@ -359,6 +371,22 @@ __global__ __launch_bounds__(256) void head_out_step_kernel(
     default: return hipErrorInvalidValue; \
   }
 
+// Token channels rounded up to 4, 8, 16, 32 or 64 (compile-time loops).
+template <int NV>
+static void encoder_input_dispatch(int grid, hipStream_t s, float *x, const float *cls,
+                                   const float *tok, const float *w_z, const float *b_z,
+                                   const float *pe, const int32_t *known, int rows, int n_enc,
+                                   int n_buf, int n_img, int n_known, int c) {
+#define E_(CM) encoder_input_kernel<NV, CM><<<grid, 256, 0, s>>>(x, cls, tok, w_z, b_z, pe, known, \
+                                                                rows, n_enc, n_buf, n_img, n_known, c)
+  if (c <= 4) E_(4);
+  else if (c <= 8) E_(8);
+  else if (c <= 16) E_(16);
+  else if (c <= 32) E_(32);
+  else E_(64);
+#undef E_
+}
+
 hipError_t launch_encoder_input(float *x, const float *cls, const float *tok, const float *w_z,
                                 const float *b_z, const float *pe, const int32_t *known,
                                 int32_t batch, int32_t n_buf, int32_t n_img, int32_t n_known,
@@ -367,9 +395,8 @@ hipError_t launch_encoder_input(float *x, const float *cls, const float *tok, co
   if (rows == 0) return hipSuccess;
   if (d_model % 256 != 0 || c_tok < 1 || c_tok > 64) return hipErrorInvalidValue;
   const int grid = (rows + 3) / 4;
-#define L_(NV)                                                                            \
-  encoder_input_kernel<NV><<<grid, 256, 0, s>>>(x, cls, tok, w_z, b_z, pe, known, rows, n_enc, \
-                                                n_buf, n_img, n_known, c_tok)
+#define L_(NV) encoder_input_dispatch<NV>(grid, s, x, cls, tok, w_z, b_z, pe, known, rows, n_enc, \
+                                         n_buf, n_img, n_known, c_tok)
   MARCHE_NV_SWITCH(d_model / 256, L_)
 #undef L_
   return hipGetLastError();
@@ -437,24 +464,44 @@ hipError_t launch_silu_cond(DType dt, void *sc, const float *cond, const float *
   return hipGetLastError();
 }
 
-hipError_t launch_head_in_mod(DType dt, void *a, float *h, const float *x, const float *w_in,
+template <typename T, int NV>
+static void head_in_mod_dispatch(int grid, hipStream_t s, T *a, float *h, const float *x,
+                                 const float *w_in_t, const float *b_in, const T *mod, int mod_ld,
+                                 int rows, int c, float eps) {
+#define E_(CM) head_in_mod_kernel<T, NV, CM><<<grid, 256, 0, s>>>(a, h, x, w_in_t, b_in, mod, mod_ld, \
+                                                                 rows, c, eps)
+  if (c <= 4) E_(4);
+  else if (c <= 8) E_(8);
+  else if (c <= 16) E_(16);
+  else if (c <= 32) E_(32);
+  else E_(64);
+#undef E_
+}
+
+hipError_t launch_transpose_f32(float *w_t, const float *w, int32_t rows, int32_t cols,
+                                hipStream_t s) {
+  const int n = rows * cols;
+  if (n == 0) return hipSuccess;
+  transpose_f32_kernel<<<(n + 255) / 256, 256, 0, s>>>(w_t, w, rows, cols);
+  return hipGetLastError();
+}
+
+hipError_t launch_head_in_mod(DType dt, void *a, float *h, const float *x, const float *w_in_t,
                               const float *b_in, const void *mod, int32_t mod_ld, int32_t rows,
                               int32_t width, int32_t c_tok, float eps, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   if (width % 256 != 0 || c_tok < 1 || c_tok > 64) return hipErrorInvalidValue;
   const int grid = (rows + 3) / 4;
   if (dt == DType::F32) {
-#define L_(NV)                                                                               \
-  head_in_mod_kernel<float, NV><<<grid, 256, 0, s>>>(static_cast<float *>(a), h, x, w_in, b_in, \
-                                                     static_cast<const float *>(mod), mod_ld,   \
-                                                     rows, c_tok, eps)
+#define L_(NV)                                                                                \
+  head_in_mod_dispatch<float, NV>(grid, s, static_cast<float *>(a), h, x, w_in_t, b_in,          \
+                                  static_cast<const float *>(mod), mod_ld, rows, c_tok, eps)
     MARCHE_NV_SWITCH(width / 256, L_)
 #undef L_
   } else {
-#define L_(NV)                                                                             \
-  head_in_mod_kernel<bf16, NV><<<grid, 256, 0, s>>>(static_cast<bf16 *>(a), h, x, w_in, b_in, \
-                                                    static_cast<const bf16 *>(mod), mod_ld,   \
-                                                    rows, c_tok, eps)
+#define L_(NV)                                                                              \
+  head_in_mod_dispatch<bf16, NV>(grid, s, static_cast<bf16 *>(a), h, x, w_in_t, b_in,          \
+                                 static_cast<const bf16 *>(mod), mod_ld, rows, c_tok, eps)
     MARCHE_NV_SWITCH(width / 256, L_)
 #undef L_
   }
@@ -486,6 +533,23 @@ hipError_t launch_head_gate_mod(DType dt, void *a, float *h, const float *t, con
   return hipGetLastError();
 }
 
+template <typename T>
+static void head_out_step_dispatch(int grid, hipStream_t s, float *x_next, float *tok_out,
+                                   const T *a, const float *w_out, const float *b_out,
+                                   const float *x_cur, const float *noise, const int32_t *out_rows,
+                                   int rows, int W, int c, const HeadStep &st) {
+#define E_(CM)                                                                                 \
+  head_out_step_kernel<T, CM><<<grid, 256, 0, s>>>(x_next, tok_out, a, w_out, b_out, x_cur, noise, \
+                                                   out_rows, rows, W, c, st.sra, st.srm1, st.c1,   \
+                                                   st.c2, st.sigma)
+  if (c <= 4) E_(4);
+  else if (c <= 8) E_(8);
+  else if (c <= 16) E_(16);
+  else if (c <= 32) E_(32);
+  else E_(64);
+#undef E_
+}
+
 hipError_t launch_head_out_step(DType dt, float *x_next, float *tok_out, const void *a,
                                 const float *w_out, const float *b_out, const float *x_cur,
                                 const float *noise, const int32_t *out_rows, int32_t rows,
@@ -494,13 +558,11 @@ hipError_t launch_head_out_step(DType dt, float *x_next, float *tok_out, const v
   if (width % 256 != 0 || c_tok < 1 || c_tok > 64) return hipErrorInvalidValue;
   const int grid = (rows + 3) / 4;
   if (dt == DType::F32)
-    head_out_step_kernel<float><<<grid, 256, 0, s>>>(
-        x_next, tok_out, static_cast<const float *>(a), w_out, b_out, x_cur, noise, out_rows, rows,
-        width, c_tok, st.sra, st.srm1, st.c1, st.c2, st.sigma);
+    head_out_step_dispatch(grid, s, x_next, tok_out, static_cast<const float *>(a), w_out, b_out,
+                           x_cur, noise, out_rows, rows, width, c_tok, st);
   else
-    head_out_step_kernel<bf16><<<grid, 256, 0, s>>>(
-        x_next, tok_out, static_cast<const bf16 *>(a), w_out, b_out, x_cur, noise, out_rows, rows,
-        width, c_tok, st.sra, st.srm1, st.c1, st.c2, st.sigma);
+    head_out_step_dispatch(grid, s, x_next, tok_out, static_cast<const bf16 *>(a), w_out, b_out,
+                           x_cur, noise, out_rows, rows, width, c_tok, st);
   return hipGetLastError();
 }
 

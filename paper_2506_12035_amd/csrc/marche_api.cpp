@@ -91,7 +91,8 @@ enum KClass {
   K_SELECT, K_DECODER_INPUT, K_FILL, K_ATTN2_W1, K_ATTN2_W2, K_ATTN2_W4, K_CONCAT, K_ATTN_RES,
   K_ENC_INPUT, K_MASK_FILL, K_LN_ROWS, K_GEMM_EMBED, K_GEMM_EMBED_L, K_TIME_SINUS, K_GEMM_HEAD,
   K_GEMM_HEAD_L, K_GEMM_HEAD_SILU, K_GEMM_HEAD_SILU_L, K_HEAD_SILU_COND, K_HEAD_IN_MOD,
-  K_HEAD_GATE_MOD, K_HEAD_OUT_STEP,
+  K_HEAD_GATE_MOD, K_HEAD_OUT_STEP, K_GEMM_QKV_S, K_GEMM_O_S, K_GEMM_FC1_S, K_GEMM_FC2_S,
+  K_GEMM_EMBED_S, K_GEMM_HEAD_S, K_GEMM_HEAD_SILU_S, K_TRANSPOSE,
   K_NCLASS
 };
 const char *const kClassNames[K_NCLASS] = {
@@ -103,11 +104,25 @@ const char *const kClassNames[K_NCLASS] = {
     "concat_kv",         "attention_res",  "encoder_input",     "mask_fill",
     "ln_rows",           "gemm_embed_t128x256", "gemm_embed_t256", "time_sinus",
     "gemm_head_t128x256", "gemm_head_t256", "gemm_head_silu_t128x256", "gemm_head_silu_t256",
-    "head_silu_cond",    "head_in_mod",    "head_gate_mod",     "head_out_step"};
+    "head_silu_cond",    "head_in_mod",    "head_gate_mod",     "head_out_step",
+    "gemm_qkv_t64x128",  "gemm_o_t64x128", "gemm_fc1_t64x128",  "gemm_fc2_t64x128",
+    "gemm_embed_t64x128", "gemm_head_t64x128", "gemm_head_silu_t64x128", "transpose"};
 
-// Timing class of a GEMM launch: base is the projection's 128x256 class.
+// Timing class of a GEMM launch: base is the projection's 128x256 class, the
+// 256x256 class follows it; the 64x128 classes are listed separately.
 int gemm_class(int base, DType dt, int32_t m, int32_t n, int32_t k) {
-  return base + (gemm_tile_kind(dt, m, n, k) == GEMM_TILE_256 ? 1 : 0);
+  const int kind = gemm_tile_kind(dt, m, n, k);
+  if (kind == GEMM_TILE_256) return base + 1;
+  if (kind != GEMM_TILE_64x128) return base;
+  switch (base) {
+    case K_GEMM_QKV: return K_GEMM_QKV_S;
+    case K_GEMM_O: return K_GEMM_O_S;
+    case K_GEMM_FC1: return K_GEMM_FC1_S;
+    case K_GEMM_FC2: return K_GEMM_FC2_S;
+    case K_GEMM_EMBED: return K_GEMM_EMBED_S;
+    case K_GEMM_HEAD: return K_GEMM_HEAD_S;
+    default: return K_GEMM_HEAD_SILU_S;
+  }
 }
 
 int attn_class(DType dt, int a_max, int n_tokens) {
@@ -601,7 +616,7 @@ marche_status_t check_head(const marche_head_t *h) {
 
 // Workspace of the sampler, in carve order.
 struct HeadWs {
-  size_t z, cond, sinus, h1, temb, sc, mod, h, a, y, t, x, total;
+  size_t z, cond, sinus, h1, temb, sc, mod, h, a, y, t, x, w_in_t, total;
 };
 
 HeadWs head_ws(const marche_head_t *hd, int32_t n_rows, int32_t n_steps) {
@@ -620,7 +635,9 @@ HeadWs head_ws(const marche_head_t *hd, int32_t n_rows, int32_t n_steps) {
   w.y = align256(M * W * es);
   w.t = align256(M * W * 4);
   w.x = align256(M * hd->c_tok * 4);
-  w.total = w.z + w.cond + w.sinus + w.h1 + w.temb + w.sc + w.mod + w.h + w.a + w.y + w.t + w.x;
+  w.w_in_t = align256(W * hd->c_tok * 4);
+  w.total = w.z + w.cond + w.sinus + w.h1 + w.temb + w.sc + w.mod + w.h + w.a + w.y + w.t + w.x +
+            w.w_in_t;
   return w;
 }
 
@@ -688,8 +705,11 @@ marche_status_t marche_diffusion_sample(const marche_head_t *hd, const marche_he
   void *ybuf = take(L.y);
   float *tbuf = reinterpret_cast<float *>(take(L.t));
   float *xs = reinterpret_cast<float *>(take(L.x));
+  float *w_in_t = reinterpret_cast<float *>(take(L.w_in_t));
   auto fp = [](const void *q) { return static_cast<const float *>(q); };
 
+  LAUNCH(K_TRANSPOSE, 0, 8.0 * W * C,
+         launch_transpose_f32(w_in_t, fp(w->w_in), W, C, stream));
   // condition rows and the time-embedding table (all timesteps)
   LAUNCH(K_LN_ROWS, 0, (double)M * D * (4 + es) + 4.0 * M * D,
          launch_ln_rows(dt, z, x_dec, rows, dec_ln_g, dec_ln_b, pe_diff, M, n_tokens, n_buf, D,
@@ -729,7 +749,7 @@ marche_status_t marche_diffusion_sample(const marche_head_t *hd, const marche_he
            launch_gemm_plain(dt, sc, w->w_ada, fp(w->b_ada), M, ML, W, mod, dt, false, stream));
     LAUNCH(K_HEAD_IN_MOD, 2.0 * M * (double)W * C,
            4.0 * M * C + 4.0 * M * W + es * 3.0 * M * W,
-           launch_head_in_mod(dt, abuf, hbuf, xc, fp(w->w_in), fp(w->b_in), mod, ML, M, W, C,
+           launch_head_in_mod(dt, abuf, hbuf, xc, w_in_t, fp(w->b_in), mod, ML, M, W, C,
                               hd->ln_eps, stream));
     for (int k = 0; k < nb; ++k) {
       const char *w1 = static_cast<const char *>(w->w_1) + (size_t)k * W * W * es;

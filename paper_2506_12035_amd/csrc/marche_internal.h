@@ -57,8 +57,12 @@ hipError_t launch_time_sinus(DType dt, void *out, int32_t n_steps, int32_t freq,
 // sc = SiLU(cond + temb_row), [rows][width].
 hipError_t launch_silu_cond(DType dt, void *sc, const float *cond, const float *temb, int32_t rows,
                             int32_t width, hipStream_t s);
-// h = w_in x + b_in; a = LN(h) (1 + scale) + shift with block 0's modulation.
-hipError_t launch_head_in_mod(DType dt, void *a, float *h, const float *x, const float *w_in,
+// w_t = w^T for a [rows][cols] float32 matrix.
+hipError_t launch_transpose_f32(float *w_t, const float *w, int32_t rows, int32_t cols,
+                                hipStream_t s);
+// h = w_in x + b_in (w_in given transposed, [C][W]); a = LN(h) (1 + scale) +
+// shift with block 0's modulation.
+hipError_t launch_head_in_mod(DType dt, void *a, float *h, const float *x, const float *w_in_t,
                               const float *b_in, const void *mod, int32_t mod_ld, int32_t rows,
                               int32_t width, int32_t c_tok, float eps, hipStream_t s);
 // h += gate t; a = LN(h) (1 + scale) + shift (slices of mod at the offsets).
@@ -110,8 +114,8 @@ hipError_t launch_gemm_embed(DType dt, const void *a, const void *w, const float
                              int32_t n_enc, int32_t n_buf, int32_t n_known, int32_t n_tokens,
                              hipStream_t s);
 // bf16 GEMM workgroup tile for an M x N x K product: 128x256 (two workgroups
-// per CU) or 256x256 (one per CU).
-enum GemmTile { GEMM_TILE_128x256 = 0, GEMM_TILE_256 = 1 };
+// per CU), 256x256 (one per CU) or 64x128 (small products).
+enum GemmTile { GEMM_TILE_128x256 = 0, GEMM_TILE_256 = 1, GEMM_TILE_64x128 = 2 };
 int gemm_tile_kind(DType dt, int32_t m, int32_t n, int32_t k);
 // Compute units of the current device (queried once per device, then cached).
 int device_cu_count();

@@ -264,3 +264,149 @@ class Engine:
             return None
         lead = p.a - p.k
         return p.ca_idx.view(self.B, p.a)[:, lead:].cpu().numpy()
+
+
+# ------------------------------------------------------------------ a whole MAR step
+
+HEAD_GEMM_WEIGHTS = ("w_t1", "w_t2", "w_c", "w_ada", "w_1", "w_2")
+
+
+class MarEngine:
+    """A whole generation step of the masked autoregressive model around the
+    cache-aware decoder: the encoder over the known tokens (Eq. 1), the
+    decoder input built from its output (Eq. 2), the decoder step of
+    ``Engine`` and the sampler that draws the generating tokens' values
+    (Eq. 3), which become known tokens of the next step.
+
+    The encoder runs as ``marche_step`` over its own stack with every row
+    active; its row count n_buf + n_known changes with the step, so it has one
+    model description per count and a scratch KV cache sized for all tokens.
+    Every index list, the sampler's draws of every step and all weights are
+    resident on the device before decoding; a step issues only kernel
+    launches on one stream.
+    """
+
+    def __init__(self, mc: workload.MarConfig, device: str = "cuda", batch: Optional[int] = None,
+                 steps: Optional[Sequence[int]] = None, **decoder_kw):
+        self.mc = mc
+        self.dec = Engine(mc.dec, device, batch, **decoder_kw)
+        d = self.dec
+        c = mc.dec
+        self.device, self.B = d.device, d.B
+        B, N, D, H, dh, C = self.B, c.n_tokens, c.d_model, c.n_heads, c.head_dim, mc.c_tok
+        self.dt, self.tdtype = d.dt, d.tdtype
+
+        # encoder stack and its scratch cache / workspace
+        ec = mc.enc
+        self.enc_params = [d._upload_layer(workload.layer_weights(ec, l)) for l in range(ec.n_layers)]
+        self.enc_layers = binding.make_layers(self.enc_params)
+        n_el = ec.n_layers * B * H * N * dh
+        self.enc_k = torch.empty(n_el, dtype=self.tdtype, device=self.device)
+        self.enc_v = torch.empty(n_el, dtype=self.tdtype, device=self.device)
+        self.x_enc = torch.empty(B, N, D, dtype=torch.float32, device=self.device)
+        big = self._enc_model(N)
+        self.enc_ws_bytes = binding.workspace_bytes(big, B, B * N)
+        self.enc_ws = torch.empty(self.enc_ws_bytes, dtype=torch.uint8, device=self.device)
+        self.e2d_ws_bytes = max(256, binding.encoder_to_decoder_workspace_bytes(B, c.n_buf, c.n_img,
+                                                                                D, self.dt))
+        self.e2d_ws = torch.empty(self.e2d_ws_bytes, dtype=torch.uint8, device=self.device)
+
+        emb = workload.mar_embeddings(mc, B)
+        self.emb = {k: torch.from_numpy(np.ascontiguousarray(v, np.float32)).to(
+            self.tdtype if k == "w_de" else torch.float32).to(self.device).contiguous()
+            for k, v in emb.items()}
+
+        # sampler head
+        hw = workload.head_weights(mc)
+        self.head_params = {k: torch.from_numpy(np.ascontiguousarray(v, np.float32)).to(
+            self.tdtype if k in HEAD_GEMM_WEIGHTS else torch.float32).to(self.device).contiguous()
+            for k, v in hw.items()}
+        self.head = binding.make_head(mc.head_width, mc.head_blocks, C, D, mc.t_freq, self.dt,
+                                      mc.head_eps)
+        self.head_weights = binding.make_head_weights(self.head_params)
+        self.tok = torch.zeros(B, c.n_img, C, dtype=torch.float32, device=self.device)
+
+        # per-step resident lists and draws
+        self.steps = list(range(c.n_steps)) if steps is None else list(steps)
+        self.enc_lists: Dict[int, tuple] = {}
+        self.known: Dict[int, Optional[torch.Tensor]] = {}
+        self.gen_rows: Dict[int, tuple] = {}
+        self.noise: Dict[int, torch.Tensor] = {}
+        max_rows = 0
+        for t in self.steps:
+            p = d.plans[t]
+            n_enc = c.n_buf + p.n_known
+            if n_enc not in self.enc_lists:
+                self.enc_lists[n_enc] = (
+                    self._enc_model(n_enc),
+                    _dev_i32(np.tile(np.arange(n_enc), B), self.device),
+                    _dev_i32(np.arange(B + 1) * n_enc, self.device))
+            known = np.sort(d.orders[:, :p.n_known], axis=1)
+            self.known[t] = _dev_i32(known.reshape(-1), self.device) if p.n_known else None
+            gen = np.stack(self._gen_tokens(t))  # [B][g] sequence positions
+            b_idx = np.repeat(np.arange(B), gen.shape[1])
+            pos = gen.reshape(-1) - c.n_buf
+            rows = b_idx * N + c.n_buf + pos
+            out_rows = b_idx * c.n_img + pos
+            self.gen_rows[t] = (_dev_i32(rows, self.device), _dev_i32(out_rows, self.device),
+                                int(rows.size))
+            self.noise[t] = torch.from_numpy(workload.head_noise(mc, t, int(rows.size))).to(self.device)
+            max_rows = max(max_rows, int(rows.size))
+        self.head_ws_bytes = binding.diffusion_workspace_bytes(self.head, max_rows, mc.sample_steps)
+        self.head_ws = torch.empty(self.head_ws_bytes, dtype=torch.uint8, device=self.device)
+
+    def _enc_model(self, n_enc: int) -> binding.Model:
+        c = self.mc.enc
+        return binding.make_model(c.n_layers, c.d_model, c.n_heads, c.head_dim, c.d_mlp, n_enc,
+                                  self.dt, c.ln_eps)
+
+    def _gen_tokens(self, t: int) -> List[np.ndarray]:
+        c = self.mc.dec
+        m = schedule.masked_counts(c.n_img, c.n_steps)
+        lo, hi = c.n_img - m[t], c.n_img - m[t + 1]
+        return [c.n_buf + self.dec.orders[b, lo:hi] for b in range(self.B)]
+
+    @property
+    def stream(self):
+        return self.dec.stream
+
+    def encode(self, t: int) -> None:
+        """Eq. 1 and 2: encoder over the known tokens, then the decoder input."""
+        c, d, e = self.mc.dec, self.dec, self.emb
+        p = d.plans[t]
+        n_known = p.n_known
+        n_enc = c.n_buf + n_known
+        model, idx, off = self.enc_lists[n_enc]
+        binding.encoder_input(self.x_enc, e["cls"], self.tok, e["w_z"], e["b_z"], e["pe_enc"],
+                              self.known[t], self.B, c.n_buf, c.n_img, n_known, c.d_model,
+                              self.mc.c_tok, stream=self.stream)
+        ec = self.mc.enc
+        cache = binding.KVCache(self.enc_k.data_ptr(), self.enc_v.data_ptr(), ec.n_layers, self.B,
+                                ec.n_heads, n_enc, ec.head_dim, self.dt)
+        binding.marche_step(model, self.enc_layers, cache, 0, ec.n_layers, self.B, self.x_enc, idx,
+                            off, None, self.B * n_enc, n_enc, 0, None, -1, self.enc_ws,
+                            self.enc_ws_bytes, stream=self.stream)
+        binding.encoder_to_decoder(d.x, self.x_enc, e["enc_ln_g"], e["enc_ln_b"], c.ln_eps,
+                                   e["w_de"], e["b_de"], e["mask"], e["pe_dec"], self.known[t],
+                                   d.rank, self.B, c.n_buf, c.n_img, n_known, c.d_model, self.dt,
+                                   self.e2d_ws, self.e2d_ws_bytes, stream=self.stream)
+
+    def sample(self, t: int) -> None:
+        """Eq. 3: draw the generating tokens' values from the decoder output."""
+        c, e = self.mc.dec, self.emb
+        rows, out_rows, n_rows = self.gen_rows[t]
+        binding.diffusion_sample(self.head, self.head_weights, self.dec.x, c.n_tokens, c.n_buf,
+                                 e["dec_ln_g"], e["dec_ln_b"], c.ln_eps, e["pe_diff"], rows,
+                                 out_rows, n_rows, self.noise[t], self.mc.sample_steps,
+                                 self.mc.temperature, self.tok, self.head_ws, self.head_ws_bytes,
+                                 stream=self.stream)
+
+    def step(self, t: int) -> None:
+        self.encode(t)
+        self.dec.step(t, build_input=False)
+        self.sample(t)
+
+    def generate(self) -> None:
+        self.tok.zero_()
+        for t in self.steps:
+            self.step(t)

@@ -250,7 +250,7 @@ def test_diffusion_sample_validation_and_workspace():
     W, M, T = 256, 10, 8
     assert need == (a(M * 256 * 2) + a(M * W * 4) + a(T * 256 * 2) + a(T * W * 2) + a(T * W * 4) +
                     a(M * W * 2) + a(M * 8 * W * 2) + a(M * W * 4) + 2 * a(M * W * 2) + a(M * W * 4) +
-                    a(M * 16 * 4))
+                    a(M * 16 * 4) + a(W * 16 * 4))
     assert call(ws=None) == binding.MARCHE_ERR_WORKSPACE
     assert call(ws_bytes=need - 1) == binding.MARCHE_ERR_WORKSPACE
     assert call(ws=FAKE + 64) == binding.MARCHE_ERR_INVALID_ARG

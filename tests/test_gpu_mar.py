@@ -179,3 +179,86 @@ def test_diffusion_sample_temperature_zero_ignores_step_noise():
     other[:mc.sample_steps] = np.random.default_rng(9).standard_normal(other[:mc.sample_steps].shape)
     b = _run_head(mc, head, emb, x_dec, rows, out_rows, other.astype(np.float32), 0.0)[out_rows]
     np.testing.assert_array_equal(a, b)
+
+
+def _oracle_whole_step(eng, t, tok_before, noise):
+    """One whole step of every image by the oracle, from the GPU's token values
+    before the step: encoder input, encoder, decoder input, the decoder (all
+    layers full), condition and sampler.  Returns (x_out [B][N][D], new token
+    values [B][g][C])."""
+    from oracle import block
+
+    mc = eng.mc
+    c, ec = mc.dec, mc.enc
+    emb = workload.mar_embeddings(mc, eng.B)
+    enc_p = [workload.layer_weights(ec, l) for l in range(ec.n_layers)]
+    dec_p = [workload.layer_weights(c, l) for l in range(c.n_layers)]
+    head = {k: np.asarray(v, np.float64) for k, v in workload.head_weights(mc).items()}
+    hs = mar.HeadShape(mc.head_width, mc.head_blocks, mc.c_tok, c.d_model, mc.t_freq, mc.head_eps)
+    n_known = eng.dec.plans[t].n_known
+    gens = eng._gen_tokens(t)
+    g = len(gens[0])
+    xs, toks = [], []
+    for b in range(eng.B):
+        known = [c.n_buf + int(p) for p in np.sort(eng.dec.orders[b, :n_known])]
+        e = mar.encoder_input(emb["cls"][b], tok_before[b], emb["w_z"], emb["b_z"], emb["pe_enc"],
+                              known, c.n_buf)
+        h = mar.encoder(e, enc_p, ec.n_heads, ec.ln_eps)
+        x = mar.encoder_to_decoder(h, emb["enc_ln_g"], emb["enc_ln_b"], c.ln_eps, emb["w_de"],
+                                   emb["b_de"], emb["mask"], emb["pe_dec"], known, c.n_buf)
+        kc = np.zeros((c.n_heads, c.n_tokens, c.head_dim))
+        for p in dec_p:
+            x = block.full_layer(p, x, kc, kc.copy(), n_heads=c.n_heads, eps=c.ln_eps).x_out
+        gen = [int(j) for j in gens[b]]
+        z = mar.decoder_cond(x, emb["dec_ln_g"], emb["dec_ln_b"], c.ln_eps, emb["pe_diff"], gen, c.n_buf)
+        toks.append(mar.sample(z, noise[:, b * g:(b + 1) * g], mc.sample_steps, mc.temperature, head, hs))
+        xs.append(x)
+    return np.stack(xs), np.stack(toks)
+
+
+def test_whole_mar_steps_against_oracle():
+    """Four whole steps (every decoder step full) of the tiny model: the decoder
+    output and the sampled token values of each step against the oracle given
+    the same token values before the step."""
+    import torch
+    from paper_2506_12035_amd import driver
+
+    mc = workload.MAR_CONFIGS["tiny"]
+    eng = driver.MarEngine(mc, steps=[0, 1, 2, 3], full_every=1)
+    eng.tok.zero_()
+    c = mc.dec
+    for t in eng.steps:
+        say(f"whole MAR step {t}")
+        tok_before = eng.tok.cpu().numpy().copy()
+        eng.step(t)
+        torch.cuda.synchronize()
+        x_gpu = eng.dec.x.cpu().numpy()
+        tok_gpu = eng.tok.cpu().numpy()
+        x_ref, tok_ref = _oracle_whole_step(eng, t, tok_before, eng.noise[t].cpu().numpy())
+        ex = rel_err(x_gpu, x_ref)
+        gens = eng._gen_tokens(t)
+        got = np.stack([tok_gpu[b, gens[b] - c.n_buf] for b in range(eng.B)])
+        et = rel_err(got, tok_ref)
+        say(f"  decoder output {ex:.2e}, sampled tokens {et:.2e}")
+        assert ex <= TOL["bf16"] and et <= TOL["bf16"]
+        # tokens not generated at this step keep their values
+        keep = np.ones(tok_gpu.shape[:2], bool)
+        for b in range(eng.B):
+            keep[b, gens[b] - c.n_buf] = False
+        np.testing.assert_array_equal(tok_gpu[keep], tok_before[keep])
+
+
+def test_whole_generation_default_schedule():
+    """Every step of the tiny model under the paper's schedule (periodic full
+    refresh, 10% refresh tokens): every image token is sampled exactly once and
+    all values are finite."""
+    import torch
+    from paper_2506_12035_amd import driver
+
+    mc = workload.MAR_CONFIGS["tiny"]
+    eng = driver.MarEngine(mc)
+    eng.generate()
+    torch.cuda.synchronize()
+    tok = eng.tok.cpu().numpy()
+    assert np.isfinite(tok).all()
+    assert (np.abs(tok).sum(axis=2) > 0).all()
