@@ -16,7 +16,10 @@ against the paper:
 * ``schedule`` -- the mask schedule and the generating / caching token sets
                   (Section 3, Eq. 1-4) and the full-refresh rules (Section 4.3).
 * ``step``     -- one MARche decoding step over a stack of blocks.
+* ``mar``      -- the rest of a MAR step around the decoder: encoder input and
+                  encoder (Eq. 1), decoder input (Eq. 2), the condition and
+                  the DDPM sampler of Eq. 3.
 
 Parity status per function is listed in each module's header.
 """
-from . import block, schedule, select, step  # noqa: F401
+from . import block, mar, schedule, select, step  # noqa: F401
