@@ -262,3 +262,66 @@ def test_whole_generation_default_schedule():
     tok = eng.tok.cpu().numpy()
     assert np.isfinite(tok).all()
     assert (np.abs(tok).sum(axis=2) > 0).all()
+
+
+def test_sampler_full_size_sampled_rows():
+    """The sampler at the MAR-L head (width 1280, 8 blocks, 100 DDPM steps) on
+    512 rows (batch 128 x 4 generating tokens), as the whole-generation bench
+    runs it; rows are independent, so the oracle recomputes sampled rows."""
+    mc = workload.MAR_CONFIGS["mar-l-e2e"]
+    cfg = mc.dec
+    hs = mar.HeadShape(mc.head_width, mc.head_blocks, mc.c_tok, cfg.d_model, mc.t_freq, mc.head_eps)
+    head = workload.head_weights(mc)
+    emb = workload.mar_embeddings(mc)
+    rng = np.random.default_rng(77)
+    B, N, n_rows = cfg.batch, cfg.n_tokens, 512
+    say(f"sampler full size: {n_rows} rows, {mc.sample_steps} steps")
+    x_dec = rng.standard_normal((B, N, cfg.d_model)).astype(np.float32)
+    cells = rng.choice(B * cfg.n_img, size=n_rows, replace=False)
+    b_of, p_of = cells // cfg.n_img, cells % cfg.n_img
+    rows = (b_of * N + cfg.n_buf + p_of).astype(np.int32)
+    out_rows = (b_of * cfg.n_img + p_of).astype(np.int32)
+    noise = workload.head_noise(mc, 5, n_rows)
+    got = _run_head(mc, head, emb, x_dec, rows, out_rows, noise, mc.temperature)[out_rows]
+    assert np.isfinite(got).all()
+    pick = [0, 211, 511]
+    ref = _oracle_head(mc, hs, head, emb, x_dec, b_of[pick], p_of[pick], noise[:, pick], mc.temperature)
+    e = rel_err(got[pick], ref)
+    say(f"  sampled rows max rel err {e:.2e}")
+    assert e <= TOL["bf16"]
+
+
+def test_encoder_to_decoder_full_size_sampled_images():
+    """The decoder input at MAR-L size (batch 128, 64 buffer + 256 image tokens,
+    half of them known), every row written, two sampled images against the
+    oracle."""
+    import torch
+    from paper_2506_12035_amd import binding
+
+    B, n_buf, n_img, n_known, D = 128, 64, 256, 128, 1024
+    say("decoder input full size")
+    rng = np.random.default_rng(314)
+    N = n_buf + n_img
+    x_enc = rng.standard_normal((B, n_buf + n_known, D)).astype(np.float32)
+    g = (1 + 0.02 * rng.standard_normal(D)).astype(np.float32)
+    bb = (0.02 * rng.standard_normal(D)).astype(np.float32)
+    w_de = workload.round_to((0.02 * rng.standard_normal((D, D))).astype(np.float32), "bf16")
+    b_de = (0.02 * rng.standard_normal(D)).astype(np.float32)
+    mask = rng.standard_normal(D).astype(np.float32)
+    pe = rng.standard_normal((N, D)).astype(np.float32)
+    known, rank = _known_and_rank(rng, B, n_img, n_known)
+    x_dec = torch.full((B, N, D), float("nan"), device="cuda")
+    wsb = binding.encoder_to_decoder_workspace_bytes(B, n_buf, n_known, D, binding.MARCHE_BF16)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    binding.encoder_to_decoder(x_dec, _dev(x_enc), _dev(g), _dev(bb), 1e-6, _dev(w_de, torch.bfloat16),
+                               _dev(b_de), _dev(mask), _dev(pe), _dev(known), _dev(rank), B, n_buf,
+                               n_img, n_known, D, binding.MARCHE_BF16, ws, wsb)
+    torch.cuda.synchronize()
+    assert torch.isfinite(x_dec).all().item()
+    got = x_dec[[5, 127]].cpu().numpy()
+    for i, b in enumerate((5, 127)):
+        ref = mar.encoder_to_decoder(x_enc[b], g, bb, 1e-6, w_de, b_de, mask, pe,
+                                     [n_buf + int(p) for p in known[b]], n_buf)
+        e = rel_err(got[i], ref)
+        say(f"  image {b}: max rel err {e:.2e}")
+        assert e <= TOL["bf16"]
