@@ -188,6 +188,21 @@ def test_bf16_layer_ragged(shape):
         _check_refresh(sel[b], ref[b].scores, excl[b], k, TOL["bf16"])
 
 
+@pytest.mark.parametrize("n_tokens", [320, 300])
+def test_bf16_layer_short_active_sets(n_tokens):
+    """Cache-aware layers where every image has at most 64 active rows (the
+    short-query resident attention at head width 64): a single token, a
+    typical set, exactly 64 and a ragged one; full and ragged key counts."""
+    cfg = workload.CONFIGS[3].with_(n_tokens=n_tokens)
+    sizes, gens = [1, 39, 64, 23], [1, 5, 9, 3]
+    x, kc, vc, active, gens = _ragged_case(cfg, len(sizes), sizes, gens, seed=23 + n_tokens)
+    p = workload.layer_weights(cfg, 2)
+    say(f"bf16 layer short active sets N={n_tokens}")
+    ref = _oracle_layer(cfg, f64(p), x, kc, vc, active, gens)
+    gpu = SingleLayer(cfg, p, x, kc, vc).run(active, gens)
+    _check_layer(cfg, x, kc, vc, active, gens, gpu, ref, TOL["bf16"])
+
+
 def test_bf16_layer_deterministic():
     cfg = workload.CONFIGS[3]
     sizes, gens = [44, 320, 7], [6, 6, 1]
