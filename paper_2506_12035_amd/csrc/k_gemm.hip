@@ -403,25 +403,24 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
     for (int i = 0; i < 4; ++i) acc[j][i] = f32x16{};
   const int nk = K / 64;
 
-  // k-tile 0 into stage 0; the first quarter of k-tile 1 into stage 1
+  // The write-back's bias (threads < 64, four columns each) and row record
+  // (one row per thread), loaded first and kept in registers: they reach LDS
+  // only after the main loop, so no wait on them holds up the pipeline.
+  const typename Epi::Row rec = epi.row(min(m0 + tid, M - 1));
+  const f32x4 bias = tid < 64 ? epi.bias4(n0 + tid * 4) : f32x4{};
+  // k-tiles 0 and 1 into both stages, then wait for k-tile 0 only
 #pragma unroll
   for (int p = 0; p < 16; ++p) load_lds(lds_stage[0], q0 + p, A, W, M, K, m0, n0, 0, lane);
-  // the write-back's biases and row records, loaded while the tile computes
-  if (tid < 64)
-    *reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(side) + tid * 4) = epi.bias4(n0 + tid * 4);
-  reinterpret_cast<typename Epi::Row *>(side + 1024)[tid] = epi.row(min(m0 + tid, M - 1));
-  barrier();
+  if (nk > 1) {
+#pragma unroll
+    for (int p = 0; p < 16; ++p) load_lds(lds_stage[1], q0 + p, A, W, M, K, m0, n0, 64, lane);
+    asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  } else {
+    barrier();
+  }
   Frag fa, fb;
 #pragma unroll
   for (int r = 0; r < 8; ++r) read_frag(fa, r, smem, 0, wm, wn, lane);
-  {
-    const int k1 = min(1, nk - 1) * 64;
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      load_lds(lds_stage[1], q0 + p, A, W, M, K, m0, n0, k1, lane);
-      pin();
-    }
-  }
 
   for (int kt = 0; kt + 1 < nk; ++kt) {
     const int cur = kt & 1;
@@ -438,8 +437,10 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
       for (int q = 0; q < 16; ++q) {
         mfma(acc, fc, q);
         if (q < 8) read_frag(fn, q, sc, st + 1, wm, wn, lane);
-        else if (st == 0) load_lds(ln, q0 + 4 + (q - 8), A, W, M, K, m0, n0, k1, lane);
-        else if (st == 1 && q < 12) load_lds(ln, q0 + 12 + (q - 8), A, W, M, K, m0, n0, k1, lane);
+        // (k-tile 1 was loaded whole in the prologue)
+        else if (st == 0 && kt > 0) load_lds(ln, q0 + 4 + (q - 8), A, W, M, K, m0, n0, k1, lane);
+        else if (st == 1 && q < 12 && kt > 0)
+          load_lds(ln, q0 + 12 + (q - 8), A, W, M, K, m0, n0, k1, lane);
         pin();
       }
     }
@@ -479,9 +480,11 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
       }
     }
   }
-  // the last quarter-tile loads (a clamped repeat of the final k-tile) land
-  // and every wavefront is done with the stages before they hold the
-  // write-back's staging rows
+  // the write-back's biases and row records into LDS; the last quarter-tile
+  // loads (a clamped repeat of the final k-tile) land and every wavefront is
+  // done with the stages before they hold the write-back's staging rows
+  if (tid < 64) *reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(side) + tid * 4) = bias;
+  reinterpret_cast<typename Epi::Row *>(side + 1024)[tid] = rec;
   barrier();
   const f32x4 b = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(side) +
                                                     wn * 128 + (lane & 31) * 4);
