@@ -95,7 +95,7 @@ __global__ __launch_bounds__(256) void encoder_input_kernel(
     for (int e = 0; e < 4; ++e) {
       const float *wr = w_z + (size_t)(d0 + e) * C;
       float s = 0.f;
-#pragma unroll
+#pragma unroll 16
       for (int c = 0; c < CM; ++c) s = fmaf(wr[min(c, C - 1)], tv[w][c], s);
       acc[e] = s;
     }
@@ -240,7 +240,7 @@ __global__ __launch_bounds__(256) void head_in_mod_kernel(T *__restrict__ a_out,
   for (int k = 0; k < NV; ++k) {
     const int c4 = lane + 64 * k;
     float4 acc = bi[c4];
-#pragma unroll
+#pragma unroll 16
     for (int c = 0; c < CM; ++c) {  // channels past C have tv = 0 and repeat row C - 1
       const float4 wv = reinterpret_cast<const float4 *>(w_in_t + (size_t)min(c, C - 1) * W)[c4];
       const float xc = tv[w][c];
