@@ -217,16 +217,22 @@ __device__ __forceinline__ void tile_coords(int id, int tiles_m, int tiles_n, in
 // on four wavefronts of 128x128 (16 accumulators each, which live in the
 // accumulation registers).  Operands go from global memory straight into LDS
 // (global_load_lds_dwordx4: no staging registers, no LDS write instructions)
-// through two 64 KB stages of 128-byte rows whose 16-byte chunks are permuted
-// by an XOR with the row pair index, so the 16 rows one fragment read touches
-// per chunk hit 16 distinct bank groups.  Every MFMA is issued in a fixed
-// slot with at most one memory operation beside it (sched_barrier): the eight
-// fragment reads of the next k16 step, the sixteen loads of the next k-tile
-// and the barrier are spread over the 64 MFMAs of a k-tile, and the loads of
-// k-tile t+1 have the whole of k-tile t to land.
+// as 32 KB stages of 256 rows x 64 k, 128-byte rows whose 16-byte chunks are
+// permuted by an XOR with the row pair index, so the 16 rows one fragment
+// read touches per chunk hit 16 distinct bank groups.  The activation rows,
+// streamed from memory once per column tile, get three stages and are loaded
+// two k-tiles ahead of use; the weight rows, shared by every tile and served
+// from L2, get two and are loaded one k-tile ahead: all of the CU's 160 KB.
+// Every MFMA is issued in a fixed slot with at most one memory operation
+// beside it (sched_barrier): the eight fragment reads of the next k16 step,
+// the sixteen loads of a k-tile and the barrier are spread over the 64 MFMAs
+// of a k-tile.
 namespace big {
 
-constexpr int kStage = 65536;  // bytes per stage: activation rows [0, 32K), weight rows [32K, 64K)
+constexpr int kStage = 32768;  // bytes per operand stage: 256 rows x 64 k
+constexpr int kAStages = 3, kWStages = 2;
+constexpr int kWBase = kAStages * kStage;               // weight stages start at 96 KB
+constexpr int kSmem = (kAStages + kWStages) * kStage;   // 160 KB
 
 struct Frag {
   bf16x8 x[4];  // activation rows (MFMA B operand)
@@ -237,23 +243,16 @@ __device__ __forceinline__ void pin() { __builtin_amdgcn_sched_barrier(0); }
 
 __device__ __forceinline__ int swz(int r, int kc) { return kc ^ ((r >> 1) & 7); }
 
-// Load instruction q (0..63 per k-tile, 16 per wavefront) moves 1 KB: q < 32
-// carries activation rows 8q..8q+7, q >= 32 weight rows 8(q-32)..; lane l
-// writes LDS bytes [16 l, 16 l + 16) of the block, i.e. row 8q + l / 8 at
-// physical chunk l % 8, which holds logical chunk swz(row, l % 8).
-// `stage` is the LDS byte address of the stage (wave-uniform, so M0 is set
-// from a scalar register).
-__device__ __forceinline__ void load_lds(unsigned stage, int q, const bf16 *A, const bf16 *W,
-                                         int M, int K, int m0, int n0, int k0, int lane) {
-  const int rr = lane >> 3, pc = lane & 7;
-  const bf16 *g;
-  if (q < 32) {
-    const int r = q * 8 + rr;
-    g = A + (size_t)min(m0 + r, M - 1) * K + k0 + swz(r, pc) * 8;
-  } else {
-    const int r = (q - 32) * 8 + rr;
-    g = W + (size_t)(n0 + r) * K + k0 + swz(r, pc) * 8;
-  }
+// Load instruction q (0..31 per operand and k-tile, 8 per wavefront) moves
+// 1 KB: rows 8q..8q+7 of the operand's 256-row block; lane l writes LDS bytes
+// [16 l, 16 l + 16) of it, i.e. row 8q + l / 8 at physical chunk l % 8, which
+// holds logical chunk swz(row, l % 8).  `stage` is the LDS byte address of the
+// stage (wave-uniform, so M0 is set from a scalar register).  Activation rows
+// past M repeat row M - 1 (their results are never stored).
+__device__ __forceinline__ void load_lds(unsigned stage, int q, const bf16 *src, int rows, int K,
+                                         int r0, int k0, int lane) {
+  const int r = q * 8 + (lane >> 3), pc = lane & 7;
+  const bf16 *g = src + (size_t)min(r0 + r, rows - 1) * K + k0 + swz(r, pc) * 8;
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
                :
                : "v"(g), "s"(__builtin_amdgcn_readfirstlane(stage + q * 1024))
@@ -261,17 +260,18 @@ __device__ __forceinline__ void load_lds(unsigned stage, int q, const bf16 *A, c
 }
 
 // Fragment r of k16 step s, in the order the MFMAs need them: x0 w0 x1 x2 x3 w1 w2 w3.
-__device__ __forceinline__ void read_frag(Frag &f, int r, const unsigned char *stage, int s, int wm,
-                                          int wn, int lane) {
+__device__ __forceinline__ void read_frag(Frag &f, int r, const unsigned char *sa,
+                                          const unsigned char *sw, int s, int wm, int wn,
+                                          int lane) {
   const bool is_x = (r == 0 || r == 2 || r == 3 || r == 4);
   const int idx = r <= 1 ? 0 : (r <= 4 ? r - 1 : r - 4);
   const int kc = s * 2 + (lane >> 5);
   if (is_x) {
     const int row = wm * 128 + idx * 32 + (lane & 31);
-    f.x[idx] = *reinterpret_cast<const bf16x8 *>(stage + row * 128 + swz(row, kc) * 16);
+    f.x[idx] = *reinterpret_cast<const bf16x8 *>(sa + row * 128 + swz(row, kc) * 16);
   } else {
     const int row = wn * 128 + idx * 32 + (lane & 31);
-    f.w[idx] = *reinterpret_cast<const bf16x8 *>(stage + 32768 + row * 128 + swz(row, kc) * 16);
+    f.w[idx] = *reinterpret_cast<const bf16x8 *>(sw + row * 128 + swz(row, kc) * 16);
   }
 }
 
@@ -280,10 +280,13 @@ __device__ __forceinline__ void mfma(f32x16 (&acc)[4][4], const Frag &f, int q) 
   acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.w[j], f.x[i], acc[j][i], 0, 0, 0);
 }
 
-// Own loads landed in LDS, own LDS reads done, then the workgroup barrier.
-__device__ __forceinline__ void barrier() {
-  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+// Own loads landed in LDS (all, or all but the last VM issued), own LDS reads
+// done, then the workgroup barrier.
+template <int VM>
+__device__ __forceinline__ void barrier_vm() {
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(VM) : "memory");
 }
+__device__ __forceinline__ void barrier() { barrier_vm<0>(); }
 
 }  // namespace big
 
@@ -296,7 +299,7 @@ __device__ __forceinline__ void barrier() {
 // priors of the next batch of rows are loaded before this batch's stores.
 namespace big {
 constexpr int kWbStride = 132;  // floats per staged row (128 + 4: no bank conflicts)
-static_assert(4 * 32 * kWbStride * 4 <= 2 * kStage, "staged write-back fits the stages");
+static_assert(4 * 32 * kWbStride * 4 <= kWBase, "staged write-back fits the activation stages");
 }  // namespace big
 
 // One wavefront's TM 32-row blocks of TN * 32 columns (accumulators acc[j][i]:
@@ -383,9 +386,11 @@ template <class Epi>
 __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, const bf16 *W, int M,
                                                                int N, int K, Epi epi) {
   using namespace big;
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * kStage];
-  // biases and row records of the tile for the write-back (5 KB)
-  __shared__ __attribute__((aligned(16))) unsigned char side[1024 + 256 * sizeof(typename Epi::Row)];
+  // activation stages at [0, 96K), weight stages at [96K, 160K); after the
+  // main loop the write-back stages rows in [0, 66K) and keeps the tile's
+  // biases and row records in the weight stage the last k-tile left free
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[kSmem];
+  static_assert(1024 + 256 * sizeof(typename Epi::Row) <= kStage, "row records fit one stage");
   const int tiles_m = (M + 255) / 256, tiles_n = N / 256;
   int tm, tn;
   tile_coords(xcd_remap(blockIdx.x, gridDim.x), tiles_m, tiles_n, tm, tn);
@@ -393,42 +398,54 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar address math
   const int wm = wave >> 1, wn = wave & 1;
-  const int q0 = wave * 16;  // this wavefront's load instructions q0 .. q0 + 15
+  const int q0 = wave * 8;  // this wavefront's load instructions q0 .. q0 + 7 of each operand
   const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void *)smem;
-  const unsigned lds_stage[2] = {lds0, lds0 + kStage};
   f32x16 acc[4][4];
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[j][i] = f32x16{};
   const int nk = K / 64;
+  auto load_a = [&](int sa, int kt, int p) {
+    load_lds(lds0 + sa * kStage, q0 + p, A, M, K, m0, kt * 64, lane);
+  };
+  auto load_w = [&](int kt, int p) {
+    load_lds(lds0 + kWBase + (kt & 1) * kStage, q0 + p, W, N, K, n0, kt * 64, lane);
+  };
 
   // The write-back's bias (threads < 64, four columns each) and row record
   // (one row per thread), loaded first and kept in registers: they reach LDS
   // only after the main loop, so no wait on them holds up the pipeline.
   const typename Epi::Row rec = epi.row(min(m0 + tid, M - 1));
   const f32x4 bias = tid < 64 ? epi.bias4(n0 + tid * 4) : f32x4{};
-  // k-tiles 0 and 1 into both stages, then wait for k-tile 0 only
+  // k-tiles 0 and 1 of both operands, then wait for k-tile 0 only
 #pragma unroll
-  for (int p = 0; p < 16; ++p) load_lds(lds_stage[0], q0 + p, A, W, M, K, m0, n0, 0, lane);
+  for (int p = 0; p < 8; ++p) load_a(0, 0, p);
+#pragma unroll
+  for (int p = 0; p < 8; ++p) load_w(0, p);
   if (nk > 1) {
 #pragma unroll
-    for (int p = 0; p < 16; ++p) load_lds(lds_stage[1], q0 + p, A, W, M, K, m0, n0, 64, lane);
-    asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    for (int p = 0; p < 8; ++p) load_a(1, 1, p);
+#pragma unroll
+    for (int p = 0; p < 8; ++p) load_w(1, p);
+    barrier_vm<16>();
   } else {
     barrier();
   }
   Frag fa, fb;
 #pragma unroll
-  for (int r = 0; r < 8; ++r) read_frag(fa, r, smem, 0, wm, wn, lane);
+  for (int r = 0; r < 8; ++r) read_frag(fa, r, smem, smem + kWBase, 0, wm, wn, lane);
 
+  // activation stage of k-tiles kt, kt + 1, kt + 2 (kt mod 3, ...)
+  int sa0 = 0, sa1 = 1, sa2 = 2;
   for (int kt = 0; kt + 1 < nk; ++kt) {
-    const int cur = kt & 1;
-    const unsigned char *sc = smem + cur * kStage;
-    const unsigned char *sn = smem + (cur ^ 1) * kStage;
-    const unsigned ln = lds_stage[cur ^ 1], lc = lds_stage[cur];
-    const int k1 = (kt + 1) * 64, k2 = min(kt + 2, nk - 1) * 64;
-    // k16 steps 0..2: fragments of the next step; the rest of k-tile kt+1
+    const unsigned char *ac = smem + sa0 * kStage, *wc = smem + kWBase + (kt & 1) * kStage;
+    const unsigned char *an = smem + sa1 * kStage, *wnx = smem + kWBase + ((kt + 1) & 1) * kStage;
+    const bool a2 = kt + 2 < nk;  // k-tile kt+2 exists: its activation rows go out now
+    // k16 steps 0..2: fragments of the next step; the second half of the
+    // weight rows of k-tile kt+1 (the first went out at the end of k-tile
+    // kt-1; k-tile 1 was loaded whole in the prologue), then the activation
+    // rows of k-tile kt+2 into the stage k-tile kt-1 left
 #pragma unroll
     for (int st = 0; st < 3; ++st) {
       Frag &fc = (st & 1) ? fb : fa;
@@ -436,38 +453,44 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         mfma(acc, fc, q);
-        if (q < 8) read_frag(fn, q, sc, st + 1, wm, wn, lane);
-        // (k-tile 1 was loaded whole in the prologue)
-        else if (st == 0 && kt > 0) load_lds(ln, q0 + 4 + (q - 8), A, W, M, K, m0, n0, k1, lane);
-        else if (st == 1 && q < 12 && kt > 0)
-          load_lds(ln, q0 + 12 + (q - 8), A, W, M, K, m0, n0, k1, lane);
+        if (q < 8) read_frag(fn, q, ac, wc, st + 1, wm, wn, lane);
+        else if (st == 0 && q < 12 && kt > 0) load_w(kt + 1, 4 + (q - 8));
+        else if (st == 0 && q >= 12 && a2) load_a(sa2, kt + 2, q - 12);
+        else if (st == 1 && q < 12 && a2) load_a(sa2, kt + 2, 4 + (q - 8));
         pin();
       }
     }
-    // k16 step 3: barrier (k-tile kt+1 complete, stage cur free), first
-    // fragments of k-tile kt+1, first quarter of k-tile kt+2 into stage cur
+    // k16 step 3: barrier (k-tile kt+1 complete -- only the activation loads
+    // of k-tile kt+2 may still be in flight -- and every wavefront done with
+    // k-tile kt), first fragments of k-tile kt+1, first half of the weight
+    // rows of k-tile kt+2 into the weight stage of k-tile kt
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       mfma(acc, fb, q);
       pin();
     }
-    barrier();
+    if (a2) barrier_vm<8>();
+    else barrier();
     pin();
 #pragma unroll
     for (int q = 4; q < 12; ++q) {
       mfma(acc, fb, q);
-      read_frag(fa, q - 4, sn, 0, wm, wn, lane);
+      read_frag(fa, q - 4, an, wnx, 0, wm, wn, lane);
       pin();
     }
 #pragma unroll
     for (int q = 12; q < 16; ++q) {
       mfma(acc, fb, q);
-      load_lds(lc, q0 + (q - 12), A, W, M, K, m0, n0, k2, lane);
+      if (a2) load_w(kt + 2, q - 12);
       pin();
     }
+    const int t = sa0;
+    sa0 = sa1;
+    sa1 = sa2;
+    sa2 = t;
   }
-  {  // last k-tile
-    const unsigned char *sc = smem + ((nk - 1) & 1) * kStage;
+  {  // last k-tile: no loads in flight
+    const unsigned char *ac = smem + sa0 * kStage, *wc = smem + kWBase + ((nk - 1) & 1) * kStage;
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
       Frag &fc = (st & 1) ? fb : fa;
@@ -475,14 +498,16 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         mfma(acc, fc, q);
-        if (st < 3 && q < 8) read_frag(fn, q, sc, st + 1, wm, wn, lane);
+        if (st < 3 && q < 8) read_frag(fn, q, ac, wc, st + 1, wm, wn, lane);
         pin();
       }
     }
   }
-  // the write-back's biases and row records into LDS; the last quarter-tile
-  // loads (a clamped repeat of the final k-tile) land and every wavefront is
-  // done with the stages before they hold the write-back's staging rows
+  // the write-back's biases and row records into the weight stage that the
+  // last k-tile does not read (no wavefront reads it after the last
+  // k-tile's barrier); then every wavefront is done with the stages before
+  // they hold the write-back's staging rows
+  unsigned char *side = smem + kWBase + (nk & 1) * kStage;
   if (tid < 64) *reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(side) + tid * 4) = bias;
   reinterpret_cast<typename Epi::Row *>(side + 1024)[tid] = rec;
   barrier();
