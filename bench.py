@@ -427,6 +427,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=64)
     ap.add_argument("--config", type=int, default=3, help="workload id (2: MAR-B, 3: MAR-L, 4: MAR-H, 5: high-res)")
     ap.add_argument("--batch", type=int, default=None)
+    ap.add_argument("--micro-batches", type=int, default=1,
+                    help="split the batch into this many micro-batches of consecutive images, "
+                         "each on its own HIP stream (default 1: the whole batch on one stream)")
     ap.add_argument("--ratio-bp", type=int, default=None, help="refresh ratio in basis points")
     ap.add_argument("--full-every", type=int, default=None)
     ap.add_argument("--no-full-recompute", action="store_true")
@@ -511,7 +514,8 @@ def main() -> int:
     log(f"[bench] workload {cfg.name}: generating weights")
     weights = workload.all_weights(cfg)
     log("[bench] uploading")
-    eng = driver.Engine(cfg, batch=B, weights=weights, strategy=args.strategy)
+    eng = driver.MicroBatchEngine(cfg, batch=B, micro_batches=args.micro_batches, weights=weights,
+                                  strategy=args.strategy)
     torch.cuda.synchronize()
 
     log(f"[bench] warmup {args.warmup} steps")
@@ -541,6 +545,7 @@ def main() -> int:
                    "d_model": cfg.d_model, "n_heads": cfg.n_heads, "head_dim": cfg.head_dim,
                    "refresh_ratio": cfg.ratio_bp / 10000, "sel_layer": cfg.sel_layer,
                    "full_every": cfg.full_every, "decode_steps": T, "strategy": args.strategy,
+                   "micro_batches": args.micro_batches,
                    "full_steps_in_schedule": sum(p.full for p in eng.plans)},
         "step_us": step_us,
     }
@@ -596,7 +601,12 @@ def main() -> int:
         eng.set_schedule(cfg.full_every, "ratio", cfg.ratio_bp)
 
     if not args.no_roofline:
-        log(f"[bench] instrumented pass over the same {args.steps} steps")
+        # the same steps and micro-batches, run one micro-batch after another
+        # on one stream, so that each kernel's duration is its own and not
+        # stretched by a kernel of another micro-batch sharing the GPU
+        log(f"[bench] instrumented pass over the same {args.steps} steps "
+            f"({args.micro_batches} micro-batch(es) in turn on one stream)")
+        eng.overlap = False
         for i in range(args.warmup):
             eng.step(i % T)
         torch.cuda.synchronize()
@@ -606,6 +616,7 @@ def main() -> int:
             eng.step((first + i) % T)
         torch.cuda.synchronize()
         binding.profile_enable(False)
+        eng.overlap = True
         prof = binding.profile_collect()
         rates = kernel_rates(prof, cfg.dtype)
         dom = max(rates, key=lambda k: rates[k]["total_ms"])

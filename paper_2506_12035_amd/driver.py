@@ -70,7 +70,11 @@ class Engine:
                  policy: str = "ratio", budget: Optional[int] = None,
                  full_every: Optional[int] = None, sel_layer: Optional[int] = None,
                  weights: Optional[Sequence[Dict[str, np.ndarray]]] = None,
-                 strategy: str = "marche"):
+                 strategy: str = "marche", first_image: int = 0,
+                 share_weights_with: Optional["Engine"] = None):
+        """``batch`` images starting at image ``first_image`` of the workload's
+        batch; ``share_weights_with`` reuses another engine's resident
+        weights (same configuration) instead of uploading a copy."""
         if n_layers is not None:
             cfg = cfg.with_(n_layers=n_layers)
         self.cfg = cfg
@@ -95,9 +99,15 @@ class Engine:
                              cfg.d_mlp)
         self.model = binding.make_model(L, D, H, dh, F, N, self.dt, cfg.ln_eps)
 
-        ws = weights if weights is not None else [workload.layer_weights(cfg, l) for l in range(L)]
-        self.params = [self._upload_layer(w) for w in ws]
-        self.layers = binding.make_layers(self.params)
+        if share_weights_with is not None:
+            if share_weights_with.cfg != cfg or share_weights_with.device != self.device:
+                raise ValueError("shared weights belong to another configuration or device")
+            self.params, self.layers = share_weights_with.params, share_weights_with.layers
+        else:
+            ws = weights if weights is not None else [workload.layer_weights(cfg, l)
+                                                      for l in range(L)]
+            self.params = [self._upload_layer(w) for w in ws]
+            self.layers = binding.make_layers(self.params)
 
         es = 2 if cfg.dtype == "bf16" else 4
         n_el = L * self.B * H * N * dh
@@ -110,8 +120,9 @@ class Engine:
         self.ws_bytes = binding.workspace_bytes(self.model, self.B, self.B * N)
         self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
 
-        emb = workload.embeddings(cfg, self.B)
-        self.orders = workload.orders(cfg, self.B)
+        self.first_image = first_image
+        emb = workload.embeddings(cfg, self.B, first_image)
+        self.orders = workload.orders(cfg, self.B, first_image)
         rank = np.empty_like(self.orders)
         for b in range(self.B):
             rank[b, self.orders[b]] = np.arange(cfg.n_img, dtype=np.int32)
@@ -183,7 +194,7 @@ class Engine:
         ca[:, :lead.shape[1]] = lead
         if st == "random":
             cand = np.stack([np.setdiff1d(np.arange(N), excl[b]) for b in range(B)])
-            ca[:, lead.shape[1]:] = workload.random_refresh(c, t, cand, plan.k)
+            ca[:, lead.shape[1]:] = workload.random_refresh(c, t, cand, plan.k, self.first_image)
             plan.device_select = False
         plan.select_lowest = st == "low-attention"
         plan.a = a
@@ -264,6 +275,77 @@ class Engine:
             return None
         lead = p.a - p.k
         return p.ca_idx.view(self.B, p.a)[:, lead:].cpu().numpy()
+
+
+class MicroBatchEngine:
+    """The batch as ``micro_batches`` micro-batches of consecutive images, each
+    an ``Engine`` with its own KV cache, residual stream and workspace (the
+    weights are resident once and shared), each enqueued on a HIP stream of
+    its own.  Images are independent at every step, so the micro-batches
+    never exchange data: a step forks from the caller's current stream, runs
+    every micro-batch's step on its stream and joins back, and the GPU runs
+    the micro-batches' kernels side by side -- one's attention or row kernels
+    beside another's GEMMs, one's partly filled last wave of tiles beside
+    another's first.  Each image's results are those of one ``Engine`` over
+    the whole batch.  With ``overlap`` False the micro-batches run one after
+    another on the caller's stream (each kernel alone on the GPU, for per-
+    kernel timing).  Every stream has the default priority."""
+
+    def __init__(self, cfg: workload.Config, device: str = "cuda", batch: Optional[int] = None,
+                 micro_batches: int = 2, weights: Optional[Sequence[Dict[str, np.ndarray]]] = None,
+                 **engine_kw):
+        B = cfg.batch if batch is None else batch
+        S = micro_batches
+        if not 1 <= S <= max(B, 1):
+            raise ValueError(f"micro_batches={S} must lie in [1, batch={B}]")
+        sizes = [B // S + (1 if i < B % S else 0) for i in range(S)]
+        self.cfg, self.B = cfg, B
+        self.engines: List[Engine] = []
+        first = 0
+        for n in sizes:
+            share = self.engines[0] if self.engines else None
+            self.engines.append(Engine(cfg, device, batch=n, weights=None if share else weights,
+                                       first_image=first, share_weights_with=share, **engine_kw))
+            first += n
+        self.device = self.engines[0].device
+        self.streams = [torch.cuda.Stream(device=self.device) for _ in range(S - 1)]
+        self.overlap = True
+
+    @property
+    def plans(self) -> List[StepPlan]:
+        return self.engines[0].plans
+
+    def set_schedule(self, full_every: int, policy: str, budget: int) -> None:
+        for e in self.engines:
+            e.set_schedule(full_every, policy, budget)
+
+    def configure(self, **kw) -> None:
+        for e in self.engines:
+            e.configure(**kw)
+
+    def step(self, t: int) -> None:
+        """Step t of every micro-batch; done on the caller's current stream
+        when this returns (everything enqueued after it waits for it)."""
+        first, rest = self.engines[0], self.engines[1:]
+        if not self.overlap or not rest:
+            for e in self.engines:
+                e.step(t)
+            return
+        cur = torch.cuda.current_stream(self.device)
+        fork = torch.cuda.Event()
+        fork.record(cur)
+        first.step(t)
+        for e, s in zip(rest, self.streams):
+            s.wait_event(fork)
+            with torch.cuda.stream(s):
+                e.step(t)
+            done = torch.cuda.Event()
+            done.record(s)
+            cur.wait_event(done)
+
+    def generate(self, steps: Optional[Sequence[int]] = None) -> None:
+        for t in (range(self.cfg.n_steps) if steps is None else steps):
+            self.step(t)
 
 
 # ------------------------------------------------------------------ a whole MAR step

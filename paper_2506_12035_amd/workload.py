@@ -169,26 +169,35 @@ class Embeddings:
     pos: np.ndarray
 
 
-def embeddings(cfg: Config, batch: Optional[int] = None) -> Embeddings:
+def _image_range(cfg: Config, batch: Optional[int], first: int) -> slice:
     B = cfg.batch if batch is None else batch
+    if first < 0 or B < 0 or first + B > cfg.batch:
+        raise ValueError(f"images [{first}, {first + B}) outside the workload's {cfg.batch}")
+    return slice(first, first + B)
+
+
+def embeddings(cfg: Config, batch: Optional[int] = None, first: int = 0) -> Embeddings:
+    """Images ``first .. first + batch - 1`` of the workload's batch."""
+    sl = _image_range(cfg, batch, first)
     rng = streams(cfg.seed_value)[STREAM_STATE]
     D = cfg.d_model
-    cls = rng.standard_normal((cfg.batch, D), dtype=np.float32)[:B]
-    value = rng.standard_normal((cfg.batch, cfg.n_img, D), dtype=np.float32)[:B]
+    cls = rng.standard_normal((cfg.batch, D), dtype=np.float32)[sl]
+    value = rng.standard_normal((cfg.batch, cfg.n_img, D), dtype=np.float32)[sl]
     mask = rng.standard_normal((D,), dtype=np.float32)
     pos = rng.standard_normal((cfg.n_tokens, D), dtype=np.float32)
     return Embeddings(np.ascontiguousarray(cls), np.ascontiguousarray(value), mask, pos)
 
 
-def orders(cfg: Config, batch: Optional[int] = None) -> np.ndarray:
+def orders(cfg: Config, batch: Optional[int] = None, first: int = 0) -> np.ndarray:
     """Generation order per image: ``[B][N_img]``, a permutation of ``0..N_img-1``
-    (image-local positions; token index = ``n_buf + position``)."""
-    B = cfg.batch if batch is None else batch
+    (image-local positions; token index = ``n_buf + position``), for images
+    ``first .. first + batch - 1`` of the workload's batch."""
+    sl = _image_range(cfg, batch, first)
     rng = streams(cfg.seed_value)[STREAM_ORDERS]
     out = np.empty((cfg.batch, cfg.n_img), dtype=np.int32)
     for b in range(cfg.batch):
         out[b] = rng.permutation(cfg.n_img)
-    return out[:B].copy()
+    return out[sl].copy()
 
 
 @dataclass
@@ -240,14 +249,17 @@ def planted_rows(cfg: Config, candidates: np.ndarray, k: int, batch: Optional[in
     return out
 
 
-def random_refresh(cfg: Config, t: int, candidates: np.ndarray, k: int) -> np.ndarray:
+def random_refresh(cfg: Config, t: int, candidates: np.ndarray, k: int,
+                   first: int = 0) -> np.ndarray:
     """Seeded random refresh set of step ``t`` for the random-refresh ablation:
-    ``candidates`` is [B][n_cand] per image; returns [B][k] (ascending), drawn
-    without replacement from each image's candidates."""
-    ss = np.random.SeedSequence([cfg.seed_value, STREAM_PLANTED, 1 + t])
-    rng = np.random.Generator(np.random.PCG64(ss))
+    ``candidates`` is [B][n_cand] per image (images ``first`` ..); returns
+    [B][k] (ascending), drawn without replacement from each image's
+    candidates with a generator of its own (seeded by step and image), so an
+    image's draw does not depend on which other images share the call."""
     out = np.empty((candidates.shape[0], k), dtype=np.int32)
     for b in range(candidates.shape[0]):
+        ss = np.random.SeedSequence([cfg.seed_value, STREAM_PLANTED, 1 + t, first + b])
+        rng = np.random.Generator(np.random.PCG64(ss))
         out[b] = np.sort(rng.choice(candidates[b], size=k, replace=False))
     return out
 

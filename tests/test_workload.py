@@ -44,3 +44,29 @@ def test_config_shapes():
         assert c.d_model == c.n_heads * c.head_dim
         assert c.d_mlp == 4 * c.d_model
     assert workload.CONFIGS[5].n_tokens == 1088 and workload.CONFIGS[4].head_dim == 80
+
+
+def test_image_ranges_are_slices_of_the_whole_batch():
+    cfg = workload.CONFIGS[2].with_(batch=7, d_model=64, n_heads=4, head_dim=16, d_mlp=256)
+    whole_e, whole_o = workload.embeddings(cfg), workload.orders(cfg)
+    part_e, part_o = workload.embeddings(cfg, 3, first=2), workload.orders(cfg, 3, first=2)
+    np.testing.assert_array_equal(part_o, whole_o[2:5])
+    np.testing.assert_array_equal(part_e.cls, whole_e.cls[2:5])
+    np.testing.assert_array_equal(part_e.value, whole_e.value[2:5])
+    np.testing.assert_array_equal(part_e.pos, whole_e.pos)
+    np.testing.assert_array_equal(part_e.mask, whole_e.mask)
+    for bad in ((5, 3), (-1, 0)):
+        with np.testing.assert_raises(ValueError):
+            workload.orders(cfg, *bad)
+
+
+def test_random_refresh_draws_per_image():
+    cfg = workload.CONFIGS[2]
+    rng = np.random.default_rng(3)
+    cand = np.stack([np.sort(rng.choice(320, size=200, replace=False)) for _ in range(6)]).astype(np.int32)
+    whole = workload.random_refresh(cfg, 4, cand, 20)
+    np.testing.assert_array_equal(workload.random_refresh(cfg, 4, cand[2:5], 20, first=2), whole[2:5])
+    for b in range(6):
+        assert len(set(whole[b].tolist())) == 20 and set(whole[b].tolist()) <= set(cand[b].tolist())
+        assert list(whole[b]) == sorted(whole[b])
+    assert not np.array_equal(whole, workload.random_refresh(cfg, 5, cand, 20))
