@@ -589,17 +589,38 @@ __device__ __forceinline__ void barrier_vm() {
   asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(VM) : "memory");
 }
 
+// The same with the loads of n whole k-tiles (six per wavefront each) still
+// in flight, n in [0, NS - 2].
+template <int NS>
+__device__ __forceinline__ void barrier_tiles(int n) {
+  static_assert(NS >= 3 && NS <= 7, "stage count");
+  if (NS > 6 && n >= 5) barrier_vm<30>();
+  else if (NS > 5 && n >= 4) barrier_vm<24>();
+  else if (NS > 4 && n >= 3) barrier_vm<18>();
+  else if (NS > 3 && n >= 2) barrier_vm<12>();
+  else if (n >= 1) barrier_vm<6>();
+  else barrier_vm<0>();
+}
+
 }  // namespace pair
 
-template <class Epi>
-__global__ __launch_bounds__(256, 2) void gemm_bf16_pair_kernel(const bf16 *A, const bf16 *W,
-                                                                int M, int N, int K, Epi epi) {
+// NS stages of 24 KB: three when two workgroups share a CU; six for long
+// reductions (K >= 2048) whose workgroups each have a CU to themselves, so
+// that operands streamed from HBM (a cache-aware fc2's hidden rows, a
+// layer's weights not touched since the previous step) have five k-tiles to
+// land instead of two (measured: 82 -> 78 us for a cache-aware MAR-L fc2 with
+// operands not in any cache; short reductions gain nothing).  The loads of
+// k-tile t+NS go into the stage k-tile t leaves, issued once every wavefront
+// is done with k-tile t.
+template <class Epi, int NS>
+__global__ __launch_bounds__(256, NS <= 3 ? 2 : 1) void gemm_bf16_pair_kernel(
+    const bf16 *A, const bf16 *W, int M, int N, int K, Epi epi) {
   using namespace pair;
   using big::pin;
   using Row = typename Epi::Row;
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[3 * kStage];
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[NS * kStage];
   __shared__ __attribute__((aligned(16))) Row rows_lds[kBM];
-  static_assert(4 * 32 * big::kWbStride * 4 <= 3 * kStage, "staged write-back fits the stages");
+  static_assert(4 * 32 * big::kWbStride * 4 <= NS * kStage, "staged write-back fits the stages");
   const int tiles_m = (M + kBM - 1) / kBM, tiles_n = N / kBN;
   int tm, tn;
   tile_coords(xcd_remap(blockIdx.x, gridDim.x), tiles_m, tiles_n, tm, tn);
@@ -615,6 +636,7 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_pair_kernel(const bf16 *A, c
 #pragma unroll
     for (int i = 0; i < 2; ++i) acc[j][i] = f32x16{};
   const int nk = K / kBK;
+  auto stage = [&](int kt) { return lds0 + (unsigned)(kt % NS) * kStage; };
 
   // The write-back's row record (threads < 128) and bias (each lane's four
   // columns), loaded before the tile loads and kept in registers: they reach
@@ -623,64 +645,63 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_pair_kernel(const bf16 *A, c
   if (tid < kBM) rec = epi.row(min(m0 + tid, M - 1));
   const f32x4 bias = epi.bias4(n0 + wn * 128 + (lane & 31) * 4);
 
-  // k-tiles 0 and 1 and the first half of k-tile 2
-  unsigned s0 = lds0, s1 = lds0 + kStage, s2 = lds0 + 2 * kStage;
+  // k-tiles 0 .. NS-2 and the first half of k-tile NS-1, then wait for k-tile 0
 #pragma unroll
-  for (int p = 0; p < kLoads; ++p) load_lds(s0, q0 + p, A, W, M, K, m0, n0, 0, lane);
-  if (nk > 1) {
+  for (int kt = 0; kt + 1 < NS; ++kt) {
+    if (kt < nk) {
 #pragma unroll
-    for (int p = 0; p < kLoads; ++p) load_lds(s1, q0 + p, A, W, M, K, m0, n0, kBK, lane);
+      for (int p = 0; p < kLoads; ++p)
+        load_lds(lds0 + kt * kStage, q0 + p, A, W, M, K, m0, n0, kt * kBK, lane);
+    }
   }
-  if (nk > 2) {
+  if (nk >= NS) {
 #pragma unroll
-    for (int p = 0; p < 3; ++p) load_lds(s2, q0 + p, A, W, M, K, m0, n0, 2 * kBK, lane);
+    for (int p = 0; p < 3; ++p)
+      load_lds(lds0 + (NS - 1) * kStage, q0 + p, A, W, M, K, m0, n0, (NS - 1) * kBK, lane);
+    barrier_vm<6 * (NS - 2) + 3>();
+  } else {
+    barrier_tiles<NS>(nk - 1);
   }
-  if (nk > 2) barrier_vm<9>();
-  else if (nk > 1) barrier_vm<6>();
-  else barrier_vm<0>();
   Frag fa, fb;
   const unsigned char *smem_u = smem;
 #pragma unroll
-  for (int r = 0; r < 6; ++r) read_frag(fa, r, smem_u + (s0 - lds0), 0, wm, wn, lane);
+  for (int r = 0; r < 6; ++r) read_frag(fa, r, smem_u, 0, wm, wn, lane);
 
   for (int t = 0; t + 1 < nk; ++t) {
-    // s0: k-tile t; s1: k-tile t+1; s2: k-tile t+2 (its first half in flight)
-    const bool has2 = t + 2 < nk, has3 = t + 3 < nk;
-    const int k2 = (t + 2) * kBK, k3 = (t + 3) * kBK;
-    const unsigned char *sc = smem_u + (s0 - lds0), *sn = smem_u + (s1 - lds0);
-    // k16 step 0: step-1 fragments; second half of k-tile t+2
+    // k-tile t+NS-1: its first half is in flight, the rest goes out now;
+    // k-tile t+NS: into k-tile t's stage once every wavefront is done with it
+    const int kl = t + NS - 1, kn = t + NS;
+    const bool has_l = kl < nk, has_n = kn < nk;
+    const unsigned sl = stage(kl), s_t = stage(t);
+    const unsigned char *sc = smem_u + (s_t - lds0), *sn = smem_u + (stage(t + 1) - lds0);
+    // k16 step 0: step-1 fragments; loads 3 and 4 of k-tile t+NS-1
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       mfma(acc, fa, q);
       if (q < 6) read_frag(fb, q, sc, 1, wm, wn, lane);
-      else if (has2) load_lds(s2, q0 + 3 + (q - 6), A, W, M, K, m0, n0, k2, lane);
+      else if (has_l) load_lds(sl, q0 + 3 + (q - 6), A, W, M, K, m0, n0, kl * kBK, lane);
       pin();
     }
-    // k16 step 1: last load of k-tile t+2; barrier (k-tile t+1 complete,
+    // k16 step 1: load 5 of k-tile t+NS-1; barrier (k-tile t+1 complete,
     // k-tile t read by all); step-0 fragments of k-tile t+1; first half of
-    // k-tile t+3 into the stage k-tile t leaves
+    // k-tile t+NS into the stage k-tile t leaves
     mfma(acc, fb, 0);
-    if (has2) load_lds(s2, q0 + 5, A, W, M, K, m0, n0, k2, lane);
+    if (has_l) load_lds(sl, q0 + 5, A, W, M, K, m0, n0, kl * kBK, lane);
     pin();
     mfma(acc, fb, 1);
     pin();
-    if (has2) barrier_vm<6>();
-    else barrier_vm<0>();
+    barrier_tiles<NS>(min(NS - 2, nk - t - 2));
     pin();
 #pragma unroll
     for (int q = 2; q < 8; ++q) {
       mfma(acc, fb, q);
       read_frag(fa, q - 2, sn, 0, wm, wn, lane);
-      if (q >= 5 && has3) load_lds(s0, q0 + (q - 5), A, W, M, K, m0, n0, k3, lane);
+      if (q >= 5 && has_n) load_lds(s_t, q0 + (q - 5), A, W, M, K, m0, n0, kn * kBK, lane);
       pin();
     }
-    const unsigned s_old = s0;
-    s0 = s1;
-    s1 = s2;
-    s2 = s_old;
   }
   {  // last k-tile
-    const unsigned char *sc = smem_u + (s0 - lds0);
+    const unsigned char *sc = smem_u + (stage(nk - 1) - lds0);
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       mfma(acc, fa, q);
@@ -887,9 +908,13 @@ static hipError_t run_bf16(const void *a, const void *w, int m, int n, int k, co
       gemm_bf16_small_kernel<Epi>
           <<<((m + small::kBM - 1) / small::kBM) * (n / small::kBN), 256, 0, s>>>(A, W, m, n, k, epi);
       break;
-    default:
-      gemm_bf16_pair_kernel<Epi>
-          <<<((m + pair::kBM - 1) / pair::kBM) * (n / pair::kBN), 256, 0, s>>>(A, W, m, n, k, epi);
+    default: {
+      const int tiles = ((m + pair::kBM - 1) / pair::kBM) * (n / pair::kBN);
+      if (tiles <= device_cu_count() && k >= 2048)
+        gemm_bf16_pair_kernel<Epi, 6><<<tiles, 256, 0, s>>>(A, W, m, n, k, epi);
+      else
+        gemm_bf16_pair_kernel<Epi, 3><<<tiles, 256, 0, s>>>(A, W, m, n, k, epi);
+    }
   }
   return hipGetLastError();
 }
