@@ -327,7 +327,23 @@ __global__ __launch_bounds__(NW * 64) void attn_resident_kernel(AttnArgs a) {
       Vt[t][DH * (TK + 8) + rem] = (bf16)0.0f;
     }
   }
-  // all tiles' loads first, then all LDS writes
+  // this wavefront's queries of every block it computes, issued first so
+  // that their latency hides behind the K/V loads instead of stalling the
+  // start of each block
+  bf16x8 qall[NQB][QS];
+#pragma unroll
+  for (int qb = 0; qb < NQB; ++qb) {
+    const int wq0 = (qb * NW + wave) * 32;
+    if (wq0 < na) {
+      const int qi = wq0 + (lane & 31);
+      const bf16 *qrow =
+          static_cast<const bf16 *>(a.q) + (size_t)(r0 + min(qi, na - 1)) * D + h * DH;
+#pragma unroll
+      for (int st = 0; st < QS; ++st)
+        qall[qb][st] = *reinterpret_cast<const bf16x8 *>(qrow + st * 16 + (lane >> 5) * 8);
+    }
+  }
+  // all tiles' loads, then all LDS writes
   u32x4 rk[NTL][LPT], rv0[NTL][LPV], rv1[NTL][LPV];
 #pragma unroll
   for (int t = 0; t < NTL; ++t) {
@@ -382,16 +398,12 @@ __global__ __launch_bounds__(NW * 64) void attn_resident_kernel(AttnArgs a) {
   __syncthreads();
 
   const float sl2 = 1.4426950408889634f / sqrtf((float)DH);
-#pragma unroll 1
+#pragma unroll
   for (int qb = 0; qb < NQB; ++qb) {
     const int wq0 = (qb * NW + wave) * 32;
     if (wq0 >= na) break;  // uniform over the wavefront; no barrier follows
     const int qi = wq0 + (lane & 31);
-    const bf16 *qrow = static_cast<const bf16 *>(a.q) + (size_t)(r0 + min(qi, na - 1)) * D + h * DH;
-    bf16x8 qf[QS];
-#pragma unroll
-    for (int st = 0; st < QS; ++st)
-      qf[st] = *reinterpret_cast<const bf16x8 *>(qrow + st * 16 + (lane >> 5) * 8);
+    const bf16x8 (&qf)[QS] = qall[qb];
     float m_run = -INFINITY, l_run = 0.f;
     f32x16 acc[ODB];
 #pragma unroll
