@@ -237,7 +237,7 @@ def appb_main(args) -> int:
       torch_cat   = the same with torch.cat as the concatenation;
       two_segment = one pass over the two segments' own buffers (the method);
       resident    = attention over one buffer that already holds both segments
-                    (this build's production layout: the QKV epilogue writes the
+                    (the library's production layout: the QKV epilogue writes the
                     fresh rows into the cache, so no merge step exists at all).
     Each timed with HIP events over 20 calls after 3 warm-up calls."""
     import numpy as np
@@ -471,8 +471,8 @@ def main() -> int:
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
-              "the decode step shards over images without collectives and no multi-GPU run is "
-              "part of this build", file=sys.stderr)
+              "the decode step shards over images without collectives; this benchmark "
+              "measures one GPU's share", file=sys.stderr)
         return 2
     if args.steps < 1 or args.warmup < 0:
         print("--steps must be >= 1 and --warmup >= 0", file=sys.stderr)
