@@ -427,9 +427,10 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=64)
     ap.add_argument("--config", type=int, default=3, help="workload id (2: MAR-B, 3: MAR-L, 4: MAR-H, 5: high-res)")
     ap.add_argument("--batch", type=int, default=None)
-    ap.add_argument("--micro-batches", type=int, default=1,
-                    help="split the batch into this many micro-batches of consecutive images, "
-                         "each on its own HIP stream (default 1: the whole batch on one stream)")
+    ap.add_argument("--micro-batches", type=int, default=2,
+                    help="run the cache-aware layers of every cache-aware step as this many "
+                         "ranges of consecutive images, each on its own HIP stream (default 2; "
+                         "1: the whole batch in one call)")
     ap.add_argument("--ratio-bp", type=int, default=None, help="refresh ratio in basis points")
     ap.add_argument("--full-every", type=int, default=None)
     ap.add_argument("--no-full-recompute", action="store_true")
@@ -514,8 +515,8 @@ def main() -> int:
     log(f"[bench] workload {cfg.name}: generating weights")
     weights = workload.all_weights(cfg)
     log("[bench] uploading")
-    eng = driver.MicroBatchEngine(cfg, batch=B, micro_batches=args.micro_batches, weights=weights,
-                                  strategy=args.strategy)
+    eng = driver.Engine(cfg, batch=B, weights=weights, strategy=args.strategy,
+                        micro_batches=args.micro_batches)
     torch.cuda.synchronize()
 
     log(f"[bench] warmup {args.warmup} steps")
@@ -601,11 +602,11 @@ def main() -> int:
         eng.set_schedule(cfg.full_every, "ratio", cfg.ratio_bp)
 
     if not args.no_roofline:
-        # the same steps and micro-batches, run one micro-batch after another
-        # on one stream, so that each kernel's duration is its own and not
-        # stretched by a kernel of another micro-batch sharing the GPU
+        # the same steps and image ranges, the ranges one after another on one
+        # stream, so that each kernel's duration is its own and not stretched
+        # by a kernel of another range sharing the GPU
         log(f"[bench] instrumented pass over the same {args.steps} steps "
-            f"({args.micro_batches} micro-batch(es) in turn on one stream)")
+            f"({args.micro_batches} image range(s) in turn on one stream)")
         eng.overlap = False
         for i in range(args.warmup):
             eng.step(i % T)

@@ -143,6 +143,25 @@ marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layer
                             int32_t a_max, int32_t gen_max, float *scores, int32_t score_layer,
                             void *workspace, size_t workspace_bytes, marche_stream_t stream);
 
+/* marche_step over images [first_image, first_image + batch) of `cache`
+ * (Algorithm 1 runs per image, so any group of images is a step of its
+ * own).  x, a_idx / a_off / n_gen, scores and the workspace describe only
+ * those images: image first_image of the cache is image 0 of the call, a_off
+ * starts at 0, x points at that image's [n_tokens][d_model] rows and scores
+ * (if any) at its [n_heads][n_tokens] block.  The cache's other images are
+ * neither read nor written, so calls on disjoint image ranges may run
+ * concurrently on different streams, each with its own workspace.
+ * marche_step is this call with first_image = 0.  Returns INVALID_ARG when
+ * the range leaves the cache, otherwise as marche_step. */
+marche_status_t marche_step_images(const marche_model_t *m, const marche_layer_t *layers,
+                                   const marche_kv_cache_t *cache, int32_t first_image,
+                                   int32_t layer_begin, int32_t layer_end, int32_t batch, float *x,
+                                   const int32_t *a_idx, const int32_t *a_off,
+                                   const int32_t *n_gen, int32_t a_total, int32_t a_max,
+                                   int32_t gen_max, float *scores, int32_t score_layer,
+                                   void *workspace, size_t workspace_bytes,
+                                   marche_stream_t stream);
+
 /* Refresh selection (Section 4.2, top-k of the head-aggregated scores).
  * For each image b: s_j = sum_{p < n_parts} scores[b][p][j] (summed in p
  * order, float32); candidates are the tokens not in

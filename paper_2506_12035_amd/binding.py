@@ -22,7 +22,8 @@ MARCHE_SELECT_HIGHEST, MARCHE_SELECT_LOWEST = 0, 1
 MARCHE_ATTN_TWO_SEGMENT, MARCHE_ATTN_CONCAT = 0, 1
 
 EXPORTED = (
-    "kv_cache_init", "marche_step_workspace_bytes", "marche_step", "select_refresh",
+    "kv_cache_init", "marche_step_workspace_bytes", "marche_step", "marche_step_images",
+    "select_refresh",
     "select_refresh_ordered",
     "marche_decoder_input", "marche_attention_workspace_bytes", "marche_attention_segments",
     "marche_encoder_input", "marche_encoder_to_decoder_workspace_bytes",
@@ -83,6 +84,9 @@ def lib() -> C.CDLL:
         L.marche_step_workspace_bytes.restype = sz
         L.marche_step.argtypes = [C.POINTER(Model), C.POINTER(Layer), C.POINTER(KVCache), i32, i32,
                                   i32, vp, vp, vp, vp, i32, i32, i32, vp, i32, vp, sz, vp]
+        L.marche_step_images.argtypes = [C.POINTER(Model), C.POINTER(Layer), C.POINTER(KVCache),
+                                         i32, i32, i32, i32, vp, vp, vp, vp, i32, i32, i32, vp,
+                                         i32, vp, sz, vp]
         L.select_refresh.argtypes = [vp, i32, vp, vp, i32, i32, i32, vp, vp, vp]
         L.select_refresh_ordered.argtypes = [vp, i32, vp, vp, i32, i32, i32, vp, vp, i32, vp]
         L.marche_decoder_input.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, vp]
@@ -113,7 +117,8 @@ def lib() -> C.CDLL:
                                            C.POINTER(C.c_double)]
         L.marche_profile_reset.argtypes = []
         L.marche_profile_reset.restype = None
-        for name in ("kv_cache_init", "marche_step", "select_refresh", "select_refresh_ordered",
+        for name in ("kv_cache_init", "marche_step", "marche_step_images", "select_refresh",
+                     "select_refresh_ordered",
                      "marche_decoder_input", "marche_attention_segments",
                      "marche_encoder_input", "marche_encoder_to_decoder",
                      "marche_diffusion_sample", "marche_profile_enable", "marche_profile_entry"):
@@ -184,6 +189,17 @@ def marche_step(model: Model, layers, cache: KVCache, layer_begin: int, layer_en
                              _ptr(x), _ptr(a_idx), _ptr(a_off), _ptr(n_gen), a_total, a_max,
                              gen_max, _ptr(scores), score_layer, _ptr(workspace), workspace_bytes,
                              _stream(stream)))
+
+
+def marche_step_images(model: Model, layers, cache: KVCache, first_image: int, layer_begin: int,
+                       layer_end: int, batch: int, x, a_idx, a_off, n_gen, a_total: int,
+                       a_max: int, gen_max: int, scores=None, score_layer: int = -1,
+                       workspace=None, workspace_bytes: int = 0, stream=None) -> None:
+    _check(lib().marche_step_images(C.byref(model), layers, C.byref(cache), first_image,
+                                    layer_begin, layer_end, batch, _ptr(x), _ptr(a_idx),
+                                    _ptr(a_off), _ptr(n_gen), a_total, a_max, gen_max,
+                                    _ptr(scores), score_layer, _ptr(workspace), workspace_bytes,
+                                    _stream(stream)))
 
 
 def select_refresh(scores, n_parts: int, excl_idx, excl_off, batch: int, n_tokens: int, k: int,

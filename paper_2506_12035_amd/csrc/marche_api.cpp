@@ -253,12 +253,13 @@ size_t marche_step_workspace_bytes(const marche_model_t *m, int32_t batch, int32
          align256(M * m->d_mlp * es);
 }
 
-marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layers,
-                            const marche_kv_cache_t *cache, int32_t layer_begin,
-                            int32_t layer_end, int32_t batch, float *x, const int32_t *a_idx,
-                            const int32_t *a_off, const int32_t *n_gen, int32_t a_total,
-                            int32_t a_max, int32_t gen_max, float *scores, int32_t score_layer,
-                            void *workspace, size_t workspace_bytes, marche_stream_t stream_) {
+static marche_status_t step_impl(const marche_model_t *m, const marche_layer_t *layers,
+                                 const marche_kv_cache_t *cache, int32_t first_image,
+                                 int32_t layer_begin, int32_t layer_end, int32_t batch, float *x,
+                                 const int32_t *a_idx, const int32_t *a_off, const int32_t *n_gen,
+                                 int32_t a_total, int32_t a_max, int32_t gen_max, float *scores,
+                                 int32_t score_layer, void *workspace, size_t workspace_bytes,
+                                 marche_stream_t stream_) {
   marche_status_t st = check_model(m);
   if (st != MARCHE_OK) return st;
   if (!layers) return fail(MARCHE_ERR_INVALID_ARG, "layers is NULL");
@@ -269,6 +270,9 @@ marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layer
     return fail(MARCHE_ERR_INVALID_ARG, "cache shape/dtype does not match the model");
   if (batch < 0 || batch > cache->batch)
     return fail(MARCHE_ERR_INVALID_ARG, "batch=%d outside [0, cache.batch=%d]", batch, cache->batch);
+  if (first_image < 0 || first_image > cache->batch - batch)
+    return fail(MARCHE_ERR_INVALID_ARG, "images [%d, %d) outside the cache's [0, %d)", first_image,
+                first_image + batch, cache->batch);
   if (layer_begin < 0 || layer_end < layer_begin || layer_end > m->n_layers)
     return fail(MARCHE_ERR_INVALID_ARG, "layer range [%d, %d) outside [0, %d]", layer_begin,
                 layer_end, m->n_layers);
@@ -330,8 +334,10 @@ marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layer
 
   for (int l = layer_begin; l < layer_end; ++l) {
     const marche_layer_t &L = layers[l];
-    char *kc = static_cast<char *>(cache->k) + (size_t)l * layer_elems * es;
-    char *vc = static_cast<char *>(cache->v) + (size_t)l * layer_elems * es;
+    // layer l, image first_image: the call's image 0
+    const size_t base = ((size_t)l * layer_elems + (size_t)first_image * H * N * dh) * es;
+    char *kc = static_cast<char *>(cache->k) + base;
+    char *vc = static_cast<char *>(cache->v) + base;
 
     LAUNCH(K_GATHER_LN, 0, (double)M * D * (4 + es),
            launch_gather_ln(dt, buf0, x, map, static_cast<const float *>(L.ln1_g),
@@ -367,6 +373,29 @@ marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layer
                              1, stream));
   }
   return MARCHE_OK;
+}
+
+marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layers,
+                            const marche_kv_cache_t *cache, int32_t layer_begin,
+                            int32_t layer_end, int32_t batch, float *x, const int32_t *a_idx,
+                            const int32_t *a_off, const int32_t *n_gen, int32_t a_total,
+                            int32_t a_max, int32_t gen_max, float *scores, int32_t score_layer,
+                            void *workspace, size_t workspace_bytes, marche_stream_t stream) {
+  return step_impl(m, layers, cache, 0, layer_begin, layer_end, batch, x, a_idx, a_off, n_gen,
+                   a_total, a_max, gen_max, scores, score_layer, workspace, workspace_bytes, stream);
+}
+
+marche_status_t marche_step_images(const marche_model_t *m, const marche_layer_t *layers,
+                                   const marche_kv_cache_t *cache, int32_t first_image,
+                                   int32_t layer_begin, int32_t layer_end, int32_t batch, float *x,
+                                   const int32_t *a_idx, const int32_t *a_off,
+                                   const int32_t *n_gen, int32_t a_total, int32_t a_max,
+                                   int32_t gen_max, float *scores, int32_t score_layer,
+                                   void *workspace, size_t workspace_bytes,
+                                   marche_stream_t stream) {
+  return step_impl(m, layers, cache, first_image, layer_begin, layer_end, batch, x, a_idx, a_off,
+                   n_gen, a_total, a_max, gen_max, scores, score_layer, workspace,
+                   workspace_bytes, stream);
 }
 
 marche_status_t select_refresh(const float *scores, int32_t n_parts, const int32_t *excl_idx,

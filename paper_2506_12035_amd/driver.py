@@ -9,11 +9,13 @@ One step t of a batch of images (Section 4.2-4.3, Algorithm 1):
   and the generating tokens first, writing the selection layer's per-head
   attention mass; select_refresh picks R per image into the tail of the
   cache-aware active list [G | N | R]; marche_step over layers
-  [sel_layer, L) on that list.
+  [sel_layer, L) on that list -- or, with micro_batches > 1, the selection
+  and those layers per range of consecutive images (marche_step_images),
+  each range on its own stream.
 
 All index lists of every step are built on the host once, before decoding,
-and kept resident on the device; a step issues only kernel launches on one
-stream (no host synchronisation, no host-device copies).
+and kept resident on the device; a step issues only kernel launches and
+stream events (no host synchronisation, no host-device copies).
 """
 from __future__ import annotations
 
@@ -60,6 +62,24 @@ class StepPlan:
     out_off: Optional[torch.Tensor] = None
     device_select: bool = True                # R chosen on the device from the scores
     select_lowest: bool = False
+    parts: Optional[list] = None              # per image range of a split step (RangePlan)
+
+
+@dataclass
+class RangePlan:
+    """The cache-aware lists of one range of consecutive images: views of the
+    step's lists with offsets rebased to the range's first image, and the
+    range's piece of the workspace."""
+    first: int
+    count: int
+    ca_idx: torch.Tensor
+    ca_off: torch.Tensor
+    ca_gen: torch.Tensor
+    excl_idx: torch.Tensor
+    excl_off: torch.Tensor
+    out_off: torch.Tensor
+    ws_offset: int
+    ws_bytes: int
 
 
 class Engine:
@@ -70,11 +90,11 @@ class Engine:
                  policy: str = "ratio", budget: Optional[int] = None,
                  full_every: Optional[int] = None, sel_layer: Optional[int] = None,
                  weights: Optional[Sequence[Dict[str, np.ndarray]]] = None,
-                 strategy: str = "marche", first_image: int = 0,
-                 share_weights_with: Optional["Engine"] = None):
+                 strategy: str = "marche", first_image: int = 0, micro_batches: int = 1):
         """``batch`` images starting at image ``first_image`` of the workload's
-        batch; ``share_weights_with`` reuses another engine's resident
-        weights (same configuration) instead of uploading a copy."""
+        batch.  ``micro_batches`` > 1 splits the cache-aware layers of every
+        cache-aware step into that many ranges of consecutive images, each
+        enqueued on a HIP stream of its own (see ``step``)."""
         if n_layers is not None:
             cfg = cfg.with_(n_layers=n_layers)
         self.cfg = cfg
@@ -99,15 +119,9 @@ class Engine:
                              cfg.d_mlp)
         self.model = binding.make_model(L, D, H, dh, F, N, self.dt, cfg.ln_eps)
 
-        if share_weights_with is not None:
-            if share_weights_with.cfg != cfg or share_weights_with.device != self.device:
-                raise ValueError("shared weights belong to another configuration or device")
-            self.params, self.layers = share_weights_with.params, share_weights_with.layers
-        else:
-            ws = weights if weights is not None else [workload.layer_weights(cfg, l)
-                                                      for l in range(L)]
-            self.params = [self._upload_layer(w) for w in ws]
-            self.layers = binding.make_layers(self.params)
+        ws = weights if weights is not None else [workload.layer_weights(cfg, l) for l in range(L)]
+        self.params = [self._upload_layer(w) for w in ws]
+        self.layers = binding.make_layers(self.params)
 
         es = 2 if cfg.dtype == "bf16" else 4
         n_el = L * self.B * H * N * dh
@@ -119,6 +133,13 @@ class Engine:
         self.scores = torch.empty(self.B, H, N, dtype=torch.float32, device=self.device)
         self.ws_bytes = binding.workspace_bytes(self.model, self.B, self.B * N)
         self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+        S = micro_batches
+        if not 1 <= S <= max(self.B, 1):
+            raise ValueError(f"micro_batches={S} must lie in [1, batch={self.B}]")
+        sizes = [self.B // S + (1 if i < self.B % S else 0) for i in range(S)]
+        self.ranges = [(sum(sizes[:i]), sizes[i]) for i in range(S)]  # (first image, count)
+        self.streams = [torch.cuda.Stream(device=self.device) for _ in range(S - 1)]
+        self.overlap = True  # False: the ranges one after another on the current stream
 
         self.first_image = first_image
         emb = workload.embeddings(cfg, self.B, first_image)
@@ -206,7 +227,26 @@ class Engine:
         plan.excl_idx = _dev_i32(excl.reshape(-1), self.device)
         plan.excl_off = _dev_i32(np.arange(B + 1) * excl.shape[1], self.device)
         plan.out_off = _dev_i32(np.arange(B) * a + lead.shape[1], self.device)
+        if len(self.ranges) > 1:
+            plan.parts = self._range_plans(plan, excl.shape[1], lead.shape[1])
         return plan
+
+    def _range_plans(self, plan: StepPlan, n_excl: int, n_lead: int) -> List[RangePlan]:
+        B, a = self.B, plan.a
+        parts, off = [], 0
+        for first, n in self.ranges:
+            sl = slice(first, first + n)
+            ws = binding.workspace_bytes(self.model, n, n * a)
+            parts.append(RangePlan(
+                first, n, plan.ca_idx.view(B, a)[sl].reshape(-1),
+                _dev_i32(np.arange(n + 1) * a, self.device), plan.ca_gen[sl],
+                plan.excl_idx.view(B, n_excl)[sl].reshape(-1),
+                _dev_i32(np.arange(n + 1) * n_excl, self.device),
+                _dev_i32(np.arange(n) * a + n_lead, self.device), off, ws))
+            off += (ws + 255) // 256 * 256
+        if off > self.ws_bytes:
+            raise RuntimeError(f"image ranges need {off} workspace bytes > {self.ws_bytes}")
+        return parts
 
     # ------------------------------------------------------------------ step
 
@@ -243,9 +283,48 @@ class Engine:
             return
         self.run_layers(0, self.sel, p.full_idx, p.full_off, B * N, N, p.g, p.n_gen,
                         score_layer=self.sel - 1 if p.device_select else -1)
-        self.select(p)
+        if p.parts is None:
+            self.select(p)
+            if p.a > 0:
+                self.run_layers(self.sel, L, p.ca_idx, p.ca_off, B * p.a, p.a, p.ca_gen_max,
+                                p.ca_gen)
+            return
+        # The selection and the cache-aware layers per image range, each range
+        # on its own stream between a fork from and a join back into the
+        # current one: ranges share no rows, so their kernels overlap on the
+        # GPU (one range's attention beside another's GEMMs, one's partly
+        # filled last wave of tiles beside another's first).
+        if not self.overlap:
+            for part in p.parts:
+                self._cache_aware_range(p, part)
+            return
+        cur = self.stream
+        fork = torch.cuda.Event()
+        fork.record(cur)
+        for i, part in enumerate(p.parts):
+            s = cur if i == 0 else self.streams[i - 1]
+            if i > 0:
+                s.wait_event(fork)
+            with torch.cuda.stream(s):
+                self._cache_aware_range(p, part)
+            if i > 0:
+                done = torch.cuda.Event()
+                done.record(s)
+                cur.wait_event(done)
+
+    def _cache_aware_range(self, p: StepPlan, r: RangePlan) -> None:
+        c = self.cfg
+        sl = slice(r.first, r.first + r.count)
+        if p.device_select:
+            binding.select_refresh(self.scores[sl], c.n_heads, r.excl_idx, r.excl_off, r.count,
+                                   c.n_tokens, p.k, r.ca_idx, r.out_off, stream=self.stream,
+                                   lowest=p.select_lowest)
         if p.a > 0:
-            self.run_layers(self.sel, L, p.ca_idx, p.ca_off, B * p.a, p.a, p.ca_gen_max, p.ca_gen)
+            ws = self.workspace[r.ws_offset:r.ws_offset + r.ws_bytes]
+            binding.marche_step_images(self.model, self.layers, self.cache, r.first, self.sel,
+                                       c.n_layers, r.count, self.x[sl], r.ca_idx, r.ca_off,
+                                       r.ca_gen, r.count * p.a, p.a, p.ca_gen_max, None, -1, ws,
+                                       r.ws_bytes, stream=self.stream)
 
     def generate(self, steps: Optional[Sequence[int]] = None) -> None:
         for t in (range(self.cfg.n_steps) if steps is None else steps):
@@ -275,77 +354,6 @@ class Engine:
             return None
         lead = p.a - p.k
         return p.ca_idx.view(self.B, p.a)[:, lead:].cpu().numpy()
-
-
-class MicroBatchEngine:
-    """The batch as ``micro_batches`` micro-batches of consecutive images, each
-    an ``Engine`` with its own KV cache, residual stream and workspace (the
-    weights are resident once and shared), each enqueued on a HIP stream of
-    its own.  Images are independent at every step, so the micro-batches
-    never exchange data: a step forks from the caller's current stream, runs
-    every micro-batch's step on its stream and joins back, and the GPU runs
-    the micro-batches' kernels side by side -- one's attention or row kernels
-    beside another's GEMMs, one's partly filled last wave of tiles beside
-    another's first.  Each image's results are those of one ``Engine`` over
-    the whole batch.  With ``overlap`` False the micro-batches run one after
-    another on the caller's stream (each kernel alone on the GPU, for per-
-    kernel timing).  Every stream has the default priority."""
-
-    def __init__(self, cfg: workload.Config, device: str = "cuda", batch: Optional[int] = None,
-                 micro_batches: int = 2, weights: Optional[Sequence[Dict[str, np.ndarray]]] = None,
-                 **engine_kw):
-        B = cfg.batch if batch is None else batch
-        S = micro_batches
-        if not 1 <= S <= max(B, 1):
-            raise ValueError(f"micro_batches={S} must lie in [1, batch={B}]")
-        sizes = [B // S + (1 if i < B % S else 0) for i in range(S)]
-        self.cfg, self.B = cfg, B
-        self.engines: List[Engine] = []
-        first = 0
-        for n in sizes:
-            share = self.engines[0] if self.engines else None
-            self.engines.append(Engine(cfg, device, batch=n, weights=None if share else weights,
-                                       first_image=first, share_weights_with=share, **engine_kw))
-            first += n
-        self.device = self.engines[0].device
-        self.streams = [torch.cuda.Stream(device=self.device) for _ in range(S - 1)]
-        self.overlap = True
-
-    @property
-    def plans(self) -> List[StepPlan]:
-        return self.engines[0].plans
-
-    def set_schedule(self, full_every: int, policy: str, budget: int) -> None:
-        for e in self.engines:
-            e.set_schedule(full_every, policy, budget)
-
-    def configure(self, **kw) -> None:
-        for e in self.engines:
-            e.configure(**kw)
-
-    def step(self, t: int) -> None:
-        """Step t of every micro-batch; done on the caller's current stream
-        when this returns (everything enqueued after it waits for it)."""
-        first, rest = self.engines[0], self.engines[1:]
-        if not self.overlap or not rest:
-            for e in self.engines:
-                e.step(t)
-            return
-        cur = torch.cuda.current_stream(self.device)
-        fork = torch.cuda.Event()
-        fork.record(cur)
-        first.step(t)
-        for e, s in zip(rest, self.streams):
-            s.wait_event(fork)
-            with torch.cuda.stream(s):
-                e.step(t)
-            done = torch.cuda.Event()
-            done.record(s)
-            cur.wait_event(done)
-
-    def generate(self, steps: Optional[Sequence[int]] = None) -> None:
-        for t in (range(self.cfg.n_steps) if steps is None else steps):
-            self.step(t)
 
 
 # ------------------------------------------------------------------ a whole MAR step

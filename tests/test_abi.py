@@ -105,6 +105,30 @@ def test_step_argument_validation():
     assert _step(m, cache=mism) == binding.MARCHE_ERR_INVALID_ARG
 
 
+def _step_images(m, first, batch, cache=None, **kw):
+    args = dict(layer_begin=0, layer_end=m.n_layers, x=FAKE, a_idx=FAKE, a_off=FAKE, n_gen=FAKE,
+                a_total=10, a_max=5, gen_max=2, scores=None, score_layer=-1, workspace=FAKE,
+                workspace_bytes=0)
+    args.update(kw)
+    return binding.lib().marche_step_images(
+        C.byref(m), _layers(m.n_layers), C.byref(cache if cache is not None else _cache(m, 4)),
+        first, args["layer_begin"], args["layer_end"], batch, args["x"], args["a_idx"],
+        args["a_off"], args["n_gen"], args["a_total"], args["a_max"], args["gen_max"],
+        args["scores"], args["score_layer"], args["workspace"], args["workspace_bytes"], None)
+
+
+def test_step_images_range_validation():
+    m = _model()
+    # images [first, first + batch) must lie inside the cache's 4 images
+    for first, batch in ((-1, 2), (3, 2), (5, 0), (0, 5)):
+        assert _step_images(m, first, batch) == binding.MARCHE_ERR_INVALID_ARG, (first, batch)
+    assert "outside" in binding.last_error()
+    # a valid range reaches the workspace check (nothing is launched)
+    assert _step_images(m, 2, 2) == binding.MARCHE_ERR_WORKSPACE
+    assert _step_images(m, 4, 0, a_total=0, a_max=0, gen_max=0) == binding.MARCHE_OK
+    assert _step_images(m, 1, 2, layer_begin=1, layer_end=1) == binding.MARCHE_OK
+
+
 def test_workspace_validation_and_size():
     m = _model()
     need = binding.workspace_bytes(m, 2, 10)

@@ -1,9 +1,10 @@
-"""Micro-batched decoding: the batch split into micro-batches of consecutive
-images, each on its own HIP stream, against one engine over the whole batch.
+"""Cache-aware layers split into ranges of consecutive images, each range on
+its own HIP stream (marche_step_images), against the whole batch in one call.
 
 Images are independent and every kernel computes a row (or an image and head)
 the same way whatever else shares the launch, so the KV cache and the
-residual stream must match bit for bit over full and cache-aware steps."""
+residual stream must match bit for bit over full and cache-aware steps, with
+the ranges overlapping on the GPU or run one after another."""
 import pytest
 import torch
 
@@ -27,19 +28,21 @@ def whole():
 
 
 @pytest.mark.parametrize("parts,overlap", [(2, True), (3, True), (2, False)])
-def test_micro_batches_match_the_whole_batch(whole, parts, overlap):
+def test_image_ranges_match_the_whole_batch(whole, parts, overlap):
     cfg, ws, ref = whole
-    say(f"micro-batches: {cfg.name} B={ref.B} parts={parts} overlap={overlap}")
-    mb = driver.MicroBatchEngine(cfg, micro_batches=parts, weights=ws)
-    mb.overlap = overlap
-    assert sum(e.B for e in mb.engines) == ref.B
-    assert all(e.params is mb.engines[0].params for e in mb.engines)
+    say(f"image ranges: {cfg.name} B={ref.B} parts={parts} overlap={overlap}")
+    eng = driver.Engine(cfg, weights=ws, micro_batches=parts)
+    eng.overlap = overlap
+    assert sum(n for _, n in eng.ranges) == ref.B
     for t in STEPS:
-        mb.step(t)
+        eng.step(t)
+        if not eng.plans[t].full:
+            assert eng.plans[t].parts is not None and len(eng.plans[t].parts) == parts
     torch.cuda.synchronize()
-    for e in mb.engines:
-        sl = slice(e.first_image, e.first_image + e.B)
-        assert torch.equal(e.x, ref.x[sl]), f"x of images {sl}"
-        for l in range(cfg.n_layers):
-            assert torch.equal(e.k_layer(l), ref.k_layer(l)[sl]), f"K of layer {l}, images {sl}"
-            assert torch.equal(e.v_layer(l), ref.v_layer(l)[sl]), f"V of layer {l}, images {sl}"
+    assert torch.equal(eng.x, ref.x)
+    for l in range(cfg.n_layers):
+        assert torch.equal(eng.k_layer(l), ref.k_layer(l)), f"K of layer {l}"
+        assert torch.equal(eng.v_layer(l), ref.v_layer(l)), f"V of layer {l}"
+    for t in STEPS:
+        if not eng.plans[t].full:
+            assert torch.equal(eng.plans[t].ca_idx, ref.plans[t].ca_idx), f"active lists of step {t}"
