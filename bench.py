@@ -428,9 +428,8 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=3, help="workload id (2: MAR-B, 3: MAR-L, 4: MAR-H, 5: high-res)")
     ap.add_argument("--batch", type=int, default=None)
     ap.add_argument("--micro-batches", type=int, default=2,
-                    help="run the cache-aware layers of every cache-aware step as this many "
-                         "ranges of consecutive images, each on its own HIP stream (default 2; "
-                         "1: the whole batch in one call)")
+                    help="run every decoding step as this many ranges of consecutive images, "
+                         "each on its own HIP stream (default 2; 1: the whole batch in one call)")
     ap.add_argument("--ratio-bp", type=int, default=None, help="refresh ratio in basis points")
     ap.add_argument("--full-every", type=int, default=None)
     ap.add_argument("--no-full-recompute", action="store_true")

@@ -870,8 +870,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_small_kernel(const bf16 *A, con
 
 // Tile choice.  The 256x256 tile (one workgroup per CU) when its tiles fill
 // the compute units in whole waves well enough: at least 90% of the last
-// wave, or 80% when K >= 2048 (the longer main loop amortises the tile's
-// fixed start and write-back).  Otherwise the 128x256 tile, two workgroups
+// wave, or 60% when K >= 2048 (the longer main loop amortises the tile's
+// fixed start and write-back, and a partly filled last wave runs at a higher
+// clock under the chip's power limit, or beside another image range's
+// kernels).  Otherwise the 128x256 tile, two workgroups
 // per CU, whose write-backs overlap the other workgroup's main loop and whose
 // finer steps fill the chip better; and when even 128x256 tiles would occupy
 // fewer than half the compute units, the 64x128 tile (K a multiple of 128).  Measured at MAR-L
@@ -887,7 +889,7 @@ int gemm_tile_kind(DType dt, int32_t m, int32_t n, int32_t k) {
   const long tiles = (long)((m + 255) / 256) * (n / 256);
   const long waves = (tiles + cus - 1) / cus;
   const double fill = (double)tiles / (double)(waves * cus);
-  if (fill >= 0.9 || (fill >= 0.8 && k >= 2048)) return GEMM_TILE_256;
+  if (fill >= 0.9 || (fill >= 0.6 && k >= 2048)) return GEMM_TILE_256;
   if (k % small::kBK == 0 && (long)((m + 127) / 128) * (n / 256) * 2 < cus) return GEMM_TILE_64x128;
   return GEMM_TILE_128x256;
 }

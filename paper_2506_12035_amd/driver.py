@@ -9,9 +9,9 @@ One step t of a batch of images (Section 4.2-4.3, Algorithm 1):
   and the generating tokens first, writing the selection layer's per-head
   attention mass; select_refresh picks R per image into the tail of the
   cache-aware active list [G | N | R]; marche_step over layers
-  [sel_layer, L) on that list -- or, with micro_batches > 1, the selection
-  and those layers per range of consecutive images (marche_step_images),
-  each range on its own stream.
+  [sel_layer, L) on that list.  With micro_batches > 1 every step after
+  the decoder input runs per range of consecutive images
+  (marche_step_images), each range on its own stream.
 
 All index lists of every step are built on the host once, before decoding,
 and kept resident on the device; a step issues only kernel launches and
@@ -67,19 +67,20 @@ class StepPlan:
 
 @dataclass
 class RangePlan:
-    """The cache-aware lists of one range of consecutive images: views of the
-    step's lists with offsets rebased to the range's first image, and the
-    range's piece of the workspace."""
+    """The lists of one range of consecutive images: views of the step's
+    lists with offsets rebased to the range's first image (the cache-aware
+    ones only in cache-aware steps)."""
     first: int
     count: int
-    ca_idx: torch.Tensor
-    ca_off: torch.Tensor
-    ca_gen: torch.Tensor
-    excl_idx: torch.Tensor
-    excl_off: torch.Tensor
-    out_off: torch.Tensor
-    ws_offset: int
-    ws_bytes: int
+    full_idx: torch.Tensor
+    full_off: torch.Tensor
+    n_gen: torch.Tensor
+    ca_idx: Optional[torch.Tensor] = None
+    ca_off: Optional[torch.Tensor] = None
+    ca_gen: Optional[torch.Tensor] = None
+    excl_idx: Optional[torch.Tensor] = None
+    excl_off: Optional[torch.Tensor] = None
+    out_off: Optional[torch.Tensor] = None
 
 
 class Engine:
@@ -92,9 +93,9 @@ class Engine:
                  weights: Optional[Sequence[Dict[str, np.ndarray]]] = None,
                  strategy: str = "marche", first_image: int = 0, micro_batches: int = 1):
         """``batch`` images starting at image ``first_image`` of the workload's
-        batch.  ``micro_batches`` > 1 splits the cache-aware layers of every
-        cache-aware step into that many ranges of consecutive images, each
-        enqueued on a HIP stream of its own (see ``step``)."""
+        batch.  ``micro_batches`` > 1 runs every step (after the decoder input)
+        as that many ranges of consecutive images, each enqueued on a HIP
+        stream of its own (see ``step``)."""
         if n_layers is not None:
             cfg = cfg.with_(n_layers=n_layers)
         self.cfg = cfg
@@ -131,14 +132,22 @@ class Engine:
                                            stream=self.stream)
         self.x = torch.empty(self.B, N, D, dtype=torch.float32, device=self.device)
         self.scores = torch.empty(self.B, H, N, dtype=torch.float32, device=self.device)
-        self.ws_bytes = binding.workspace_bytes(self.model, self.B, self.B * N)
-        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
         S = micro_batches
         if not 1 <= S <= max(self.B, 1):
             raise ValueError(f"micro_batches={S} must lie in [1, batch={self.B}]")
         sizes = [self.B // S + (1 if i < self.B % S else 0) for i in range(S)]
         self.ranges = [(sum(sizes[:i]), sizes[i]) for i in range(S)]  # (first image, count)
         self.streams = [torch.cuda.Stream(device=self.device) for _ in range(S - 1)]
+        # one workspace region per range, sized for the range with every token
+        # active (a cache-aware step's range needs less and reuses it)
+        self.ws_regions = []
+        off = 0
+        for _, n in self.ranges:
+            nb = binding.workspace_bytes(self.model, n, n * N)
+            self.ws_regions.append((off, nb))
+            off += (nb + 255) // 256 * 256
+        self.ws_bytes = off
+        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
         self.overlap = True  # False: the ranges one after another on the current stream
 
         self.first_image = first_image
@@ -203,6 +212,8 @@ class Engine:
                         _dev_i32(np.arange(B + 1) * N, self.device),
                         _dev_i32(np.full(B, g), self.device))
         if si.full:
+            if len(self.ranges) > 1:
+                plan.parts = self._range_plans(plan, 0, 0)
             return plan
         st = self.strategy
         forced_cache = si.cache if st != "no-caching" else si.cache[:, :0]
@@ -232,20 +243,20 @@ class Engine:
         return plan
 
     def _range_plans(self, plan: StepPlan, n_excl: int, n_lead: int) -> List[RangePlan]:
-        B, a = self.B, plan.a
-        parts, off = [], 0
+        B, N, a = self.B, self.cfg.n_tokens, plan.a
+        parts = []
         for first, n in self.ranges:
             sl = slice(first, first + n)
-            ws = binding.workspace_bytes(self.model, n, n * a)
-            parts.append(RangePlan(
-                first, n, plan.ca_idx.view(B, a)[sl].reshape(-1),
-                _dev_i32(np.arange(n + 1) * a, self.device), plan.ca_gen[sl],
-                plan.excl_idx.view(B, n_excl)[sl].reshape(-1),
-                _dev_i32(np.arange(n + 1) * n_excl, self.device),
-                _dev_i32(np.arange(n) * a + n_lead, self.device), off, ws))
-            off += (ws + 255) // 256 * 256
-        if off > self.ws_bytes:
-            raise RuntimeError(f"image ranges need {off} workspace bytes > {self.ws_bytes}")
+            r = RangePlan(first, n, plan.full_idx.view(B, N)[sl].reshape(-1),
+                          _dev_i32(np.arange(n + 1) * N, self.device), plan.n_gen[sl])
+            if not plan.full:
+                r.ca_idx = plan.ca_idx.view(B, a)[sl].reshape(-1)
+                r.ca_off = _dev_i32(np.arange(n + 1) * a, self.device)
+                r.ca_gen = plan.ca_gen[sl]
+                r.excl_idx = plan.excl_idx.view(B, n_excl)[sl].reshape(-1)
+                r.excl_off = _dev_i32(np.arange(n + 1) * n_excl, self.device)
+                r.out_off = _dev_i32(np.arange(n) * a + n_lead, self.device)
+            parts.append(r)
         return parts
 
     # ------------------------------------------------------------------ step
@@ -272,59 +283,71 @@ class Engine:
 
     def step(self, t: int, build_input: bool = True) -> None:
         """One decoding step (all layers) of the whole batch, enqueued on the
-        current stream."""
+        current stream (with image ranges: forked from and joined back into
+        it)."""
         p = self.plans[t]
         c = self.cfg
         N, L, B = c.n_tokens, c.n_layers, self.B
         if build_input:
             self.decoder_input(t)
-        if p.full:
-            self.run_layers(0, L, p.full_idx, p.full_off, B * N, N, p.g, p.n_gen)
-            return
-        self.run_layers(0, self.sel, p.full_idx, p.full_off, B * N, N, p.g, p.n_gen,
-                        score_layer=self.sel - 1 if p.device_select else -1)
         if p.parts is None:
+            if p.full:
+                self.run_layers(0, L, p.full_idx, p.full_off, B * N, N, p.g, p.n_gen)
+                return
+            self.run_layers(0, self.sel, p.full_idx, p.full_off, B * N, N, p.g, p.n_gen,
+                            score_layer=self.sel - 1 if p.device_select else -1)
             self.select(p)
             if p.a > 0:
                 self.run_layers(self.sel, L, p.ca_idx, p.ca_off, B * p.a, p.a, p.ca_gen_max,
                                 p.ca_gen)
             return
-        # The selection and the cache-aware layers per image range, each range
-        # on its own stream between a fork from and a join back into the
-        # current one: ranges share no rows, so their kernels overlap on the
-        # GPU (one range's attention beside another's GEMMs, one's partly
-        # filled last wave of tiles beside another's first).
+        # Image ranges: each range runs the whole step (every layer, the
+        # selection) on its own stream between a fork from and a join back
+        # into the current one, with its own workspace region.  Ranges share
+        # no rows, so their kernels overlap on the GPU: one range's attention,
+        # LayerNorm or partly filled last wave of tiles beside another's GEMMs.
         if not self.overlap:
-            for part in p.parts:
-                self._cache_aware_range(p, part)
+            for i, r in enumerate(p.parts):
+                self._range_step(p, r, i)
             return
         cur = self.stream
         fork = torch.cuda.Event()
         fork.record(cur)
-        for i, part in enumerate(p.parts):
+        for i, r in enumerate(p.parts):
             s = cur if i == 0 else self.streams[i - 1]
             if i > 0:
                 s.wait_event(fork)
             with torch.cuda.stream(s):
-                self._cache_aware_range(p, part)
+                self._range_step(p, r, i)
             if i > 0:
                 done = torch.cuda.Event()
                 done.record(s)
                 cur.wait_event(done)
 
-    def _cache_aware_range(self, p: StepPlan, r: RangePlan) -> None:
+    def _range_step(self, p: StepPlan, r: RangePlan, i: int) -> None:
         c = self.cfg
-        sl = slice(r.first, r.first + r.count)
+        N, L, n = c.n_tokens, c.n_layers, r.count
+        sl = slice(r.first, r.first + n)
+        off, nb = self.ws_regions[i]
+        ws = self.workspace[off:off + nb]
+
+        def layers(begin, end, idx, a_off, gen, rows, a_max, gen_max, scores=None, score_layer=-1):
+            binding.marche_step_images(self.model, self.layers, self.cache, r.first, begin, end, n,
+                                       self.x[sl], idx, a_off, gen, rows, a_max, gen_max, scores,
+                                       score_layer, ws, nb, stream=self.stream)
+
+        if p.full:
+            layers(0, L, r.full_idx, r.full_off, r.n_gen, n * N, N, p.g)
+            return
+        sel_scores = p.device_select
+        layers(0, self.sel, r.full_idx, r.full_off, r.n_gen, n * N, N, p.g,
+               self.scores[sl] if sel_scores else None, self.sel - 1 if sel_scores else -1)
         if p.device_select:
-            binding.select_refresh(self.scores[sl], c.n_heads, r.excl_idx, r.excl_off, r.count,
-                                   c.n_tokens, p.k, r.ca_idx, r.out_off, stream=self.stream,
+            binding.select_refresh(self.scores[sl], c.n_heads, r.excl_idx, r.excl_off, n, N, p.k,
+                                   r.ca_idx, r.out_off, stream=self.stream,
                                    lowest=p.select_lowest)
         if p.a > 0:
-            ws = self.workspace[r.ws_offset:r.ws_offset + r.ws_bytes]
-            binding.marche_step_images(self.model, self.layers, self.cache, r.first, self.sel,
-                                       c.n_layers, r.count, self.x[sl], r.ca_idx, r.ca_off,
-                                       r.ca_gen, r.count * p.a, p.a, p.ca_gen_max, None, -1, ws,
-                                       r.ws_bytes, stream=self.stream)
+            layers(self.sel, L, r.ca_idx, r.ca_off, r.ca_gen, n * p.a, p.a, p.ca_gen_max)
 
     def generate(self, steps: Optional[Sequence[int]] = None) -> None:
         for t in (range(self.cfg.n_steps) if steps is None else steps):
