@@ -405,9 +405,12 @@ def ingest_main(args) -> int:
                           {"copy_bytes": 1024 * (1 << 20)})
     with open(bjson) as f:
         lines = [ln for ln in f.read().splitlines() if ln.startswith("{")]
-    launches = {k: v["launches"] for k, v in json.loads(lines[-1]).get("kernels", {}).items()}
+    line = json.loads(lines[-1])
+    launches = {k: v["launches"] for k, v in line.get("kernels", {}).items()}
+    # with S image ranges every layer pass launches each kernel once per range
+    ranges = line.get("config", {}).get("micro_batches", 1)
     for c, e in rec["classes"].items():
-        e["full_layer_only"] = launches.get(c) == passes
+        e["full_layer_only"] = launches.get(c) == passes * ranges
     path = os.path.join(ROOT, "profiles", "traffic.json")
     allrec = {}
     if os.path.exists(path):
