@@ -328,7 +328,7 @@ def e2e_main(args) -> int:
 
     mc = workload.MAR_CONFIGS[args.e2e_config]
     log(f"[e2e] {mc.name}: building the engine")
-    eng = driver.MarEngine(mc)
+    eng = driver.MarEngine(mc, micro_batches=args.micro_batches)
     B, T = eng.B, mc.dec.n_steps
 
     def generation():
@@ -383,7 +383,8 @@ def e2e_main(args) -> int:
                    "d_model": mc.dec.d_model, "head_blocks": mc.head_blocks,
                    "head_width": mc.head_width, "token_channels": mc.c_tok,
                    "sampling_steps": mc.sample_steps, "refresh_ratio": mc.dec.ratio_bp / 10000,
-                   "full_every": mc.dec.full_every, "sel_layer": mc.dec.sel_layer},
+                   "full_every": mc.dec.full_every, "sel_layer": mc.dec.sel_layer,
+                   "micro_batches": args.micro_batches},
         "phase_ms_per_generation": split,
         "full_recompute": {"s_per_image": fwall / B, "phase_ms_per_generation": fsplit},
         "speedup_vs_full_recompute": fwall / wall,

@@ -418,7 +418,13 @@ class MarEngine:
         self.enc_v = torch.empty(n_el, dtype=self.tdtype, device=self.device)
         self.x_enc = torch.empty(B, N, D, dtype=torch.float32, device=self.device)
         big = self._enc_model(N)
-        self.enc_ws_bytes = binding.workspace_bytes(big, B, B * N)
+        # one workspace region per image range of the decoder engine
+        self.enc_regions, off = [], 0
+        for _, n in d.ranges:
+            nb = binding.workspace_bytes(big, n, n * N)
+            self.enc_regions.append((off, nb))
+            off += (nb + 255) // 256 * 256
+        self.enc_ws_bytes = off
         self.enc_ws = torch.empty(self.enc_ws_bytes, dtype=torch.uint8, device=self.device)
         self.e2d_ws_bytes = max(256, binding.encoder_to_decoder_workspace_bytes(B, c.n_buf, c.n_img,
                                                                                 D, self.dt))
@@ -496,9 +502,25 @@ class MarEngine:
         ec = self.mc.enc
         cache = binding.KVCache(self.enc_k.data_ptr(), self.enc_v.data_ptr(), ec.n_layers, self.B,
                                 ec.n_heads, n_enc, ec.head_dim, self.dt)
-        binding.marche_step(model, self.enc_layers, cache, 0, ec.n_layers, self.B, self.x_enc, idx,
-                            off, None, self.B * n_enc, n_enc, 0, None, -1, self.enc_ws,
-                            self.enc_ws_bytes, stream=self.stream)
+        # every image has the same encoder rows, so a range of n images takes
+        # the first n lists; each range on its own stream, like the decoder's
+        cur = self.stream
+        fork = torch.cuda.Event()
+        if len(d.ranges) > 1:
+            fork.record(cur)
+        for i, (first, n) in enumerate(d.ranges):
+            s = cur if i == 0 else d.streams[i - 1]
+            if i > 0:
+                s.wait_event(fork)
+            wo, wb = self.enc_regions[i]
+            binding.marche_step_images(
+                model, self.enc_layers, cache, first, 0, ec.n_layers, n,
+                self.x_enc.view(-1)[first * n_enc * c.d_model:], idx[:n * n_enc], off[:n + 1],
+                None, n * n_enc, n_enc, 0, None, -1, self.enc_ws[wo:wo + wb], wb, stream=s)
+            if i > 0:
+                done = torch.cuda.Event()
+                done.record(s)
+                cur.wait_event(done)
         binding.encoder_to_decoder(d.x, self.x_enc, e["enc_ln_g"], e["enc_ln_b"], c.ln_eps,
                                    e["w_de"], e["b_de"], e["mask"], e["pe_dec"], self.known[t],
                                    d.rank, self.B, c.n_buf, c.n_img, n_known, c.d_model, self.dt,

@@ -264,6 +264,24 @@ def test_whole_generation_default_schedule():
     assert (np.abs(tok).sum(axis=2) > 0).all()
 
 
+def test_whole_generation_image_ranges_match_one_call():
+    """Encoder and decoder as two image ranges on two streams (2 + 1 images of
+    the tiny model's 3): every image is computed exactly as in one call, so
+    the whole generation's token values match bit for bit."""
+    import torch
+    from paper_2506_12035_amd import driver
+
+    mc = workload.MAR_CONFIGS["tiny"]
+    ref = driver.MarEngine(mc)
+    ref.generate()
+    eng = driver.MarEngine(mc, micro_batches=2)
+    assert [n for _, n in eng.dec.ranges] == [2, 1]
+    eng.generate()
+    torch.cuda.synchronize()
+    assert torch.equal(eng.tok, ref.tok)
+    assert torch.equal(eng.dec.x, ref.dec.x)
+
+
 def test_sampler_full_size_sampled_rows():
     """The sampler at the MAR-L head (width 1280, 8 blocks, 100 DDPM steps) on
     512 rows (batch 128 x 4 generating tokens), as the whole-generation bench
