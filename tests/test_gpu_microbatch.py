@@ -46,3 +46,55 @@ def test_image_ranges_match_the_whole_batch(whole, parts, overlap):
     for t in STEPS:
         if not eng.plans[t].full:
             assert torch.equal(eng.plans[t].ca_idx, ref.plans[t].ca_idx), f"active lists of step {t}"
+
+
+def test_step_images_touches_only_its_range():
+    """marche_step_images on images [2, 4) of a 4-image cache and residual
+    stream: images 0 and 1 keep every bit of x and of both caches, and images
+    2 and 3 equal what marche_step over all four images computes for them."""
+    import numpy as np
+    from paper_2506_12035_amd import binding
+
+    cfg = workload.CONFIGS[2].with_(n_layers=2, batch=4)
+    B, N, D, H, dh, L = 4, cfg.n_tokens, cfg.d_model, cfg.n_heads, cfg.head_dim, 2
+    say(f"marche_step_images: {cfg.name} reduced to L={L}, B={B}, images [2, 4)")
+    rng = np.random.default_rng(5)
+    model = binding.make_model(L, D, H, dh, cfg.d_mlp, N, binding.MARCHE_BF16, cfg.ln_eps)
+    params = []
+    for l in range(L):
+        w = workload.layer_weights(cfg, l)
+        params.append({k: torch.from_numpy(np.ascontiguousarray(v, np.float32)).to(
+            torch.bfloat16 if k.startswith("w_") else torch.float32).cuda() for k, v in w.items()})
+    layers = binding.make_layers(params)
+    x0 = torch.from_numpy(rng.standard_normal((B, N, D)).astype(np.float32)).cuda()
+    n_el = L * B * H * N * dh
+    k0 = torch.from_numpy(rng.standard_normal(n_el).astype(np.float32)).to(torch.bfloat16).cuda()
+    v0 = torch.from_numpy(rng.standard_normal(n_el).astype(np.float32)).to(torch.bfloat16).cuda()
+    act = [np.sort(rng.choice(N, size=a, replace=False)).astype(np.int32) for a in (40, 37, 44, 29)]
+    n_gen = [5, 4, 6, 3]
+
+    def run(first, count):
+        x = x0.clone()
+        k, v = k0.clone(), v0.clone()
+        cache = binding.kv_cache_init(model, B, k, v, n_el * 2, k_init=k0, v_init=v0)
+        lists = act[first:first + count]
+        idx = torch.from_numpy(np.concatenate(lists)).cuda()
+        off = torch.from_numpy(np.concatenate([[0], np.cumsum([len(a) for a in lists])]).astype(np.int32)).cuda()
+        gen = torch.tensor(n_gen[first:first + count], dtype=torch.int32).cuda()
+        total, a_max = int(off[-1]), max(len(a) for a in lists)
+        wsb = binding.workspace_bytes(model, count, total)
+        ws = torch.empty(wsb, dtype=torch.uint8).cuda()
+        binding.marche_step_images(model, layers, cache, first, 0, L, count, x[first:first + count],
+                                   idx, off, gen, total, a_max, max(n_gen[first:first + count]),
+                                   None, -1, ws, wsb)
+        torch.cuda.synchronize()
+        return x, k.view(L, B, H, N, dh), v.view(L, B, H, N, dh)
+
+    x_all, k_all, v_all = run(0, 4)
+    x_part, k_part, v_part = run(2, 2)
+    k_in, v_in = k0.view(L, B, H, N, dh), v0.view(L, B, H, N, dh)
+    assert torch.equal(x_part[:2], x0[:2])
+    assert torch.equal(k_part[:, :2], k_in[:, :2]) and torch.equal(v_part[:, :2], v_in[:, :2])
+    assert torch.equal(x_part[2:], x_all[2:])
+    assert torch.equal(k_part[:, 2:], k_all[:, 2:]) and torch.equal(v_part[:, 2:], v_all[:, 2:])
+    assert not torch.equal(x_part[2:], x0[2:])  # the range was really computed
