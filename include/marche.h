@@ -135,7 +135,17 @@ size_t marche_step_workspace_bytes(const marche_model_t *m, int32_t batch, int32
  *
  * `layers` is a host array of n_layers entries; `workspace` holds at least
  * marche_step_workspace_bytes(m, batch, a_total) bytes of device memory and
- * must not be used by another call in flight. */
+ * must not be used by another call in flight.
+ *
+ * The device lists are preconditions the host cannot see.  With the
+ * environment variable MARCHE_VALIDATE set (to anything but "0"), the call
+ * first checks them with a kernel and waits for the result on the host:
+ * a_off[0] = 0, a_off[batch] = a_total, non-decreasing, no list longer than
+ * a_max; every token in [0, n_tokens) and none twice for one image; n_gen[b]
+ * within [0, |A_b|] and at most gen_max.  A violation returns INVALID_ARG,
+ * naming one problem found and its image (the first recorded, when several
+ * images are bad), before anything else is launched.  Without it nothing is checked on the device and the call never
+ * synchronises. */
 marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layers,
                             const marche_kv_cache_t *cache, int32_t layer_begin,
                             int32_t layer_end, int32_t batch, float *x, const int32_t *a_idx,

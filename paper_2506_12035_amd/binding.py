@@ -161,11 +161,17 @@ def make_model(n_layers, d_model, n_heads, head_dim, d_mlp, n_tokens, dtype, ln_
 
 
 def make_layers(params: Sequence[dict]):
-    """ctypes array of Layer from dicts of device tensors / addresses."""
+    """ctypes array of Layer from dicts of device tensors / addresses.
+
+    The array holds raw device addresses, so it keeps the dicts (and with them
+    the tensors) alive for as long as it lives: a caller that drops its own
+    references cannot have the weights freed and their memory reused under a
+    later step."""
     arr = (Layer * len(params))()
     for i, p in enumerate(params):
         for name, _ in Layer._fields_:
             setattr(arr[i], name, _ptr(p[name]))
+    arr._owners = [dict(p) for p in params]
     return arr
 
 
@@ -174,6 +180,7 @@ def kv_cache_init(model: Model, batch: int, k_buf, v_buf, bytes_each: int, k_ini
     cache = KVCache()
     _check(lib().kv_cache_init(C.byref(cache), C.byref(model), batch, _ptr(k_buf), _ptr(v_buf),
                                bytes_each, _ptr(k_init), _ptr(v_init), _stream(stream)))
+    cache._owners = (k_buf, v_buf)  # the handle points into these buffers: keep them alive
     return cache
 
 

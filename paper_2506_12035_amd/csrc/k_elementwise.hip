@@ -25,6 +25,61 @@ hipError_t launch_row_map(RowMap *map, const int32_t *a_idx, const int32_t *a_of
   return hipGetLastError();
 }
 
+// Validation of the device-resident active lists (debug mode of the step):
+// one workgroup per image.  report[0] receives the first failure as
+// 1 + code * batch + image (0 = none); codes: 0 offsets (a_off[0] != 0,
+// a_off[batch] != a_total, decreasing, or a list longer than a_max),
+// 1 token outside [0, n_tokens), 2 a token listed twice for one image,
+// 3 n_gen[b] outside [0, |A_b|] or above gen_max.  Every read stays inside
+// a_off[0 .. batch] and a_idx[0 .. a_total), whatever the lists hold.
+constexpr int kMaxTokens = 4096;  // the model check bounds n_tokens
+
+__global__ void clear_word_kernel(int32_t *p) {
+  if (threadIdx.x == 0) *p = 0;
+}
+
+__global__ __launch_bounds__(256) void check_active_kernel(
+    const int32_t *a_idx, const int32_t *a_off, const int32_t *n_gen, int32_t batch,
+    int32_t n_tokens, int32_t a_total, int32_t a_max, int32_t gen_max, int32_t *report) {
+  __shared__ unsigned seen[kMaxTokens / 32];
+  __shared__ int bad;
+  const int b = blockIdx.x;
+  auto fail = [&](int code) { atomicCAS(report, 0, 1 + code * batch + b); };
+  for (int i = threadIdx.x; i < (n_tokens + 31) / 32; i += blockDim.x) seen[i] = 0u;
+  if (threadIdx.x == 0) bad = 0;
+  __syncthreads();
+  const int lo = a_off[b], hi = a_off[b + 1];
+  if (threadIdx.x == 0) {
+    const bool first_ok = b > 0 || lo == 0;
+    const bool last_ok = b + 1 < batch || hi == a_total;
+    if (!first_ok || !last_ok || lo < 0 || hi < lo || hi > a_total || hi - lo > a_max) {
+      fail(0);
+      bad = 1;
+    } else if (n_gen && (n_gen[b] < 0 || n_gen[b] > hi - lo || n_gen[b] > gen_max)) {
+      fail(3);
+    }
+  }
+  __syncthreads();
+  if (bad) return;  // the list bounds are not trusted: read no index
+  for (int r = lo + threadIdx.x; r < hi; r += blockDim.x) {
+    const int tok = a_idx[r];
+    if (tok < 0 || tok >= n_tokens) {
+      fail(1);
+      continue;
+    }
+    if (atomicOr(&seen[tok >> 5], 1u << (tok & 31)) & (1u << (tok & 31))) fail(2);
+  }
+}
+
+hipError_t launch_check_active(const int32_t *a_idx, const int32_t *a_off, const int32_t *n_gen,
+                               int32_t batch, int32_t n_tokens, int32_t a_total, int32_t a_max,
+                               int32_t gen_max, int32_t *report, hipStream_t s) {
+  clear_word_kernel<<<1, 64, 0, s>>>(report);
+  check_active_kernel<<<batch, 256, 0, s>>>(a_idx, a_off, n_gen, batch, n_tokens, a_total, a_max,
+                                            gen_max, report);
+  return hipGetLastError();
+}
+
 // u[r] = LN(x[map[r].x_row]) * g + b, one wavefront per active row.
 // Each lane holds NV float4 chunks of the row (d_model = NV * 256).
 // Statistics in float32: mean, then the population variance of the centred

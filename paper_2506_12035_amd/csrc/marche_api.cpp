@@ -13,6 +13,8 @@
 #include <string>
 #include <vector>
 
+#include <cstdlib>
+
 #include "../../include/marche.h"
 #include "marche_internal.h"
 
@@ -37,6 +39,13 @@ int marche::device_cu_count() {
 namespace {
 
 thread_local std::string t_err;
+
+// Debug mode: MARCHE_VALIDATE set to anything but "" or "0" makes every step
+// check its device-resident active lists before launching (read per call).
+bool validate_requested() {
+  const char *v = std::getenv("MARCHE_VALIDATE");
+  return v && v[0] && !(v[0] == '0' && v[1] == 0);
+}
 
 marche_status_t fail(marche_status_t s, const char *fmt, ...) {
   char buf[512];
@@ -312,6 +321,24 @@ static marche_status_t step_impl(const marche_model_t *m, const marche_layer_t *
     return fail(MARCHE_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
 
   hipStream_t stream = static_cast<hipStream_t>(stream_);
+  if (validate_requested()) {
+    // the first word of the workspace (the row map's, rewritten below)
+    int32_t *report = static_cast<int32_t *>(workspace);
+    hipError_t e = launch_check_active(a_idx, a_off, n_gen, batch, m->n_tokens, a_total, a_max,
+                                       gen_max, report, stream);
+    int32_t h = 0;
+    if (e == hipSuccess) e = hipMemcpyAsync(&h, report, sizeof h, hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return fail_hip(e, "active-list validation");
+    if (h != 0) {
+      static const char *what[] = {"a_off inconsistent with a_total / a_max",
+                                   "token outside [0, n_tokens)", "token listed twice",
+                                   "n_gen outside [0, |A_b|] or above gen_max"};
+      const int code = (h - 1) / batch, image = (h - 1) % batch;
+      return fail(MARCHE_ERR_INVALID_ARG, "active lists: %s (image %d of the call)",
+                  what[code & 3], image);
+    }
+  }
   const DType dt = m->dtype == MARCHE_BF16 ? DType::BF16 : DType::F32;
   const size_t es = elem_size(m->dtype);
   const int D = m->d_model, F = m->d_mlp, H = m->n_heads, dh = m->head_dim, N = m->n_tokens;

@@ -36,6 +36,11 @@ hipError_t launch_decoder_input(float *x, const float *cls, const float *value, 
                                 int32_t n_tokens, int32_t n_buf, int32_t d_model, int32_t n_known,
                                 hipStream_t s);
 hipError_t launch_fill_zero(void *dst, size_t bytes, hipStream_t s);
+// Debug-mode check of a step's active lists; report[0] = 0 or 1 + code*batch + image
+// (codes: 0 offsets, 1 token range, 2 duplicate token, 3 n_gen).
+hipError_t launch_check_active(const int32_t *a_idx, const int32_t *a_off, const int32_t *n_gen,
+                               int32_t batch, int32_t n_tokens, int32_t a_total, int32_t a_max,
+                               int32_t gen_max, int32_t *report, hipStream_t s);
 
 // ---- the rest of a MAR step (k_mar.hip) ----
 // Encoder input rows [batch][n_buf + n_known][d_model] (Eq. 1).

@@ -278,3 +278,26 @@ def test_diffusion_sample_validation_and_workspace():
     assert call(ws=None) == binding.MARCHE_ERR_WORKSPACE
     assert call(ws_bytes=need - 1) == binding.MARCHE_ERR_WORKSPACE
     assert call(ws=FAKE + 64) == binding.MARCHE_ERR_INVALID_ARG
+
+
+def test_layer_array_keeps_its_tensors_alive():
+    """make_layers stores raw addresses; the array it returns holds the tensors,
+    so dropping the caller's own references frees nothing (a freed weight's
+    memory would be handed to the next allocation and read as weights)."""
+    import gc
+    import weakref
+
+    import torch
+
+    names = [n for n, _ in binding.Layer._fields_]
+    params = [{n: torch.ones(4) for n in names} for _ in range(2)]
+    probes = [weakref.ref(p[n]) for p in params for n in names]
+    addrs = [p["w_qkv"].data_ptr() for p in params]
+    arr = binding.make_layers(params)
+    del params
+    gc.collect()
+    assert all(r() is not None for r in probes)
+    assert [arr[i].w_qkv for i in range(2)] == addrs
+    del arr
+    gc.collect()
+    assert all(r() is None for r in probes)
