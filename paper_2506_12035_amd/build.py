@@ -35,10 +35,18 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libmarche.so)")
 
 
+# Per-source device flags.  The attention kernels hold only a few dozen
+# accumulators per lane, and MFMA results in the AGPR file would cost a copy
+# to and from the VGPRs for every softmax step on them, so their MFMAs take
+# and produce VGPRs.  The GEMM tiles keep the compiler's choice (256
+# accumulators per lane live in the AGPRs).
+EXTRA = {"k_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
     lang = [] if src.endswith(".cpp") else ["-x", "hip"]
-    cmd = [hipcc(), *COMMON, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc(), *COMMON, *EXTRA.get(src, []), *lang, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

@@ -37,11 +37,6 @@ __device__ __forceinline__ int vperm16(int k) {
   return (k & 3) | (((k >> 3) & 1) << 2) | (((k >> 2) & 1) << 3);
 }
 
-// One 64-key tile of the online softmax for one wavefront's 32 queries.
-// ks: the tile's K rows in LDS (row stride DH + 8); vt: its transposed V
-// (row stride TK + 8, keys of each 16-key group permuted by vperm16); t0: the
-// tile's first key within a segment of ns keys.  Updates the running maximum,
-// sum and the O^T accumulators (log2 domain; sl2 = log2(e) / sqrt(d_h)).
 // Element offsets inside one tile's K and V^T blocks.  Padded layout: rows of
 // DH + 8 (K) and TK + 8 (V^T) elements.  Swizzled layout (DH = 64 only): rows
 // of 64 elements whose 16-byte chunks are permuted by an XOR with the row
@@ -58,7 +53,16 @@ __device__ __forceinline__ int vt_off(int row, int pos) {
   else return row * (TK + 8) + pos;
 }
 
-template <int DH, bool SWZ = false>
+// One 64-key tile of the online softmax for one wavefront's 32 queries.
+// ks: the tile's K rows in LDS; vt: its transposed V (keys of each 16-key
+// group permuted by vperm16); t0: the tile's first key within a segment of
+// ns keys, MASK set when the tile runs past the segment's end.  Updates the
+// running maximum, sum and the O^T accumulators in the log2 domain (sl2 =
+// log2(e) / sqrt(d_h) > 0).  The maximum is taken over the raw logits: as
+// rounding a product by a positive constant is monotone, fl(max * sl2) is
+// the maximum of the scaled logits exactly, and the scale then folds into
+// the exponent's argument as one FMA per logit.
+template <int DH, bool SWZ = false, bool MASK = false>
 __device__ __forceinline__ void attn_tile(const bf16 *ks, const bf16 *vt, const bf16x8 (&qf)[DH / 16],
                                           f32x16 (&acc)[(DH + 31) / 32], float &m_run, float &l_run,
                                           int t0, int ns, float sl2, int lane) {
@@ -78,34 +82,25 @@ __device__ __forceinline__ void attn_tile(const bf16 *ks, const bf16 *vt, const 
     }
   }
   float mx = -INFINITY;
-  if (t0 + TK <= ns) {  // every key of the tile exists
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+  for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[kb][r] *= sl2;
-        mx = fmaxf(mx, s[kb][r]);
-      }
-  } else {
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
+    for (int r = 0; r < 16; ++r) {
+      if constexpr (MASK) {
         const int key = t0 + kb * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        const float v = key < ns ? s[kb][r] * sl2 : -INFINITY;
-        s[kb][r] = v;
-        mx = fmaxf(mx, v);
+        if (key >= ns) s[kb][r] = -INFINITY;
       }
-  }
+      mx = fmaxf(mx, s[kb][r]);
+    }
   mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-  const float m_new = fmaxf(m_run, mx);
+  const float m_new = fmaxf(m_run, mx * sl2);
   const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
   float psum = 0.f;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const float p = __builtin_amdgcn_exp2f(s[kb][r] - m_new);
+      const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], sl2, -m_new));
       s[kb][r] = p;
       psum += p;
     }
@@ -131,7 +126,9 @@ __device__ __forceinline__ void attn_tile(const bf16 *ks, const bf16 *vt, const 
     }
 }
 
-template <int DH, int NW, bool SEG2 = false>
+// ALIGNED: every segment's length is a multiple of TK, so no key tile runs
+// past its segment and only the unmasked tile step is compiled.
+template <int DH, int NW, bool SEG2, bool ALIGNED>
 __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chunks) {
   constexpr int NT = NW * 64;
   constexpr int KS = DH + 8;        // K tile row stride (elements)
@@ -263,7 +260,10 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
     }
     const bool more = t + 1 < ntiles;
     if (more) gload(t + 1);
-    attn_tile<DH>(Ks[cur], Vt[cur], qf, acc, m_run, l_run, t0, ns, sl2, lane);
+    if (ALIGNED || t0 + TK <= ns)
+      attn_tile<DH>(Ks[cur], Vt[cur], qf, acc, m_run, l_run, t0, ns, sl2, lane);
+    else
+      attn_tile<DH, false, true>(Ks[cur], Vt[cur], qf, acc, m_run, l_run, t0, ns, sl2, lane);
     if (more) sstore(cur ^ 1);
     __syncthreads();
   }
@@ -408,8 +408,11 @@ __global__ __launch_bounds__(NW * 64) void attn_resident_kernel(AttnArgs a) {
     f32x16 acc[ODB];
 #pragma unroll
     for (int d = 0; d < ODB; ++d) acc[d] = f32x16{};
-    for (int t = 0; t < ntiles; ++t)
+    for (int t = 0; t < N / TK; ++t)
       attn_tile<DH, SWZ>(Ks[t], Vt[t], qf, acc, m_run, l_run, t * TK, N, sl2, lane);
+    if (N % TK)
+      attn_tile<DH, SWZ, true>(Ks[N / TK], Vt[N / TK], qf, acc, m_run, l_run, (N / TK) * TK, N,
+                               sl2, lane);
 
     const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
     const float inv = 1.0f / l_tot;
@@ -444,7 +447,11 @@ template <int DH, int NW, bool SEG2>
 static hipError_t run_attn_mfma(const AttnArgs &a, hipStream_t s) {
   const int chunks = (a.a_max + NW * 32 - 1) / (NW * 32);
   const int grid = a.batch * a.n_heads * chunks;
-  attn_mfma_kernel<DH, NW, SEG2><<<grid, NW * 64, 0, s>>>(a, chunks);
+  const bool aligned = a.n_tokens % TK == 0 && (!SEG2 || a.n2 % TK == 0);
+  if (aligned)
+    attn_mfma_kernel<DH, NW, SEG2, true><<<grid, NW * 64, 0, s>>>(a, chunks);
+  else
+    attn_mfma_kernel<DH, NW, SEG2, false><<<grid, NW * 64, 0, s>>>(a, chunks);
   return hipGetLastError();
 }
 
