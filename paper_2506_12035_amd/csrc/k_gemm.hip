@@ -61,31 +61,38 @@ struct EpiQkv {
   const float *bias;
   const RowMap *map;
   int d_model, head_dim, n_heads, n_tokens;
-  using Row = RowMap;
   // 32-bit element offsets: the host limits every buffer to < 2^31 elements.
+  // A row's offset in q and in a K/V cache layer, computed once per row when
+  // the tile stages its row records, so the stores add instead of multiply.
+  struct Row {
+    uint32_t q_off;   // r * d_model
+    uint32_t kv_off;  // (b * n_heads * n_tokens + tok) * head_dim
+  };
   struct Col {
     T *base;       // q, or the K or V cache of the layer
     uint32_t off;  // column offset: c0 for q, h*n_tokens*head_dim + d for K/V
     bool is_q;
   };
-  __device__ __forceinline__ Row row(int r) const { return map[r]; }
+  __device__ __forceinline__ Row row(int r) const {
+    const RowMap m = map[r];
+    return Row{(uint32_t)(r * d_model), (uint32_t)((m.b * n_heads * n_tokens + m.tok) * head_dim)};
+  }
+  // Which of q, K and V a column belongs to is decided once per wavefront:
+  // every tile gives a wavefront a span of 64 or 128 columns aligned to its
+  // width, and d_model is a multiple of 256, so no span crosses from one of
+  // the three into the next.  The choice is then uniform (scalar) and the
+  // stores take no divergent branches.
   __device__ __forceinline__ Col col(int c0) const {
-    if (c0 < d_model) return Col{q, (uint32_t)c0, true};
-    int c = c0 - d_model;
-    T *dst = kc;
-    if (c >= d_model) {
-      c -= d_model;
-      dst = vc;
-    }
+    const int which = __builtin_amdgcn_readfirstlane(c0 < d_model ? 0 : c0 < 2 * d_model ? 1 : 2);
+    if (which == 0) return Col{q, (uint32_t)c0, true};
+    const int c = c0 - which * d_model;
     const int h = c / head_dim, d = c - h * head_dim;
-    return Col{dst, (uint32_t)(h * n_tokens * head_dim + d), false};
+    return Col{which == 1 ? kc : vc, (uint32_t)(h * n_tokens * head_dim + d), false};
   }
   __device__ __forceinline__ f32x4 bias4(int c0) const { return load_bias4(bias, c0); }
   __device__ __forceinline__ f32x4 prior(const Row &, const Col &) const { return f32x4{}; }
-  __device__ __forceinline__ void store(const Row &m, int r, const Col &c, f32x4 v) const {
-    const uint32_t row_off = c.is_q ? (uint32_t)(r * d_model)
-                                    : (uint32_t)((m.b * n_heads * n_tokens + m.tok) * head_dim);
-    store4(c.base + row_off + c.off, v);
+  __device__ __forceinline__ void store(const Row &m, int, const Col &c, f32x4 v) const {
+    store4(c.base + (c.is_q ? m.q_off : m.kv_off) + c.off, v);
   }
 };
 
