@@ -876,27 +876,27 @@ __global__ __launch_bounds__(256) void gemm_bf16_small_kernel(const bf16 *A, con
 }
 
 // Tile choice.  The 256x256 tile (one workgroup per CU) when its tiles fill
-// the compute units in whole waves well enough: at least 90% of the last
-// wave, or 60% when K >= 2048 (the longer main loop amortises the tile's
-// fixed start and write-back, and a partly filled last wave runs at a higher
-// clock under the chip's power limit, or beside another image range's
-// kernels).  Otherwise the 128x256 tile, two workgroups
-// per CU, whose write-backs overlap the other workgroup's main loop and whose
-// finer steps fill the chip better; and when even 128x256 tiles would occupy
-// fewer than half the compute units, the 64x128 tile (K a multiple of 128).  Measured at MAR-L
-// sizes: full-step QKV, fc1 and fc2 and cache-aware QKV take the 256x256
-// tile, the output projection and the other cache-aware GEMMs the 128x256
-// one, the sampler's per-block GEMMs (a few hundred rows) the 64x128 one.
-// Under sustained load the 128x256 tile runs at a lower clock (more operand
-// traffic per flop), which is why it does not replace the large tile
-// outright.
+// at least 60% of their last wave over the compute units: a partly filled
+// last wave runs at a higher clock under the chip's power limit, and beside
+// another image range's kernels when the step runs as ranges on streams.
+// Otherwise the 128x256 tile, two workgroups per CU, whose write-backs
+// overlap the other workgroup's main loop and whose finer steps fill the chip
+// better; and when even 128x256 tiles would occupy fewer than half the
+// compute units, the 64x128 tile (K a multiple of 128).  Measured at MAR-L
+// sizes, per 64-image range: every full-layer GEMM takes the 256x256 tile
+// (the output projection alone runs slower on it, 80 vs 75 us, but the
+// overlapped step is faster), the cache-aware QKV and fc1 the 128x256 tile,
+// the cache-aware output projection and fc2 the 64x128 one, as do the
+// sampler's per-block GEMMs (a few hundred rows).  Under sustained load the 128x256 tile runs
+// at a lower clock (more operand traffic per flop), which is why it does not
+// replace the large tile outright.
 int gemm_tile_kind(DType dt, int32_t m, int32_t n, int32_t k) {
   if (dt != DType::BF16 || m <= 0) return GEMM_TILE_128x256;
   const long cus = device_cu_count();
   const long tiles = (long)((m + 255) / 256) * (n / 256);
   const long waves = (tiles + cus - 1) / cus;
   const double fill = (double)tiles / (double)(waves * cus);
-  if (fill >= 0.9 || (fill >= 0.6 && k >= 2048)) return GEMM_TILE_256;
+  if (fill >= 0.6) return GEMM_TILE_256;
   if (k % small::kBK == 0 && (long)((m + 127) / 128) * (n / 256) * 2 < cus) return GEMM_TILE_64x128;
   return GEMM_TILE_128x256;
 }
