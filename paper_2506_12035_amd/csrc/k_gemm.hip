@@ -885,9 +885,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_small_kernel(const bf16 *A, con
 // compute units, the 64x128 tile (K a multiple of 128).  Measured at MAR-L
 // sizes, per 64-image range: every full-layer GEMM takes the 256x256 tile
 // (the output projection alone runs slower on it, 80 vs 75 us, but the
-// overlapped step is faster), the cache-aware QKV and fc1 the 128x256 tile,
-// the cache-aware output projection and fc2 the 64x128 one, as do the
-// sampler's per-block GEMMs (a few hundred rows).  Under sustained load the 128x256 tile runs
+// overlapped step is faster), and so does the cache-aware fc1 when a range
+// has more than 2304 active rows (10 x 16 tiles); the cache-aware QKV, and
+// fc1 below that, the 128x256 tile; the cache-aware output projection and fc2
+// the 64x128 one, as do the sampler's per-block GEMMs (a few hundred rows).  Under sustained load the 128x256 tile runs
 // at a lower clock (more operand traffic per flop), which is why it does not
 // replace the large tile outright.
 int gemm_tile_kind(DType dt, int32_t m, int32_t n, int32_t k) {
