@@ -876,19 +876,21 @@ __global__ __launch_bounds__(256) void gemm_bf16_small_kernel(const bf16 *A, con
 }
 
 // Tile choice.  The 256x256 tile (one workgroup per CU) when its tiles fill
-// at least 60% of their last wave over the compute units: a partly filled
+// at least 45% of their last wave over the compute units: a partly filled
 // last wave runs at a higher clock under the chip's power limit, and beside
-// another image range's kernels when the step runs as ranges on streams.
+// another image range's kernels when the step runs as ranges on streams
+// (which is why the bound is this low: with a single range, such a wave
+// leaves the rest of the chip idle).
 // Otherwise the 128x256 tile, two workgroups per CU, whose write-backs
 // overlap the other workgroup's main loop and whose finer steps fill the chip
 // better; and when even 128x256 tiles would occupy fewer than half the
 // compute units, the 64x128 tile (K a multiple of 128).  Measured at MAR-L
 // sizes, per 64-image range: every full-layer GEMM takes the 256x256 tile
 // (the output projection alone runs slower on it, 80 vs 75 us, but the
-// overlapped step is faster), and so does the cache-aware fc1 when a range
-// has more than 2304 active rows (10 x 16 tiles); the cache-aware QKV, and
-// fc1 below that, the 128x256 tile; the cache-aware output projection and fc2
-// the 64x128 one, as do the sampler's per-block GEMMs (a few hundred rows).  Under sustained load the 128x256 tile runs
+// overlapped step is faster), and so do the cache-aware fc1 and QKV when a
+// range has more than 2304 active rows (10 tiles of rows); below that they
+// take the 128x256 tile; the cache-aware output projection and fc2 the 64x128
+// one, as do the sampler's per-block GEMMs (a few hundred rows).  Under sustained load the 128x256 tile runs
 // at a lower clock (more operand traffic per flop), which is why it does not
 // replace the large tile outright.
 int gemm_tile_kind(DType dt, int32_t m, int32_t n, int32_t k) {
@@ -897,7 +899,7 @@ int gemm_tile_kind(DType dt, int32_t m, int32_t n, int32_t k) {
   const long tiles = (long)((m + 255) / 256) * (n / 256);
   const long waves = (tiles + cus - 1) / cus;
   const double fill = (double)tiles / (double)(waves * cus);
-  if (fill >= 0.6) return GEMM_TILE_256;
+  if (fill >= 0.45) return GEMM_TILE_256;
   if (k % small::kBK == 0 && (long)((m + 127) / 128) * (n / 256) * 2 < cus) return GEMM_TILE_64x128;
   return GEMM_TILE_128x256;
 }
