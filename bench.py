@@ -73,7 +73,9 @@ def traffic_for(kernel: str, workload: str):
     with open(path) as f:
         rec = json.load(f)
     e = rec.get(workload, {}).get("classes", {}).get(kernel)
-    if not e or e.get("source_sha") != source_hash(kernel) or not e.get("full_layer_only"):
+    if not e or e.get("source_sha") != source_hash(kernel):
+        return None
+    if not (e.get("full_layer_only") or e.get("same_launches")):
         return None
     return e.get("bytes_per_launch")
 
@@ -104,10 +106,12 @@ def counter_class(name: str):
 def ingest_counters(paths: list, workload: str, full_layer_passes: int, commands: dict) -> dict:
     """profiles/traffic.json entries from four rocprofv3 --pmc CSVs: FETCH_SIZE and
     WRITE_SIZE of one step, then of the plain copy (--calibrate-copy).  Counter
-    KiB per dispatch are scaled by known-bytes / counter for the copy.  Only
-    classes whose every launch in the 64-step schedule is a full-layer launch
-    (the kind a one-step run at t = 0 sees) are comparable per launch with the
-    live timing and are marked so."""
+    KiB per dispatch are scaled by known-bytes / counter for the copy.  A
+    class's average is comparable per launch with the live timing when the
+    counter run covered the same launches (a whole 64-step generation:
+    `same_launches`) or when every launch of the class in the schedule is a
+    full-layer launch (the kind a one-step run at t = 0 sees:
+    `full_layer_only`)."""
     import csv
     import collections
 
@@ -133,7 +137,7 @@ def ingest_counters(paths: list, workload: str, full_layer_passes: int, commands
         w = sum(write.get(c, [0.0])) / max(1, len(write.get(c, [])))
         out[c] = {"fetch_bytes": f * sf, "write_bytes": w * sw, "bytes_per_launch": f * sf + w * sw,
                   "dispatches": len(fetch.get(c, [])), "source_sha": source_hash(c),
-                  "full_layer_only": None}
+                  "full_layer_only": None, "same_launches": None}
     return {"scale": {"fetch": sf, "write": sw}, "classes": out,
             "full_layer_passes": full_layer_passes}
 
@@ -412,6 +416,9 @@ def ingest_main(args) -> int:
     ranges = line.get("config", {}).get("micro_batches", 1)
     for c, e in rec["classes"].items():
         e["full_layer_only"] = launches.get(c) == passes * ranges
+        # the counter run was one whole generation of the same schedule: its
+        # dispatches of the class are the instrumented pass's launches
+        e["same_launches"] = launches.get(c) == e["dispatches"]
     path = os.path.join(ROOT, "profiles", "traffic.json")
     allrec = {}
     if os.path.exists(path):
@@ -434,6 +441,8 @@ def main() -> int:
     ap.add_argument("--micro-batches", type=int, default=2,
                     help="run every decoding step as this many ranges of consecutive images, "
                          "each on its own HIP stream (default 2; 1: the whole batch in one call)")
+    ap.add_argument("--range-sizes", type=str, default=None,
+                    help="comma-separated image count of each range (overrides --micro-batches)")
     ap.add_argument("--ratio-bp", type=int, default=None, help="refresh ratio in basis points")
     ap.add_argument("--full-every", type=int, default=None)
     ap.add_argument("--no-full-recompute", action="store_true")
@@ -518,8 +527,9 @@ def main() -> int:
     log(f"[bench] workload {cfg.name}: generating weights")
     weights = workload.all_weights(cfg)
     log("[bench] uploading")
+    sizes = [int(v) for v in args.range_sizes.split(",")] if args.range_sizes else None
     eng = driver.Engine(cfg, batch=B, weights=weights, strategy=args.strategy,
-                        micro_batches=args.micro_batches)
+                        micro_batches=args.micro_batches, range_sizes=sizes)
     torch.cuda.synchronize()
 
     log(f"[bench] warmup {args.warmup} steps")
@@ -549,7 +559,8 @@ def main() -> int:
                    "d_model": cfg.d_model, "n_heads": cfg.n_heads, "head_dim": cfg.head_dim,
                    "refresh_ratio": cfg.ratio_bp / 10000, "sel_layer": cfg.sel_layer,
                    "full_every": cfg.full_every, "decode_steps": T, "strategy": args.strategy,
-                   "micro_batches": args.micro_batches,
+                   "micro_batches": len(eng.ranges),
+                   "range_sizes": [n for _, n in eng.ranges],
                    "full_steps_in_schedule": sum(p.full for p in eng.plans)},
         "step_us": step_us,
     }
@@ -609,7 +620,7 @@ def main() -> int:
         # stream, so that each kernel's duration is its own and not stretched
         # by a kernel of another range sharing the GPU
         log(f"[bench] instrumented pass over the same {args.steps} steps "
-            f"({args.micro_batches} image range(s) in turn on one stream)")
+            f"({len(eng.ranges)} image range(s) in turn on one stream)")
         eng.overlap = False
         for i in range(args.warmup):
             eng.step(i % T)

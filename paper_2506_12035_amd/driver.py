@@ -91,16 +91,30 @@ class Engine:
                  policy: str = "ratio", budget: Optional[int] = None,
                  full_every: Optional[int] = None, sel_layer: Optional[int] = None,
                  weights: Optional[Sequence[Dict[str, np.ndarray]]] = None,
-                 strategy: str = "marche", first_image: int = 0, micro_batches: int = 1):
+                 strategy: str = "marche", first_image: int = 0, micro_batches: int = 1,
+                 range_sizes: Optional[Sequence[int]] = None):
         """``batch`` images starting at image ``first_image`` of the workload's
         batch.  ``micro_batches`` > 1 runs every step (after the decoder input)
         as that many ranges of consecutive images, each enqueued on a HIP
-        stream of its own (see ``step``)."""
+        stream of its own (see ``step``); the ranges are as equal as possible
+        unless ``range_sizes`` gives each range's image count (positive, summing
+        to the batch; it overrides ``micro_batches``)."""
         if n_layers is not None:
             cfg = cfg.with_(n_layers=n_layers)
         self.cfg = cfg
         self.device = torch.device(device)
         self.B = cfg.batch if batch is None else batch
+        if range_sizes is not None:
+            sizes = [int(n) for n in range_sizes]
+            if not sizes or min(sizes) < 1 or sum(sizes) != self.B:
+                raise ValueError(f"range_sizes={list(range_sizes)} must be positive image "
+                                 f"counts summing to batch={self.B}")
+            S = len(sizes)
+        else:
+            S = micro_batches
+            if not 1 <= S <= max(self.B, 1):
+                raise ValueError(f"micro_batches={S} must lie in [1, batch={self.B}]")
+            sizes = [self.B // S + (1 if i < self.B % S else 0) for i in range(S)]
         if strategy not in STRATEGIES:
             raise ValueError(f"strategy must be one of {STRATEGIES}")
         self.strategy = strategy
@@ -132,10 +146,6 @@ class Engine:
                                            stream=self.stream)
         self.x = torch.empty(self.B, N, D, dtype=torch.float32, device=self.device)
         self.scores = torch.empty(self.B, H, N, dtype=torch.float32, device=self.device)
-        S = micro_batches
-        if not 1 <= S <= max(self.B, 1):
-            raise ValueError(f"micro_batches={S} must lie in [1, batch={self.B}]")
-        sizes = [self.B // S + (1 if i < self.B % S else 0) for i in range(S)]
         self.ranges = [(sum(sizes[:i]), sizes[i]) for i in range(S)]  # (first image, count)
         self.streams = [torch.cuda.Stream(device=self.device) for _ in range(S - 1)]
         # one workspace region per range, sized for the range with every token

@@ -48,6 +48,24 @@ def test_image_ranges_match_the_whole_batch(whole, parts, overlap):
             assert torch.equal(eng.plans[t].ca_idx, ref.plans[t].ca_idx), f"active lists of step {t}"
 
 
+def test_uneven_range_sizes_match_the_whole_batch(whole):
+    """Explicit image counts per range (Engine(range_sizes=...)): unequal
+    ranges, the first larger than the rest, give the same bits as one call."""
+    cfg, ws, ref = whole
+    sizes = [ref.B // 2 + 3, ref.B // 4, ref.B - (ref.B // 2 + 3) - ref.B // 4]
+    say(f"image ranges: {cfg.name} B={ref.B} sizes={sizes}")
+    eng = driver.Engine(cfg, weights=ws, range_sizes=sizes)
+    assert [n for _, n in eng.ranges] == sizes
+    assert [f for f, _ in eng.ranges] == [0, sizes[0], sizes[0] + sizes[1]]
+    for t in STEPS:
+        eng.step(t)
+    torch.cuda.synchronize()
+    assert torch.equal(eng.x, ref.x)
+    for l in range(cfg.n_layers):
+        assert torch.equal(eng.k_layer(l), ref.k_layer(l)), f"K of layer {l}"
+        assert torch.equal(eng.v_layer(l), ref.v_layer(l)), f"V of layer {l}"
+
+
 def test_step_images_touches_only_its_range():
     """marche_step_images on images [2, 4) of a 4-image cache and residual
     stream: images 0 and 1 keep every bit of x and of both caches, and images

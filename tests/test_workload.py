@@ -70,3 +70,17 @@ def test_random_refresh_draws_per_image():
         assert len(set(whole[b].tolist())) == 20 and set(whole[b].tolist()) <= set(cand[b].tolist())
         assert list(whole[b]) == sorted(whole[b])
     assert not np.array_equal(whole, workload.random_refresh(cfg, 5, cand, 20))
+
+
+def test_engine_rejects_bad_range_sizes():
+    """Explicit image counts per range are checked before any device work:
+    empty, non-positive, or not summing to the batch."""
+    import pytest
+    from paper_2506_12035_amd import driver
+
+    cfg = workload.CONFIGS[2]
+    for sizes in ([], [0, 64], [10, 10], [-1, 65], [32, 33]):
+        with pytest.raises(ValueError, match="range_sizes"):
+            driver.Engine(cfg, device="cpu", range_sizes=sizes)
+    with pytest.raises(ValueError, match="micro_batches"):
+        driver.Engine(cfg, device="cpu", micro_batches=0)
