@@ -48,6 +48,36 @@ def test_image_ranges_match_the_whole_batch(whole, parts, overlap):
             assert torch.equal(eng.plans[t].ca_idx, ref.plans[t].ca_idx), f"active lists of step {t}"
 
 
+@pytest.mark.timeout(600)
+def test_headline_ranges_match_the_whole_batch():
+    """The benchmark's default launch configuration at the headline MAR-L
+    size (batch 128, 32 layers): every step as two 64-image ranges on two
+    streams gives the same bits as the whole batch in one call, over full and
+    cache-aware steps.  Together with the stack parity test (whole batch
+    against the oracle) this covers the configuration the benchmark times."""
+    cfg = workload.CONFIGS[3]
+    say(f"image ranges: {cfg.name} B={cfg.batch} default ranges vs one call")
+    ws = workload.all_weights(cfg)
+    ref = driver.Engine(cfg, weights=ws)
+    for t in STEPS:
+        ref.step(t)
+    torch.cuda.synchronize()
+    x_ref = ref.x.clone()
+    k_ref = [ref.k_layer(l).clone() for l in range(cfg.n_layers)]
+    v_ref = [ref.v_layer(l).clone() for l in range(cfg.n_layers)]
+    del ref
+    torch.cuda.empty_cache()
+    eng = driver.Engine(cfg, weights=ws, micro_batches=2)
+    assert [n for _, n in eng.ranges] == [64, 64]
+    for t in STEPS:
+        eng.step(t)
+    torch.cuda.synchronize()
+    assert torch.equal(eng.x, x_ref)
+    for l in range(cfg.n_layers):
+        assert torch.equal(eng.k_layer(l), k_ref[l]), f"K of layer {l}"
+        assert torch.equal(eng.v_layer(l), v_ref[l]), f"V of layer {l}"
+
+
 def test_uneven_range_sizes_match_the_whole_batch(whole):
     """Explicit image counts per range (Engine(range_sizes=...)): unequal
     ranges, the first larger than the rest, give the same bits as one call."""

@@ -1,7 +1,10 @@
 """Full-size decoder-stack parity on the GPU against the fp64 oracle.
 
-The engine runs each stacked workload at its real batch and depth, in the
-launch configuration the benchmark times.  For sampled images and windows of
+The engine runs each stacked workload at its real batch and depth, with the
+whole batch in one call per layer and the benchmark's kernels and tile rule;
+the benchmark's split of every step into image ranges on streams gives the
+same bits as that one call (tests/test_gpu_microbatch.py, at the MAR-L size
+among others).  For sampled images and windows of
 consecutive steps that start at a full step (the first step, or a periodic
 full refresh), the oracle recomputes the same steps from the seeded inputs
 alone: a full step overwrites every cache row before any is read, so the
