@@ -123,8 +123,11 @@ class Engine:
             if policy != "ratio":
                 raise ValueError("a fixed budget needs `budget` (the active-set size)")
             budget = cfg.ratio_bp if ratio_bp is None else ratio_bp
+        schedule.check_budget(policy, budget, cfg.n_tokens)
         self.budget = budget
         self.full_every = cfg.full_every if full_every is None else full_every
+        if self.full_every < 0:
+            raise ValueError("full_every must be >= 0")
         self.sel = cfg.sel_layer if sel_layer is None else sel_layer
         if not 1 <= self.sel <= cfg.n_layers:
             raise ValueError("sel_layer must lie in [1, n_layers]")
@@ -193,6 +196,9 @@ class Engine:
     def set_schedule(self, full_every: int, policy: str, budget: int) -> None:
         """(Re)build the resident index lists of every step for a schedule:
         ``full_every`` = 1 with any budget is full recomputation."""
+        schedule.check_budget(policy, budget, self.cfg.n_tokens)
+        if full_every < 0:
+            raise ValueError("full_every must be >= 0")
         self.full_every, self.policy, self.budget = full_every, policy, budget
         self.plans = [self._plan(t) for t in range(self.cfg.n_steps)]
 
@@ -230,6 +236,10 @@ class Engine:
         if st == "no-caching":
             plan.k = schedule.refresh_count(self.policy, self.budget, N, g, 0)
         excl = np.concatenate([si.gen, forced_cache], axis=1)       # never refreshed
+        if not 0 <= plan.k <= N - excl.shape[1]:
+            # select_refresh would pad R with -1, which the step then indexes with
+            raise ValueError(f"step {t}: refresh count {plan.k} exceeds the "
+                             f"{N - excl.shape[1]} candidates")
         lead = forced_cache if st == "no-generating" else excl     # fixed head of A
         a = lead.shape[1] + plan.k
         ca = np.full((B, a), -1, np.int32)

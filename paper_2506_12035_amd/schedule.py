@@ -31,6 +31,21 @@ def full_step(t: int, full_every: int) -> bool:
     return t == 0 or (full_every > 0 and t % full_every == 0)
 
 
+def check_budget(policy: str, value: int, n_tokens: int) -> None:
+    """Reject budgets whose refresh count could exceed the candidates: a ratio
+    outside [0, 10000] basis points, or a fixed active-set size outside
+    [0, n_tokens].  The device selection would otherwise pad the active list
+    with -1 entries, which the step would index the cache and x with."""
+    if policy == "ratio":
+        if not 0 <= value <= 10000:
+            raise ValueError(f"refresh ratio {value} bp outside [0, 10000]")
+    elif policy == "fixed":
+        if not 0 <= value <= n_tokens:
+            raise ValueError(f"fixed active budget {value} outside [0, n_tokens={n_tokens}]")
+    else:
+        raise ValueError(f"unknown budget policy {policy!r}")
+
+
 def refresh_count(policy: str, value: int, n_tokens: int, n_gen: int, n_cache: int) -> int:
     if policy == "fixed":
         return max(0, value - n_gen - n_cache)

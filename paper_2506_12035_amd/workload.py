@@ -249,6 +249,18 @@ def planted_rows(cfg: Config, candidates: np.ndarray, k: int, batch: Optional[in
     return out
 
 
+def planted_stack_draw(cfg: Config, t: int, image: int, candidates: np.ndarray, k: int):
+    """Seeded draw of a planted-structure stack case for step ``t`` of one
+    image: ``k`` of the image's candidate tokens (ascending) and an anchor row
+    ~ N(0, 1) of width d_model.  The caller turns these into the rows it
+    plants; the generator depends only on (seed, step, image)."""
+    ss = np.random.SeedSequence([cfg.seed_value, STREAM_PLANTED, 7000 + t, image])
+    rng = np.random.Generator(np.random.PCG64(ss))
+    rows = np.sort(rng.choice(np.asarray(candidates), size=k, replace=False)).astype(np.int32)
+    anchor = rng.standard_normal(cfg.d_model, dtype=np.float32)
+    return rows, anchor
+
+
 def random_refresh(cfg: Config, t: int, candidates: np.ndarray, k: int,
                    first: int = 0) -> np.ndarray:
     """Seeded random refresh set of step ``t`` for the random-refresh ablation:

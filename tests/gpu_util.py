@@ -96,3 +96,55 @@ class SingleLayer:
             "scores": scores.cpu().numpy() if want_scores else None,
             "off": off,
         }
+
+
+def record(kind: str, **fields) -> None:
+    """Append one JSON line to the file named by MARCHE_PARITY_LOG, if set, so
+    that a run's parity summary (worst errors, refresh-set counts) outlives
+    pytest's output capture."""
+    import json
+    import os
+    path = os.environ.get("MARCHE_PARITY_LOG")
+    if not path:
+        return
+    d = os.path.dirname(path)
+    if d:
+        os.makedirs(d, exist_ok=True)
+    with open(path, "a") as f:
+        f.write(json.dumps({"kind": kind, **fields}, default=float) + "\n")
+
+
+def check_refresh_set(got, s, excl, k, tol, lowest=False):
+    """Gap rule for a GPU refresh set against the oracle's summed scores s.
+
+    Returns "exact" when the oracle's relative gap at the k-th boundary
+    exceeds tol (the set must then equal the oracle's), else "ambiguous"
+    after checking that the set is valid on both sides of the boundary:
+    every chosen token lies within tol of the k-th score, and every candidate
+    clearly past it (beyond tol) is chosen."""
+    from oracle import select as osel
+    got = sorted(int(v) for v in got)
+    excl = [int(e) for e in excl]
+    cand = np.setdiff1d(np.arange(len(s)), excl)
+    assert len(set(got)) == k and not set(got) & set(excl), "GPU refresh set invalid"
+    assert set(got) <= set(cand.tolist()), "GPU refresh set holds a non-candidate"
+    ordered = np.sort(s[cand])
+    if not lowest:
+        ordered = ordered[::-1]
+    if k == 0:
+        return "exact"
+    sk = ordered[k - 1]
+    gap = (abs(sk - ordered[k]) / max(abs(sk), abs(ordered[k])) if k < len(ordered) else np.inf)
+    if gap > tol:
+        want = osel.select_topk(s, excl, k, lowest=lowest)
+        assert got == list(want), f"refresh set differs with gap {gap:.2e}"
+        return "exact"
+    if lowest:
+        assert all(s[j] <= sk * (1 + tol) for j in got), "GPU refresh set outside tolerance"
+        must = [int(j) for j in cand if s[j] < sk * (1 - tol)]
+    else:
+        assert all(s[j] >= sk * (1 - tol) for j in got), "GPU refresh set outside tolerance"
+        must = [int(j) for j in cand if s[j] > sk * (1 + tol)]
+    missing = sorted(set(must) - set(got))
+    assert not missing, f"tokens clearly past the k-th score were not chosen: {missing[:8]}"
+    return "ambiguous"

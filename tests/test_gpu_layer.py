@@ -15,7 +15,7 @@ import torch
 
 from oracle import block, select
 from paper_2506_12035_amd import binding, workload
-from tests.gpu_util import DEV, TOL, SingleLayer, f64, rel_err, say
+from tests.gpu_util import DEV, TOL, SingleLayer, check_refresh_set, f64, rel_err, say
 
 pytestmark = pytest.mark.gpu
 
@@ -83,19 +83,11 @@ def _fp32_head_sum(scores_bh):
 
 
 def _check_refresh(gpu_sel, ref_scores, excl, k, tol):
-    """Gap rule: exact when the oracle's k-th boundary gap exceeds tol, else valid."""
-    s = ref_scores.sum(axis=0)
-    cand = np.setdiff1d(np.arange(len(s)), excl)
-    ordered = np.sort(s[cand])[::-1]
-    want = select.select_topk(s, excl, k)
-    gap = (ordered[k - 1] - ordered[k]) / ordered[k - 1] if k < len(ordered) else np.inf
+    """Gap rule: exact when the oracle's k-th boundary gap exceeds tol, else
+    valid on both sides of the boundary (tests.gpu_util.check_refresh_set)."""
     got = [int(v) for v in gpu_sel]
-    assert got == sorted(got) and len(set(got)) == k and not set(got) & set(int(e) for e in excl)
-    if gap > tol:
-        assert got == want, f"refresh set differs with gap {gap:.3e}"
-        return True
-    assert all(s[j] >= ordered[k - 1] * (1 - tol) for j in got)
-    return False
+    assert got == sorted(got), "refresh set not ascending"
+    return check_refresh_set(got, ref_scores.sum(axis=0), excl, k, tol) == "exact"
 
 
 def _single_block_inputs(planted=False):

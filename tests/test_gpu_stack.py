@@ -18,23 +18,32 @@ runs one layer per call so every layer can be compared:
   refresh set exact when the oracle's gap at the k-th boundary exceeds the
   tolerance, else valid (k distinct candidates, each within tolerance of the
   k-th score); with a valid but different set, the oracle continues with the
-  GPU's choice, since either is a correct result of the selection rule.
+  GPU's choice, since either is a correct result of the selection rule;
+  a valid set must also hold every candidate clearly above the boundary;
+* planted structure at full size (MAR-L, the cache-aware steps of the window
+  60-62): before the selection layer the generating rows of x are set to a
+  seeded anchor row and k candidate rows to the direction that maximises the
+  anchor query's logits summed over heads (W_k^T q, computed by the oracle
+  from the selection layer's weights), the same fp32 rows on both sides; the
+  refresh set must then equal the planted rows and the oracle's set exactly.
 """
 import numpy as np
 import pytest
 import torch
 
+from oracle import block as oblock
 from oracle import schedule as osched
-from oracle import select as osel
 from oracle import step as ostep
 from paper_2506_12035_amd import driver, workload
-from tests.gpu_util import TOL, rel_err, say
+from tests.gpu_util import TOL, check_refresh_set, record, rel_err, say
 
 pytestmark = pytest.mark.gpu
 
 CASES = {
     "mar-b": dict(cid=2, images=(0, 63), windows=((0, 1, 2),)),
     "mar-l": dict(cid=3, images=(0, 127), windows=((0, 1, 2), (60, 61, 62))),
+    # the selection at full size with a boundary gap far above the tolerance
+    "mar-l-planted": dict(cid=3, images=(0, 127), windows=((60, 61, 62),), planted=True),
     "mar-h": dict(cid=4, images=(255,), windows=((0, 1, 2),)),
     "hires": dict(cid=5, images=(31,), windows=((0, 1, 2),)),
     # ends of the MAR-H refresh-ratio sweep: no refreshing tokens (A = G u N)
@@ -53,7 +62,24 @@ CASES = {
 }
 
 
-def _gpu_step_layerwise(eng, t, images):
+def _plant_rows(cfg, p64, t, b, gen, cache, k):
+    """Planted rows of image b at step t: the generating rows get the seeded
+    anchor row a, k seeded candidates the row v = W_k^T q(a) of the selection
+    layer (q(a) the anchor's query over all heads), scaled to unit variance;
+    its normalised form maximises sum_h q_h(a) . k_h over unit-variance rows.
+    Returned as float32, the values both sides receive."""
+    D = cfg.d_model
+    cand = np.setdiff1d(np.arange(cfg.n_tokens), list(gen) + list(cache))
+    rows, a = workload.planted_stack_draw(cfg, t, b, cand, k)
+    w = p64[cfg.sel_layer - 1]
+    u = oblock.layer_norm(a.astype(np.float64), w["ln1_g"], w["ln1_b"], cfg.ln_eps)
+    q = oblock.linear(u, w["w_qkv"][:D], w["b_qkv"][:D])
+    v = w["w_qkv"][D:2 * D].T @ q
+    v = (v - v.mean()) / v.std()
+    return rows, a.astype(np.float32), v.astype(np.float32)
+
+
+def _gpu_step_layerwise(eng, t, images, plant=None):
     cfg = eng.cfg
     p = eng.plans[t]
     B, N, L, sel = eng.B, cfg.n_tokens, cfg.n_layers, eng.sel
@@ -62,6 +88,12 @@ def _gpu_step_layerwise(eng, t, images):
     rec = {"x_in": eng.x[img].cpu().numpy(), "layers": [], "R": None, "scores": None}
     a = p.a
     for l in range(L):
+        if plant and not p.full and l == sel - 1:
+            # the same fp32 rows the oracle receives, in the GPU's residual stream
+            for b, (rows, gen_rows, anchor, v) in plant.items():
+                eng.x[b, torch.from_numpy(rows.astype(np.int64))] = torch.from_numpy(v).to(eng.x.device)
+                eng.x[b, torch.from_numpy(np.asarray(gen_rows, np.int64))] = torch.from_numpy(anchor).to(eng.x.device)
+            rec["x_planted"] = eng.x[img].cpu().numpy()
         full_layer = p.full or l < sel
         k_before = eng.k_layer(l)[img].clone()
         v_before = eng.v_layer(l)[img].clone()
@@ -94,30 +126,15 @@ def _gpu_step_layerwise(eng, t, images):
 def _validated_override(gpu_R, tol, note, lowest=False):
     """Gap rule for the GPU refresh set (highest or lowest attention mass)."""
     def override(scores, ref_R):
-        s = scores.sum(axis=0)
-        excl = override.excl
-        k = len(ref_R)
         got = sorted(int(v) for v in gpu_R)
-        cand = np.setdiff1d(np.arange(len(s)), excl)
-        ordered = np.sort(s[cand])
-        if not lowest:
-            ordered = ordered[::-1]
-        if 0 < k < len(ordered):
-            gap = abs(ordered[k - 1] - ordered[k]) / max(abs(ordered[k - 1]), abs(ordered[k]))
-        else:
-            gap = np.inf
-        assert len(set(got)) == k and not set(got) & set(excl), "GPU refresh set invalid"
-        if gap > tol:
-            assert got == list(ref_R), f"refresh set differs with gap {gap:.2e}"
-            note["exact"] += 1
-        else:
-            if lowest:
-                assert all(s[j] <= ordered[k - 1] * (1 + tol) for j in got), "GPU refresh set outside tolerance"
-            else:
-                assert all(s[j] >= ordered[k - 1] * (1 - tol) for j in got), "GPU refresh set outside tolerance"
-            note["ambiguous"] += 1
-            note["agree"] += len(set(got) & set(ref_R)) / max(k, 1)
+        kind = check_refresh_set(got, scores.sum(axis=0), override.excl, len(ref_R), tol,
+                                 lowest=lowest)
+        note[kind] += 1
+        if kind == "ambiguous":
+            note["agree"] += len(set(got) & set(ref_R)) / max(len(ref_R), 1)
+        override.kind = kind
         return got
+    override.kind = None
     return override
 
 
@@ -143,11 +160,25 @@ def test_stack_parity(case):
     windows = spec["windows"]
     sampled = {t for w in windows for t in w}
     last = max(sampled)
+    planted = spec.get("planted", False)
+    plants = {}   # (t, b) -> planted rows of that image and step
+    if planted:
+        for t in sorted(sampled):
+            if osched.is_full_step(t, cfg.full_every):
+                continue
+            for b in spec["images"]:
+                gen = osched.generating_tokens(orders[b], cfg.n_buf, cfg.n_steps, t)
+                cache = osched.caching_tokens(orders[b], cfg.n_buf, cfg.n_steps, t)
+                k = ostep.refresh_count(policy, budget, N, len(gen), len(cache))
+                rows, anchor, v = _plant_rows(cfg, p64, t, b, gen, cache, k)
+                plants[t, b] = (rows, gen, anchor, v)
     gpu = {}
     for t in range(last + 1):
         if t in sampled:
-            say(f"  GPU step {t} layer by layer ({'full' if eng.plans[t].full else 'cache-aware'})")
-            gpu[t] = _gpu_step_layerwise(eng, t, spec["images"])
+            say(f"  GPU step {t} layer by layer ({'full' if eng.plans[t].full else 'cache-aware'})"
+                + (" with planted rows" if any(key[0] == t for key in plants) else ""))
+            pl = {b: plants[t, b] for b in spec["images"] if (t, b) in plants}
+            gpu[t] = _gpu_step_layerwise(eng, t, spec["images"], plant=pl or None)
         else:
             eng.step(t)
     torch.cuda.synchronize()
@@ -185,14 +216,36 @@ def test_stack_parity(case):
                     ov = _validated_override(g["R"][i], tol, note, lowest=strategy == "low-attention")
                     ov.excl = gen + forced
                 say(f"  oracle image {b} step {t}")
-                res = ostep.marche_step(p64, x_in, kcs, vcs, gen, forced, n_heads=H, eps=cfg.ln_eps,
-                                        sel_layer=cfg.sel_layer, full=full, k_refresh=k,
-                                        keep_layers=True, refresh_override=ov,
-                                        select_lowest=strategy == "low-attention",
-                                        include_gen=strategy != "no-generating")
+                kw = dict(n_heads=H, eps=cfg.ln_eps, sel_layer=cfg.sel_layer, full=full,
+                          k_refresh=k, keep_layers=True, refresh_override=ov,
+                          select_lowest=strategy == "low-attention",
+                          include_gen=strategy != "no-generating")
+                pl = plants.get((t, b))
+                if pl is None:
+                    res = ostep.marche_step(p64, x_in, kcs, vcs, gen, forced, **kw)
+                else:
+                    # layers before the selection layer, the planted rows, the rest
+                    sel0 = cfg.sel_layer - 1
+                    pre = ostep.marche_step(p64, x_in, kcs, vcs, gen, forced,
+                                            layer_range=range(0, sel0), **kw)
+                    x_pl = pre.x_out.copy()
+                    prow, _, anchor, v = pl
+                    x_pl[prow] = v.astype(np.float64)
+                    x_pl[gen] = anchor.astype(np.float64)
+                    np.testing.assert_array_equal(g["x_planted"][i][prow], v)
+                    res = ostep.marche_step(p64, x_pl, pre.k_caches, pre.v_caches, gen, forced,
+                                            layer_range=range(sel0, L), **kw)
+                    res.layers = pre.layers + res.layers
+                    assert ov.kind == "exact", "planted boundary gap within the tolerance"
+                    assert sorted(g["R"][i]) == prow.tolist() == sorted(res.refresh)
+                    note["planted"] = note.get("planted", 0) + 1
                 x_prev_g = g["x_in"][i].astype(np.float64)
                 x_prev_o = x_in
                 for l, (lg, lo) in enumerate(zip(g["layers"], res.layers)):
+                    if pl is not None and l == cfg.sel_layer - 1:
+                        # the layer's input is the planted stream, on both sides
+                        x_prev_g = g["x_planted"][i].astype(np.float64)
+                        x_prev_o = x_pl
                     rows = lo.rows
                     errs = {
                         "x": rel_err(lg["x"][i][rows], lo.x_out[rows]),
@@ -217,3 +270,9 @@ def test_stack_parity(case):
     say(f"  {case}: worst rel err {({k: f'{v:.2e}' for k, v in worst.items()})}; refresh sets: "
         f"{note['exact']} exact, {note['ambiguous']} ambiguous "
         f"(mean overlap {note['agree'] / max(note['ambiguous'], 1):.3f})")
+    record("stack", case=case, workload=cfg.name, images=list(spec["images"]),
+           windows=[list(w) for w in windows], worst=worst, exact=note["exact"],
+           ambiguous=note["ambiguous"], planted=note.get("planted", 0),
+           mean_overlap=note["agree"] / max(note["ambiguous"], 1))
+    if planted:
+        assert note.get("planted", 0) == len(plants) > 0

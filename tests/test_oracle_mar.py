@@ -240,3 +240,23 @@ def test_decoder_cond_matches_torch_layernorm():
         ln.bias.copy_(T64(b))
         ref = ln(T64(x[gen])).numpy() + pe_diff[[j - n_buf for j in gen]]
     np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("T", [2, 10, 100, 1000])
+def test_cosine_schedule_closed_form(T):
+    """The cosine schedule is defined by its cumulative product,
+    alpha_bar(u) = f(u) / f(0) with f(u) = cos^2((u + s) / (1 + s) * pi / 2) and
+    s = 0.008; the betas are the ratios of consecutive values, clipped at 0.999.
+    The product of (1 - beta) telescopes back to f((i + 1) / T) / f(0) wherever
+    no beta was clipped (every step but the last, where f(1) = 0)."""
+    f = lambda u: math.cos((u + 0.008) / 1.008 * math.pi / 2) ** 2
+    sch = mar.cosine_schedule(T)
+    want = np.array([f((i + 1) / T) / f(0.0) for i in range(T - 1)])
+    np.testing.assert_allclose(sch.alphas_bar[:T - 1], want, rtol=1e-12)
+    # the offset s matters: without the f(0) normalisation the first value
+    # would be f(1/T) itself, off by 1 - f(0) = 1.55e-4
+    assert abs(1.0 - f(0.0) - 1.5542e-4) < 1e-7
+    assert sch.betas[-1] == 0.999
+    # cos^2, not cos: half way through the schedule alpha_bar is near 1/2
+    if T % 2 == 0:
+        assert abs(sch.alphas_bar[T // 2 - 1] - 0.5) < 0.01

@@ -100,3 +100,57 @@ def test_full_step_is_stack_of_full_layers_and_scores_from_gen():
     # the first two layers are identical to the full step's
     np.testing.assert_array_equal(ca.layers[1].x_out, block.full_layer(
         p[1], ca.layers[0].x_out, kcs[1], vcs[1], n_heads=H, eps=cfg.ln_eps).x_out)
+
+
+def test_no_generating_ablation_against_hand_composed_layers():
+    """Table 2's variant without generating tokens: after the selection layer
+    A = N u R, R is still chosen from G's attention mass and excludes G.  Pinned
+    against the layers composed by hand, and by what the variant must leave
+    alone: the rows of G and their cache rows after the selection layer."""
+    cfg = TINY.with_(n_layers=4, sel_layer=2)
+    p, e, o = _inputs(cfg)
+    H, N, dh = cfg.n_heads, cfg.n_tokens, cfg.head_dim
+    rng = np.random.default_rng(17)
+    kcs = [rng.normal(size=(H, N, dh)) for _ in p]
+    vcs = [rng.normal(size=(H, N, dh)) for _ in p]
+    t = 4
+    gen = schedule.generating_tokens(o[1], cfg.n_buf, cfg.n_steps, t)
+    cache = schedule.caching_tokens(o[1], cfg.n_buf, cfg.n_steps, t)
+    known = schedule.known_before(o[1], cfg.n_buf, cfg.n_steps, t)
+    x = step.decoder_input(e.cls[1], e.value[1], e.mask, e.pos, known, cfg.n_buf)
+    k = 5
+    res = step.marche_step(p, x, kcs, vcs, gen, cache, n_heads=H, eps=cfg.ln_eps, sel_layer=2,
+                           full=False, k_refresh=k, keep_layers=True, include_gen=False)
+    with_g = step.marche_step(p, x, kcs, vcs, gen, cache, n_heads=H, eps=cfg.ln_eps, sel_layer=2,
+                              full=False, k_refresh=k, include_gen=True)
+
+    # by hand: two full layers (scores of G at the second), top-k over the
+    # tokens outside G u N, then cache-aware layers on N u R with no scoring rows
+    xx, kk, vv = x, [c.copy() for c in kcs], [c.copy() for c in vcs]
+    for l in range(2):
+        r = block.full_layer(p[l], xx, kk[l], vv[l], gen, H, cfg.ln_eps, score=(l == 1))
+        xx, kk[l], vv[l] = r.x_out, r.k_cache, r.v_cache
+        if l == 1:
+            sc = r.scores
+    R = select.select_topk_bruteforce(sc.sum(axis=0), gen + cache, k)
+    assert res.refresh == R == with_g.refresh
+    assert not set(R) & set(gen + cache) and len(R) == k
+    x_sel = xx
+    for l in range(2, cfg.n_layers):
+        r = block.cache_aware_layer(p[l], xx, kk[l], vv[l], cache + R, [], H, cfg.ln_eps)
+        xx, kk[l], vv[l] = r.x_out, r.k_cache, r.v_cache
+    np.testing.assert_array_equal(res.x_out, xx)
+    for l in range(cfg.n_layers):
+        np.testing.assert_array_equal(res.k_caches[l], kk[l])
+        np.testing.assert_array_equal(res.v_caches[l], vv[l])
+    assert res.active == cache + R
+
+    # G's rows keep the selection layer's output, and their cache rows in the
+    # later layers keep the input's bits; with G included both change
+    np.testing.assert_array_equal(res.x_out[gen], x_sel[gen])
+    assert not np.allclose(with_g.x_out[gen], x_sel[gen])
+    for l in range(2, cfg.n_layers):
+        np.testing.assert_array_equal(res.k_caches[l][:, gen], kcs[l][:, gen])
+        assert not np.allclose(with_g.k_caches[l][:, gen], kcs[l][:, gen])
+    # the rows both variants recompute see different keys at G, so they differ too
+    assert not np.allclose(res.x_out[cache], with_g.x_out[cache])
