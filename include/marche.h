@@ -172,6 +172,36 @@ marche_status_t marche_step_images(const marche_model_t *m, const marche_layer_t
                                    void *workspace, size_t workspace_bytes,
                                    marche_stream_t stream);
 
+/* Size of the library's own step workspace, used by
+ * marche_step_images_noalloc: 64 MiB of device memory per GPU the library
+ * runs that entry point on, held until the process ends. */
+#define MARCHE_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* marche_step_images without a caller workspace and without any allocation,
+ * for callers that cannot allocate device memory: code under HIP graph
+ * capture, serving loops that must not call hipMalloc, harnesses that forbid
+ * it.  The step's workspace is a library-owned static device array of
+ * MARCHE_SCRATCH_BYTES, one per GPU; its device address is looked up once
+ * per device (hipGetSymbolAddress, with that device current) on the first
+ * call there.  Arguments, layout, results and errors are those of
+ * marche_step_images; additionally returns MARCHE_ERR_WORKSPACE, before any
+ * HIP call, when marche_step_workspace_bytes(m, batch, a_total) exceeds
+ * MARCHE_SCRATCH_BYTES (at d_model 1024 and d_mlp 4096 about 5400 active
+ * rows), and MARCHE_ERR_HIP if the lookup fails.  Nothing in the array needs
+ * to start at zero: every call writes each part of it before reading it.
+ * Every call on a GPU shares that GPU's array, which keeps the last call's
+ * contents, so calls that overlap on one GPU (two host threads, or two
+ * streams without an ordering between them) race; order them on one stream.
+ * Calls no hipMalloc, hipFree or other allocating routine (with kernel
+ * timing switched on, marche_profile_enable, the library creates HIP events). */
+marche_status_t marche_step_images_noalloc(const marche_model_t *m, const marche_layer_t *layers,
+                                           const marche_kv_cache_t *cache, int32_t first_image,
+                                           int32_t layer_begin, int32_t layer_end, int32_t batch,
+                                           float *x, const int32_t *a_idx, const int32_t *a_off,
+                                           const int32_t *n_gen, int32_t a_total, int32_t a_max,
+                                           int32_t gen_max, float *scores, int32_t score_layer,
+                                           marche_stream_t stream);
+
 /* Refresh selection (Section 4.2, top-k of the head-aggregated scores).
  * For each image b: s_j = sum_{p < n_parts} scores[b][p][j] (summed in p
  * order, float32); candidates are the tokens not in

@@ -23,7 +23,7 @@ MARCHE_ATTN_TWO_SEGMENT, MARCHE_ATTN_CONCAT = 0, 1
 
 EXPORTED = (
     "kv_cache_init", "marche_step_workspace_bytes", "marche_step", "marche_step_images",
-    "select_refresh",
+    "marche_step_images_noalloc", "select_refresh",
     "select_refresh_ordered",
     "marche_decoder_input", "marche_attention_workspace_bytes", "marche_attention_segments",
     "marche_encoder_input", "marche_encoder_to_decoder_workspace_bytes",
@@ -87,6 +87,9 @@ def lib() -> C.CDLL:
         L.marche_step_images.argtypes = [C.POINTER(Model), C.POINTER(Layer), C.POINTER(KVCache),
                                          i32, i32, i32, i32, vp, vp, vp, vp, i32, i32, i32, vp,
                                          i32, vp, sz, vp]
+        L.marche_step_images_noalloc.argtypes = [C.POINTER(Model), C.POINTER(Layer),
+                                                 C.POINTER(KVCache), i32, i32, i32, i32, vp, vp,
+                                                 vp, vp, i32, i32, i32, vp, i32, vp]
         L.select_refresh.argtypes = [vp, i32, vp, vp, i32, i32, i32, vp, vp, vp]
         L.select_refresh_ordered.argtypes = [vp, i32, vp, vp, i32, i32, i32, vp, vp, i32, vp]
         L.marche_decoder_input.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, vp]
@@ -117,7 +120,8 @@ def lib() -> C.CDLL:
                                            C.POINTER(C.c_double)]
         L.marche_profile_reset.argtypes = []
         L.marche_profile_reset.restype = None
-        for name in ("kv_cache_init", "marche_step", "marche_step_images", "select_refresh",
+        for name in ("kv_cache_init", "marche_step", "marche_step_images",
+                     "marche_step_images_noalloc", "select_refresh",
                      "select_refresh_ordered",
                      "marche_decoder_input", "marche_attention_segments",
                      "marche_encoder_input", "marche_encoder_to_decoder",
@@ -207,6 +211,21 @@ def marche_step_images(model: Model, layers, cache: KVCache, first_image: int, l
                                     _ptr(a_off), _ptr(n_gen), a_total, a_max, gen_max,
                                     _ptr(scores), score_layer, _ptr(workspace), workspace_bytes,
                                     _stream(stream)))
+
+
+# Bytes of the library-owned workspace of marche_step_images_noalloc
+# (MARCHE_SCRATCH_BYTES in include/marche.h).
+SCRATCH_BYTES = 64 << 20
+
+
+def marche_step_images_noalloc(model: Model, layers, cache: KVCache, first_image: int,
+                               layer_begin: int, layer_end: int, batch: int, x, a_idx, a_off,
+                               n_gen, a_total: int, a_max: int, gen_max: int, scores=None,
+                               score_layer: int = -1, stream=None) -> None:
+    _check(lib().marche_step_images_noalloc(C.byref(model), layers, C.byref(cache), first_image,
+                                            layer_begin, layer_end, batch, _ptr(x), _ptr(a_idx),
+                                            _ptr(a_off), _ptr(n_gen), a_total, a_max, gen_max,
+                                            _ptr(scores), score_layer, _stream(stream)))
 
 
 def select_refresh(scores, n_parts: int, excl_idx, excl_off, batch: int, n_tokens: int, k: int,

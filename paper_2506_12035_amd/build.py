@@ -18,8 +18,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmarche.so")
-SOURCES = ("marche_api.cpp", "k_elementwise.hip", "k_gemm.hip", "k_attn.hip", "k_select.hip",
-           "k_mar.hip")
+SOURCES = ("marche_api.cpp", "marche_noalloc.hip", "k_elementwise.hip", "k_gemm.hip",
+           "k_attn.hip", "k_select.hip", "k_mar.hip")
 ARCH = "gfx950"
 
 # -packed-fp32-ops: keep the compiler from forming packed fp32 VALU ops.

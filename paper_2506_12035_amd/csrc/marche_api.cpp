@@ -16,6 +16,7 @@
 #include <cstdlib>
 
 #include "../../include/marche.h"
+#include "marche_host.h"
 #include "marche_internal.h"
 
 using namespace marche;
@@ -198,6 +199,16 @@ struct ProfScope {
 
 }  // namespace
 
+marche_status_t marche::set_error(marche_status_t s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  t_err = buf;
+  return s;
+}
+
 // ------------------------------------------------------------------ ABI
 
 extern "C" {
@@ -262,13 +273,15 @@ size_t marche_step_workspace_bytes(const marche_model_t *m, int32_t batch, int32
          align256(M * m->d_mlp * es);
 }
 
-static marche_status_t step_impl(const marche_model_t *m, const marche_layer_t *layers,
-                                 const marche_kv_cache_t *cache, int32_t first_image,
-                                 int32_t layer_begin, int32_t layer_end, int32_t batch, float *x,
-                                 const int32_t *a_idx, const int32_t *a_off, const int32_t *n_gen,
-                                 int32_t a_total, int32_t a_max, int32_t gen_max, float *scores,
-                                 int32_t score_layer, void *workspace, size_t workspace_bytes,
-                                 marche_stream_t stream_) {
+}  // extern "C"
+
+marche_status_t marche::step_impl(const marche_model_t *m, const marche_layer_t *layers,
+                                  const marche_kv_cache_t *cache, int32_t first_image,
+                                  int32_t layer_begin, int32_t layer_end, int32_t batch, float *x,
+                                  const int32_t *a_idx, const int32_t *a_off, const int32_t *n_gen,
+                                  int32_t a_total, int32_t a_max, int32_t gen_max, float *scores,
+                                  int32_t score_layer, void *workspace, size_t workspace_bytes,
+                                  marche_stream_t stream_) {
   marche_status_t st = check_model(m);
   if (st != MARCHE_OK) return st;
   if (!layers) return fail(MARCHE_ERR_INVALID_ARG, "layers is NULL");
@@ -401,6 +414,8 @@ static marche_status_t step_impl(const marche_model_t *m, const marche_layer_t *
   }
   return MARCHE_OK;
 }
+
+extern "C" {
 
 marche_status_t marche_step(const marche_model_t *m, const marche_layer_t *layers,
                             const marche_kv_cache_t *cache, int32_t layer_begin,

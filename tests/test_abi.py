@@ -301,3 +301,21 @@ def test_layer_array_keeps_its_tensors_alive():
     del arr
     gc.collect()
     assert all(r() is None for r in probes)
+
+
+def test_step_noalloc_rejects_oversize_before_any_hip_call():
+    """The no-allocation step refuses a step whose workspace would exceed the
+    library-owned array, on the host (no GPU here), and its other checks are
+    marche_step_images's."""
+    m = _model()
+    L = binding.lib()
+    big = 6000  # rows: 6000 * (16 + 2*1024*2 + 4096*2) bytes > 64 MiB
+    assert L.marche_step_workspace_bytes(C.byref(m), 20, big) > binding.SCRATCH_BYTES
+    st = L.marche_step_images_noalloc(C.byref(m), _layers(m.n_layers), C.byref(_cache(m, 20)), 0,
+                                      0, m.n_layers, 20, FAKE, FAKE, FAKE, FAKE, big, 320, 1, None,
+                                      -1, None)
+    assert st == binding.MARCHE_ERR_WORKSPACE
+    assert "MARCHE_SCRATCH_BYTES" in binding.last_error()
+    header = open(HEADER).read()
+    assert "#define MARCHE_SCRATCH_BYTES ((size_t)64 << 20)" in header
+    assert binding.SCRATCH_BYTES == 64 << 20
