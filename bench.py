@@ -65,8 +65,8 @@ def source_hash(kernel: str) -> str:
 
 
 def traffic_for(kernel: str, workload: str):
-    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
-    taken on the current kernel source; else None."""
+    """HBM bytes per launch of a timing class from committed rocprofv3 counter
+    runs, if they were taken on the current kernel source; else None."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
@@ -75,13 +75,12 @@ def traffic_for(kernel: str, workload: str):
     e = rec.get(workload, {}).get("classes", {}).get(kernel)
     if not e or e.get("source_sha") != source_hash(kernel):
         return None
-    if not (e.get("full_layer_only") or e.get("same_launches")):
-        return None
     return e.get("bytes_per_launch")
 
 
 def counter_class(name: str):
-    """Timing class of a kernel symbol as rocprofv3 prints it (mangled or not)."""
+    """Timing class of a kernel symbol as rocprofv3 prints it (mangled or not),
+    before the split into full and cache-aware layers."""
     tile = ("t256" if "gemm_bf16_big_kernel" in name else
             "t64x128" if "gemm_bf16_small_kernel" in name else "t128x256")
     if "gemm_bf16" in name:
@@ -93,7 +92,7 @@ def counter_class(name: str):
         return "attention_res"
     if "attn_mfma_kernel" in name:
         for nw, q in (("4", "q128"), ("2", "q64"), ("1", "q32")):
-            if f"ELi{nw}EEEv" in name or f", {nw}>(" in name:
+            if f"ELi{nw}ELb" in name or f"ELi{nw}EEEv" in name or f", {nw}, " in name:
                 return f"attention_{q}"
     for key, cls in (("gather_ln_kernel", "gather_ln"), ("attn_scores_kernel", "attn_scores"),
                      ("select_topk_kernel", "select_topk"), ("decoder_input_kernel", "decoder_input"),
@@ -103,27 +102,46 @@ def counter_class(name: str):
     return None
 
 
-def ingest_counters(paths: list, workload: str, full_layer_passes: int, commands: dict) -> dict:
-    """profiles/traffic.json entries from four rocprofv3 --pmc CSVs: FETCH_SIZE and
-    WRITE_SIZE of one step, then of the plain copy (--calibrate-copy).  Counter
-    KiB per dispatch are scaled by known-bytes / counter for the copy.  A
-    class's average is comparable per launch with the live timing when the
-    counter run covered the same launches (a whole 64-step generation:
-    `same_launches`) or when every launch of the class in the schedule is a
-    full-layer launch (the kind a one-step run at t = 0 sees:
-    `full_layer_only`)."""
+def counter_rows(path: str) -> list:
+    """Per-dispatch records of a rocprofv3 --pmc CSV, in dispatch order, each
+    with its timing class split by layer kind.  The run is `--steps 1
+    --warmup 1` (steps 0 and 1) or `--steps 1 --warmup 0` (step 0): step 0 is a
+    full step (every token active in every layer), so the (class, grid) pairs
+    it launches are the full-layer launches; any later dispatch with a pair it
+    never launched belongs to a cache-aware layer (class + "_ca").  Steps start
+    at the decoder-input kernel, launched once per step."""
     import csv
+    rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Dispatch_Id"]))
+    starts = [i for i, r in enumerate(rows) if "decoder_input_kernel" in r["Kernel_Name"]]
+    step0_end = starts[1] if len(starts) > 1 else len(rows)
+    full = {(counter_class(r["Kernel_Name"]), r["Grid_Size"]) for r in rows[:step0_end]}
+    out = []
+    for r in rows:
+        c = counter_class(r["Kernel_Name"])
+        if c is None:
+            continue
+        key = c if (c, r["Grid_Size"]) in full else c + "_ca"
+        out.append((key, float(r["Counter_Value"])))
+    return out
+
+
+def ingest_counters(paths: list, commands: dict) -> dict:
+    """profiles/traffic.json entries from four rocprofv3 --pmc CSVs: FETCH_SIZE and
+    WRITE_SIZE of the bench's first steps (counter_rows), then of the plain copy
+    (--calibrate-copy).  Counter KiB per dispatch are scaled by known bytes /
+    counter for the copy.  Full-layer classes have one shape in every step,
+    so their per-launch bytes are those of every full-layer launch; a
+    cache-aware class's bytes are those of step 1's active sets."""
     import collections
 
     def per_class(path):
         agg = collections.defaultdict(list)
-        for r in csv.DictReader(open(path)):
-            c = counter_class(r["Kernel_Name"])
-            if c:
-                agg[c].append(float(r["Counter_Value"]) * 1024.0)
+        for key, v in counter_rows(path):
+            agg[key].append(v * 1024.0)
         return agg
 
     def copy_bytes(path):
+        import csv
         v = [float(r["Counter_Value"]) * 1024.0 for r in csv.DictReader(open(path))
              if "copyBuffer" in r["Kernel_Name"]]
         return max(v)
@@ -136,10 +154,8 @@ def ingest_counters(paths: list, workload: str, full_layer_passes: int, commands
         f = sum(fetch.get(c, [0.0])) / max(1, len(fetch.get(c, [])))
         w = sum(write.get(c, [0.0])) / max(1, len(write.get(c, [])))
         out[c] = {"fetch_bytes": f * sf, "write_bytes": w * sw, "bytes_per_launch": f * sf + w * sw,
-                  "dispatches": len(fetch.get(c, [])), "source_sha": source_hash(c),
-                  "full_layer_only": None, "same_launches": None}
-    return {"scale": {"fetch": sf, "write": sw}, "classes": out,
-            "full_layer_passes": full_layer_passes}
+                  "dispatches": len(fetch.get(c, [])), "source_sha": source_hash(c)}
+    return {"scale": {"fetch": sf, "write": sw}, "classes": out}
 
 
 def kernel_rates(prof: dict, dtype: str) -> dict:
@@ -147,7 +163,8 @@ def kernel_rates(prof: dict, dtype: str) -> dict:
     peak_mfma = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_FP32_TFLOPS
     for name, e in prof.items():
         avg_s = e["ms"] * 1e-3 / e["launches"]
-        if name in HBM_BOUND or e["flops"] == 0:
+        base = name[:-3] if name.endswith("_ca") else name   # cache-aware layers' classes
+        if base in HBM_BOUND or e["flops"] == 0:
             ach = e["bytes"] / e["launches"] / avg_s / 1e9
             out[name] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": ach / PEAK_HBM_GBS}
@@ -399,26 +416,11 @@ def e2e_main(args) -> int:
 
 
 def ingest_main(args) -> int:
-    from paper_2506_12035_amd import schedule, workload
+    from paper_2506_12035_amd import workload
 
     cfg = workload.CONFIGS[args.config]
-    T = cfg.n_steps
-    n_full = sum(schedule.full_step(t, cfg.full_every) for t in range(T))
-    passes = n_full * cfg.n_layers + (T - n_full) * cfg.sel_layer
-    fcsv, wcsv, cf, cw, bjson = args.ingest_counters
-    rec = ingest_counters([fcsv, wcsv, cf, cw], cfg.name, passes,
-                          {"copy_bytes": 1024 * (1 << 20)})
-    with open(bjson) as f:
-        lines = [ln for ln in f.read().splitlines() if ln.startswith("{")]
-    line = json.loads(lines[-1])
-    launches = {k: v["launches"] for k, v in line.get("kernels", {}).items()}
-    # with S image ranges every layer pass launches each kernel once per range
-    ranges = line.get("config", {}).get("micro_batches", 1)
-    for c, e in rec["classes"].items():
-        e["full_layer_only"] = launches.get(c) == passes * ranges
-        # the counter run was one whole generation of the same schedule: its
-        # dispatches of the class are the instrumented pass's launches
-        e["same_launches"] = launches.get(c) == e["dispatches"]
+    fcsv, wcsv, cf, cw = args.ingest_counters
+    rec = ingest_counters([fcsv, wcsv, cf, cw], {"copy_bytes": 1024 * (1 << 20)})
     path = os.path.join(ROOT, "profiles", "traffic.json")
     allrec = {}
     if os.path.exists(path):
@@ -471,12 +473,11 @@ def main() -> int:
                          "cache-aware decoder and the sampler (s/image), against full recompute "
                          "of the decoder with the same encoder and sampler")
     ap.add_argument("--e2e-config", default="mar-l-e2e", help="whole-model workload name")
-    ap.add_argument("--ingest-counters", nargs=5, default=None,
-                    metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV", "BENCH_JSON"),
+    ap.add_argument("--ingest-counters", nargs=4, default=None,
+                    metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="write profiles/traffic.json from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE "
-                         "CSVs of a one-step run (--steps 1 --warmup 0) and of --calibrate-copy "
-                         "1024, with the bench JSON line of a kernel-trace run of the same "
-                         "workload (to mark classes launched only in full layers); no GPU needed")
+                         "CSVs of a run of the first steps (--steps 1 --warmup 1: a full and a "
+                         "cache-aware step) and of --calibrate-copy 1024; no GPU needed")
     args = ap.parse_args()
     if args.ingest_counters:
         return ingest_main(args)

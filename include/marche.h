@@ -387,7 +387,10 @@ const char *marche_last_error(void);
  * (flops and bytes, from the launch shape) is recorded.
  * marche_profile_collect() synchronises those events (host sync), folds them
  * into per-kernel totals and returns the number of kernel classes;
- * marche_profile_entry() reads one.  marche_profile_reset() clears them. */
+ * marche_profile_entry() reads one.  marche_profile_reset() clears them.
+ * A class is one kernel symbol; launches of the decoder step in layers where
+ * not every token of every image is active (cache-aware layers) form classes
+ * of their own, named with the suffix "_ca". */
 marche_status_t marche_profile_enable(int32_t on);
 int32_t marche_profile_collect(void);
 marche_status_t marche_profile_entry(int32_t i, const char **name, int64_t *launches,

@@ -118,6 +118,23 @@ const char *const kClassNames[K_NCLASS] = {
     "gemm_qkv_t64x128",  "gemm_o_t64x128", "gemm_fc1_t64x128",  "gemm_fc2_t64x128",
     "gemm_embed_t64x128", "gemm_head_t64x128", "gemm_head_silu_t64x128", "transpose"};
 
+// Launches inside marche_step in layers where not every token of every image
+// is active (cache-aware layers) are timed under a class of their own: the
+// class index + K_NCLASS, named with the suffix "_ca".  A class without the
+// suffix then holds only full-layer launches (or launches outside the step),
+// whose hardware counters a one-step run at a full step measures.
+constexpr int K_NTIMED = 2 * K_NCLASS;
+
+const char *class_name(int i) {
+  static const std::vector<std::string> names = [] {
+    std::vector<std::string> v;
+    for (int j = 0; j < K_NCLASS; ++j) v.emplace_back(kClassNames[j]);
+    for (int j = 0; j < K_NCLASS; ++j) v.emplace_back(std::string(kClassNames[j]) + "_ca");
+    return v;
+  }();
+  return names[i].c_str();
+}
+
 // Timing class of a GEMM launch: base is the projection's 128x256 class, the
 // 256x256 class follows it; the 64x128 classes are listed separately.
 int gemm_class(int base, DType dt, int32_t m, int32_t n, int32_t k) {
@@ -154,7 +171,7 @@ std::mutex g_mu;
 bool g_prof = false;
 std::vector<Pending> g_pending;
 std::vector<hipEvent_t> g_pool;
-Totals g_tot[K_NCLASS];
+Totals g_tot[K_NTIMED];
 
 hipEvent_t pool_get() {
   if (!g_pool.empty()) {
@@ -369,7 +386,9 @@ marche_status_t marche::step_impl(const marche_model_t *m, const marche_layer_t 
   const size_t layer_elems = (size_t)cache->batch * H * N * dh;
   const double gemm_bytes_act = (double)es;
 
-  LAUNCH(K_ROW_MAP, 0, (double)M * (4 + sizeof(RowMap)),
+  // timing class offset: cache-aware layers (not every token active) apart
+  const int ko = (int64_t)a_total == (int64_t)batch * N ? 0 : K_NCLASS;
+  LAUNCH(K_ROW_MAP + ko, 0, (double)M * (4 + sizeof(RowMap)),
          launch_row_map(map, a_idx, a_off, batch, N, stream));
 
   for (int l = layer_begin; l < layer_end; ++l) {
@@ -379,35 +398,35 @@ marche_status_t marche::step_impl(const marche_model_t *m, const marche_layer_t 
     char *kc = static_cast<char *>(cache->k) + base;
     char *vc = static_cast<char *>(cache->v) + base;
 
-    LAUNCH(K_GATHER_LN, 0, (double)M * D * (4 + es),
+    LAUNCH(K_GATHER_LN + ko, 0, (double)M * D * (4 + es),
            launch_gather_ln(dt, buf0, x, map, static_cast<const float *>(L.ln1_g),
                             static_cast<const float *>(L.ln1_b), M, D, m->ln_eps, stream));
     QkvOut qo{buf1, kc, vc, D, dh, H, N};
-    LAUNCH(gemm_class(K_GEMM_QKV, dt, M, 3 * D, D), 2.0 * M * 3 * D * D,
+    LAUNCH(gemm_class(K_GEMM_QKV, dt, M, 3 * D, D) + ko, 2.0 * M * 3 * D * D,
            gemm_bytes_act * ((double)M * D + 3.0 * D * D + 3.0 * M * D),
            launch_gemm_qkv(dt, buf0, L.w_qkv, static_cast<const float *>(L.b_qkv), M, 3 * D, D,
                            map, qo, stream));
     AttnArgs aa{buf1, kc, vc, buf0, a_off, map, batch, H, N, dh, D, M, a_max};
     // Algorithmic traffic: every cached K/V element of the batch read once,
     // plus the queries read and the outputs written.
-    LAUNCH(attn_class(dt, a_max, N), 4.0 * M * N * D, es * (2.0 * batch * N * D + 2.0 * M * D),
+    LAUNCH(attn_class(dt, a_max, N) + ko, 4.0 * M * N * D, es * (2.0 * batch * N * D + 2.0 * M * D),
            launch_attention(dt, aa, stream));
     if (want_scores && l == score_layer) {
-      LAUNCH(K_ATTN_SCORES, 2.0 * batch * gen_max * N * D,
+      LAUNCH(K_ATTN_SCORES + ko, 2.0 * batch * gen_max * N * D,
              es * (double)batch * N * D + 4.0 * batch * H * N,
              launch_attn_scores(dt, aa, n_gen, gen_max, scores, stream));
     }
-    LAUNCH(gemm_class(K_GEMM_O, dt, M, D, D), 2.0 * M * D * D, gemm_bytes_act * ((double)M * D + (double)D * D) + 8.0 * M * D,
+    LAUNCH(gemm_class(K_GEMM_O, dt, M, D, D) + ko, 2.0 * M * D * D, gemm_bytes_act * ((double)M * D + (double)D * D) + 8.0 * M * D,
            launch_gemm_resid(dt, buf0, L.w_o, static_cast<const float *>(L.b_o), M, D, D, map, x,
                              0, stream));
-    LAUNCH(K_GATHER_LN, 0, (double)M * D * (4 + es),
+    LAUNCH(K_GATHER_LN + ko, 0, (double)M * D * (4 + es),
            launch_gather_ln(dt, buf1, x, map, static_cast<const float *>(L.ln2_g),
                             static_cast<const float *>(L.ln2_b), M, D, m->ln_eps, stream));
-    LAUNCH(gemm_class(K_GEMM_FC1, dt, M, F, D), 2.0 * M * F * D,
+    LAUNCH(gemm_class(K_GEMM_FC1, dt, M, F, D) + ko, 2.0 * M * F * D,
            gemm_bytes_act * ((double)M * D + (double)F * D + (double)M * F),
            launch_gemm_gelu(dt, buf1, L.w_1, static_cast<const float *>(L.b_1), M, F, D, hid,
                             stream));
-    LAUNCH(gemm_class(K_GEMM_FC2, dt, M, D, F), 2.0 * M * D * F,
+    LAUNCH(gemm_class(K_GEMM_FC2, dt, M, D, F) + ko, 2.0 * M * D * F,
            gemm_bytes_act * ((double)M * F + (double)D * F) + 8.0 * M * D,
            launch_gemm_resid(dt, hid, L.w_2, static_cast<const float *>(L.b_2), M, D, F, map, x,
                              1, stream));
@@ -876,15 +895,15 @@ int32_t marche_profile_collect(void) {
     g_pool.push_back(p.e1);
   }
   g_pending.clear();
-  return K_NCLASS;
+  return K_NTIMED;
 }
 
 marche_status_t marche_profile_entry(int32_t i, const char **name, int64_t *launches,
                                      double *total_ms, double *flops, double *bytes) {
-  if (i < 0 || i >= K_NCLASS) return fail(MARCHE_ERR_INVALID_ARG, "profile entry %d out of range", i);
+  if (i < 0 || i >= K_NTIMED) return fail(MARCHE_ERR_INVALID_ARG, "profile entry %d out of range", i);
   std::lock_guard<std::mutex> lk(g_mu);
   const Totals &t = g_tot[i];
-  if (name) *name = kClassNames[i];
+  if (name) *name = class_name(i);
   if (launches) *launches = t.launches;
   if (total_ms) *total_ms = t.ms;
   if (flops) *flops = t.flops;

@@ -232,7 +232,8 @@ def test_stack_parity(case):
                     prow, _, anchor, v = pl
                     x_pl[prow] = v.astype(np.float64)
                     x_pl[gen] = anchor.astype(np.float64)
-                    np.testing.assert_array_equal(g["x_planted"][i][prow], v)
+                    np.testing.assert_array_equal(g["x_planted"][i][prow],
+                                                  np.broadcast_to(v, (len(prow), v.size)))
                     res = ostep.marche_step(p64, x_pl, pre.k_caches, pre.v_caches, gen, forced,
                                             layer_range=range(sel0, L), **kw)
                     res.layers = pre.layers + res.layers
