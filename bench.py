@@ -82,7 +82,8 @@ def counter_class(name: str):
     """Timing class of a kernel symbol as rocprofv3 prints it (mangled or not),
     before the split into full and cache-aware layers."""
     tile = ("t256" if "gemm_bf16_big_kernel" in name else
-            "t64x128" if "gemm_bf16_small_kernel" in name else "t128x256")
+            "t64x128" if "gemm_bf16_small_kernel" in name else
+            "t128" if "gemm_bf16_mid_kernel" in name else "t128x256")
     if "gemm_bf16" in name:
         for key, cls in (("EpiResidILi1E", "fc2"), ("EpiResid<1>", "fc2"), ("EpiResidILi0E", "o"),
                          ("EpiResid<0>", "o"), ("EpiGelu", "fc1"), ("EpiQkv", "qkv")):

@@ -730,6 +730,154 @@ __global__ __launch_bounds__(256, NS <= 3 ? 2 : 1) void gemm_bf16_pair_kernel(
                           rows_lds + wm * 64, bias);
 }
 
+// ------------------------------------------------------------------ 128x128 tile
+//
+// For the narrow products of cache-aware layers (N = d_model: the output
+// projection and fc2 on a few thousand active rows), where 256x256 tiles
+// would occupy a few dozen compute units and the 64x128 tile moves more
+// operand bytes per k-tile than its MFMAs take cycles (so it waits on the
+// L2).  A 128x128x64 tile on four wavefronts of 64x64 (4 accumulator blocks)
+// keeps one 64-row MFMA block per operand fragment and about as many load
+// cycles per k-tile as MFMA cycles.  Operand stages use the 256x256 tile's
+// 128-byte rows, XOR swizzle and direct-to-LDS loads (big::load_lds): NS
+// stages of 32 KB, the loads of k-tile t + NS - 1 issued once every
+// wavefront is done with k-tile t - 1, so NS - 1 k-tiles are in flight.
+// No split of K: every output is one accumulation over all of K in
+// ascending k16 steps, as in every other tile, so the result does not depend
+// on which tile a shape gets.
+namespace mid {
+
+constexpr int kBM = 128, kBN = 128, kBK = 64;
+constexpr int kStage = (kBM + kBN) * kBK * 2;  // 32 KB: activation rows, then weight rows
+constexpr int kWOff = kBM * kBK * 2;           // weight rows 16 KB into a stage
+
+struct Frag {
+  bf16x8 x[2];  // activation rows (MFMA B operand)
+  bf16x8 w[2];  // weight rows (MFMA A operand)
+};
+
+// Fragments of k16 step s (0..3) of a stage for wavefront (wm, wn).
+__device__ __forceinline__ void read_frags(Frag &f, const unsigned char *stage, int s, int wm,
+                                           int wn, int lane) {
+  const int kc = s * 2 + (lane >> 5);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int row = wm * 64 + i * 32 + (lane & 31);
+    f.x[i] = *reinterpret_cast<const bf16x8 *>(stage + row * 128 + big::swz(row, kc) * 16);
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int row = wn * 64 + j * 32 + (lane & 31);
+    f.w[j] = *reinterpret_cast<const bf16x8 *>(stage + kWOff + row * 128 + big::swz(row, kc) * 16);
+  }
+}
+
+__device__ __forceinline__ void mfma(f32x16 (&acc)[2][2], const Frag &f) {
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.w[j], f.x[i], acc[j][i], 0, 0, 0);
+}
+
+}  // namespace mid
+
+// Wait until at most n whole k-tiles (8 loads per wavefront each) of this
+// wavefront's loads are in flight and its LDS reads are done, then the
+// workgroup barrier; n in [0, 3].
+__device__ __forceinline__ void mid_barrier(int n) {
+  if (n >= 3) pair::barrier_vm<24>();
+  else if (n == 2) pair::barrier_vm<16>();
+  else if (n == 1) pair::barrier_vm<8>();
+  else pair::barrier_vm<0>();
+}
+
+template <class Epi, int NS>
+__global__ __launch_bounds__(256, 1) void gemm_bf16_mid_kernel(const bf16 *A, const bf16 *W, int M,
+                                                               int N, int K, Epi epi) {
+  using namespace mid;
+  using big::pin;
+  using Row = typename Epi::Row;
+  static_assert(NS >= 3 && NS <= 5, "stage count (the staged write-back needs 3 stages)");
+  // NS stages of 32 KB; after the main loop the write-back stages its rows in
+  // [0, 66 KB) and the tile's row records sit at 96 KB (in the fourth stage,
+  // or the third's second half)
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[NS * kStage];
+  constexpr int kRowsOff = 96 * 1024 - (NS == 3 ? 16 * 1024 : 0);
+  static_assert(4 * 32 * big::kWbStride * 4 <= kRowsOff, "staged write-back below the row records");
+  static_assert(kRowsOff + kBM * sizeof(Row) <= NS * kStage, "row records fit the stages");
+  const int tiles_m = (M + kBM - 1) / kBM, tiles_n = N / kBN;
+  int tm, tn;
+  tile_coords(xcd_remap(blockIdx.x, gridDim.x), tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * kBM, n0 = tn * kBN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void *)smem;
+  const unsigned char *smem_u = smem;
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) acc[j][i] = f32x16{};
+  const int nk = K / kBK;
+  // k-tile t into stage st: 16 load instructions of 1 KB (8 rows) per operand,
+  // four of each per wavefront
+  auto load_tile = [&](int st, int t) {
+    const unsigned sb = lds0 + (unsigned)st * kStage;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      big::load_lds(sb, wave * 4 + p, A, M, K, m0, t * kBK, lane);
+      big::load_lds(sb + kWOff, wave * 4 + p, W, N, K, n0, t * kBK, lane);
+    }
+  };
+
+  // the write-back's row record (threads < 128) and this lane's bias, kept in
+  // registers until after the main loop
+  Row rec{};
+  if (tid < kBM) rec = epi.row(min(m0 + tid, M - 1));
+  const f32x4 bias = epi.bias4(n0 + wn * 64 + (lane & 15) * 4);
+
+  // k-tiles 0 .. NS-2 in flight, then wait for k-tile 0
+  const int issued = min(NS - 1, nk);
+#pragma unroll
+  for (int t = 0; t < NS - 1; ++t)
+    if (t < nk) load_tile(t, t);
+  mid_barrier(issued - 1);
+  Frag f[2];
+  read_frags(f[0], smem_u, 0, wm, wn, lane);
+
+  for (int t = 0; t < nk; ++t) {
+    const unsigned char *sc = smem_u + (t % NS) * kStage;
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      read_frags(f[(s + 1) & 1], sc, s + 1, wm, wn, lane);
+      mfma(acc, f[s & 1]);
+      pin();
+    }
+    if (t + 1 < nk) {
+      // k-tile t+1 landed and every wavefront is done with k-tile t-1's
+      // stage.  Issued so far: k-tiles up to t + NS - 2, so the ones after
+      // t + 1 that may stay in flight number min(NS - 3, nk - t - 2)
+      mid_barrier(min(NS - 3, nk - t - 2));
+      read_frags(f[0], smem_u + ((t + 1) % NS) * kStage, 0, wm, wn, lane);
+      // k-tile t+NS-1 into the stage k-tile t-1 used (free: the barrier above)
+      if (t + NS - 1 < nk) load_tile((t + NS - 1) % NS, t + NS - 1);
+    }
+    mfma(acc, f[1]);
+    pin();
+  }
+  // every wavefront is done with the stages before the row records and the
+  // staged rows overwrite them
+  pair::barrier_vm<0>();
+  Row *rows_lds = reinterpret_cast<Row *>(smem + kRowsOff);
+  if (tid < kBM) rows_lds[tid] = rec;
+  pair::barrier_vm<0>();
+  write_back_staged<2, 2, 8>(acc, epi, m0 + wm * 64, n0 + wn * 64, M, lane,
+                             reinterpret_cast<float *>(smem) + wave * 32 * big::kWbStride,
+                             rows_lds + wm * 64, bias);
+}
+
 // ------------------------------------------------------------------ 64x128 tile
 //
 // For products too small to spread 128x256 tiles over the chip (the sampler's
@@ -900,7 +1048,14 @@ int gemm_tile_kind(DType dt, int32_t m, int32_t n, int32_t k) {
   const long waves = (tiles + cus - 1) / cus;
   const double fill = (double)tiles / (double)(waves * cus);
   if (fill >= 0.45) return GEMM_TILE_256;
-  if (k % small::kBK == 0 && (long)((m + 127) / 128) * (n / 256) * 2 < cus) return GEMM_TILE_64x128;
+  if (k % small::kBK == 0 && (long)((m + 127) / 128) * (n / 256) * 2 < cus) {
+    // narrow products that 128x128 tiles still spread over half the compute
+    // units or more take them (the cache-aware output projection and fc2 of
+    // a 64-image MAR-L range: 39 vs 52 us for fc2, 13.5 vs 19.8 us for the
+    // output projection, each alone); smaller ones the 64x128 tile
+    if ((long)((m + mid::kBM - 1) / mid::kBM) * (n / mid::kBN) * 2 >= cus) return GEMM_TILE_128;
+    return GEMM_TILE_64x128;
+  }
   return GEMM_TILE_128x256;
 }
 
@@ -919,6 +1074,10 @@ static hipError_t run_bf16(const void *a, const void *w, int m, int n, int k, co
     case GEMM_TILE_64x128:
       gemm_bf16_small_kernel<Epi>
           <<<((m + small::kBM - 1) / small::kBM) * (n / small::kBN), 256, 0, s>>>(A, W, m, n, k, epi);
+      break;
+    case GEMM_TILE_128:
+      gemm_bf16_mid_kernel<Epi, 4>
+          <<<((m + mid::kBM - 1) / mid::kBM) * (n / mid::kBN), 256, 0, s>>>(A, W, m, n, k, epi);
       break;
     default: {
       const int tiles = ((m + pair::kBM - 1) / pair::kBM) * (n / pair::kBN);

@@ -102,7 +102,8 @@ enum KClass {
   K_ENC_INPUT, K_MASK_FILL, K_LN_ROWS, K_GEMM_EMBED, K_GEMM_EMBED_L, K_TIME_SINUS, K_GEMM_HEAD,
   K_GEMM_HEAD_L, K_GEMM_HEAD_SILU, K_GEMM_HEAD_SILU_L, K_HEAD_SILU_COND, K_HEAD_IN_MOD,
   K_HEAD_GATE_MOD, K_HEAD_OUT_STEP, K_GEMM_QKV_S, K_GEMM_O_S, K_GEMM_FC1_S, K_GEMM_FC2_S,
-  K_GEMM_EMBED_S, K_GEMM_HEAD_S, K_GEMM_HEAD_SILU_S, K_TRANSPOSE,
+  K_GEMM_EMBED_S, K_GEMM_HEAD_S, K_GEMM_HEAD_SILU_S, K_TRANSPOSE, K_GEMM_QKV_M, K_GEMM_O_M,
+  K_GEMM_FC1_M, K_GEMM_FC2_M, K_GEMM_EMBED_M, K_GEMM_HEAD_M, K_GEMM_HEAD_SILU_M,
   K_NCLASS
 };
 const char *const kClassNames[K_NCLASS] = {
@@ -116,7 +117,10 @@ const char *const kClassNames[K_NCLASS] = {
     "gemm_head_t128x256", "gemm_head_t256", "gemm_head_silu_t128x256", "gemm_head_silu_t256",
     "head_silu_cond",    "head_in_mod",    "head_gate_mod",     "head_out_step",
     "gemm_qkv_t64x128",  "gemm_o_t64x128", "gemm_fc1_t64x128",  "gemm_fc2_t64x128",
-    "gemm_embed_t64x128", "gemm_head_t64x128", "gemm_head_silu_t64x128", "transpose"};
+    "gemm_embed_t64x128", "gemm_head_t64x128", "gemm_head_silu_t64x128", "transpose",
+    "gemm_qkv_t128",     "gemm_o_t128",    "gemm_fc1_t128",     "gemm_fc2_t128",
+    "gemm_embed_t128",   "gemm_head_t128", "gemm_head_silu_t128"};
+static_assert(sizeof(kClassNames) / sizeof(kClassNames[0]) == K_NCLASS, "one name per class");
 
 // Launches inside marche_step in layers where not every token of every image
 // is active (cache-aware layers) are timed under a class of their own: the
@@ -140,6 +144,17 @@ const char *class_name(int i) {
 int gemm_class(int base, DType dt, int32_t m, int32_t n, int32_t k) {
   const int kind = gemm_tile_kind(dt, m, n, k);
   if (kind == GEMM_TILE_256) return base + 1;
+  if (kind == GEMM_TILE_128) {
+    switch (base) {
+      case K_GEMM_QKV: return K_GEMM_QKV_M;
+      case K_GEMM_O: return K_GEMM_O_M;
+      case K_GEMM_FC1: return K_GEMM_FC1_M;
+      case K_GEMM_FC2: return K_GEMM_FC2_M;
+      case K_GEMM_EMBED: return K_GEMM_EMBED_M;
+      case K_GEMM_HEAD: return K_GEMM_HEAD_M;
+      default: return K_GEMM_HEAD_SILU_M;
+    }
+  }
   if (kind != GEMM_TILE_64x128) return base;
   switch (base) {
     case K_GEMM_QKV: return K_GEMM_QKV_S;

@@ -243,3 +243,30 @@ def test_select_refresh_lowest_first():
     for b in range(B):
         assert list(sel[b]) == select.select_topk(_fp32_head_sum(s[b]), excl[b], k, lowest=True)
     assert 11 not in sel[2]
+
+
+def test_bf16_layer_cache_aware_range_size():
+    """A cache-aware MAR-L layer on a 64-image range (34-44 active rows per
+    image, about 2500 in all): the size at which the output projection and fc2
+    take the 128x128 tile.  Every image against the oracle; the timing classes
+    confirm which kernels ran."""
+    cfg = workload.CONFIGS[3]
+    B = 64
+    rng = np.random.default_rng(77)
+    sizes = [int(v) for v in rng.integers(34, 45, size=B)]
+    gens = [int(v) for v in rng.integers(1, 8, size=B)]
+    x, kc, vc, active, gens = _ragged_case(cfg, B, sizes, gens, seed=78)
+    p = workload.layer_weights(cfg, 5)
+    say(f"bf16 layer at a 64-image range: a_total={sum(sizes)}")
+    ref = _oracle_layer(cfg, f64(p), x, kc, vc, active, gens)
+    run = SingleLayer(cfg, p, x, kc, vc)
+    binding.profile_reset()
+    binding.profile_enable(True)
+    try:
+        gpu = run.run(active, gens)
+        prof = binding.profile_collect()
+    finally:
+        binding.profile_enable(False)
+        binding.profile_reset()
+    _check_layer(cfg, x, kc, vc, active, gens, gpu, ref, TOL["bf16"])
+    assert {"gemm_o_t128_ca", "gemm_fc2_t128_ca"} <= set(prof), sorted(prof)
