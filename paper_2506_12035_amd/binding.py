@@ -13,7 +13,9 @@ import os
 from typing import Optional, Sequence
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libmarche.so")
+# MARCHE_LIB_PATH names another build of the same ABI (the sanitized host
+# build the ABI tests run under); by default the library next to this file.
+LIB_PATH = os.environ.get("MARCHE_LIB_PATH") or os.path.join(_HERE, "libmarche.so")
 
 MARCHE_OK, MARCHE_ERR_INVALID_ARG, MARCHE_ERR_UNSUPPORTED, MARCHE_ERR_HIP, MARCHE_ERR_WORKSPACE = range(5)
 MARCHE_F32, MARCHE_BF16 = 0, 1

@@ -12,6 +12,7 @@ import shutil
 import subprocess
 import sys
 from concurrent.futures import ThreadPoolExecutor
+from typing import Optional
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
@@ -67,6 +68,50 @@ def build(verbose: bool = False) -> str:
     if verbose:
         print(f"built {LIB}")
     return LIB
+
+
+# Host-side sources of the C ABI (argument validation, workspace layout,
+# launch sequence); the sanitized build instruments these for the host only.
+HOST_SOURCES = ("marche_api.cpp", "marche_noalloc.hip")
+SAN_LIB = os.path.join(BUILD, "libmarche_san.so")
+SAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+             "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-fno-sanitize-recover=all"]
+
+
+def asan_runtime() -> Optional[str]:
+    """The clang AddressSanitizer runtime matching hipcc's host compiler."""
+    import glob
+    hits = sorted(glob.glob("/opt/rocm/lib/llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so"))
+    return hits[-1] if hits else None
+
+
+def build_sanitized() -> str:
+    """libmarche_san.so: the host-side sources built with AddressSanitizer and
+    UndefinedBehaviorSanitizer (host code only; device code is untouched),
+    linked with the kernel objects of the last build().  For running the
+    host-only ABI tests under the sanitizers; the runtime is preloaded by the
+    caller (asan_runtime())."""
+    os.makedirs(BUILD, exist_ok=True)
+    objs = []
+    for src in SOURCES:
+        obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+        if src in HOST_SOURCES:
+            obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".san.o")
+            lang = [] if src.endswith(".cpp") else ["-x", "hip"]
+            cmd = [hipcc(), *COMMON, *SAN_FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
+            r = subprocess.run(cmd, capture_output=True, text=True)
+            if r.returncode != 0:
+                raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+        elif not os.path.exists(obj):
+            _compile(src)
+        objs.append(obj)
+    tmp = SAN_LIB + ".tmp"
+    cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, SAN_LIB)
+    return SAN_LIB
 
 
 if __name__ == "__main__":

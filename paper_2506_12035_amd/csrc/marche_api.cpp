@@ -64,6 +64,18 @@ marche_status_t fail_hip(hipError_t e, const char *what) {
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
+// The int a caller stored in an enum-typed field or argument.  A C caller may
+// store any int there, and in C++ reading an enum object whose value lies
+// outside the enumeration's range is undefined, so caller-supplied enums are
+// read through their object representation before they are validated.
+template <class E>
+int32_t raw_enum(const E &e) {
+  static_assert(sizeof(E) == sizeof(int32_t), "C enums are int-sized");
+  int32_t v;
+  std::memcpy(&v, &e, sizeof v);
+  return v;
+}
+
 size_t elem_size(int32_t dt) { return dt == MARCHE_BF16 ? 2 : 4; }
 
 marche_status_t check_model(const marche_model_t *m) {
@@ -72,8 +84,8 @@ marche_status_t check_model(const marche_model_t *m) {
   if (m->n_heads < 1 || m->head_dim < 1 || m->d_model != m->n_heads * m->head_dim)
     return fail(MARCHE_ERR_INVALID_ARG, "model.d_model=%d != n_heads*head_dim (%d*%d)", m->d_model,
                 m->n_heads, m->head_dim);
-  if (m->dtype != MARCHE_F32 && m->dtype != MARCHE_BF16)
-    return fail(MARCHE_ERR_UNSUPPORTED, "model.dtype=%d is not F32 or BF16", m->dtype);
+  if (raw_enum(m->dtype) != MARCHE_F32 && raw_enum(m->dtype) != MARCHE_BF16)
+    return fail(MARCHE_ERR_UNSUPPORTED, "model.dtype=%d is not F32 or BF16", raw_enum(m->dtype));
   if (m->head_dim != 64 && m->head_dim != 80)
     return fail(MARCHE_ERR_UNSUPPORTED, "model.head_dim=%d (supported: 64, 80)", m->head_dim);
   if (m->d_model % 256 != 0 || m->d_model > 2048)
@@ -246,7 +258,7 @@ marche_status_t marche::set_error(marche_status_t s, const char *fmt, ...) {
 extern "C" {
 
 const char *marche_status_string(marche_status_t s) {
-  switch (s) {
+  switch (raw_enum(s)) {
     case MARCHE_OK: return "MARCHE_OK";
     case MARCHE_ERR_INVALID_ARG: return "MARCHE_ERR_INVALID_ARG";
     case MARCHE_ERR_UNSUPPORTED: return "MARCHE_ERR_UNSUPPORTED";
@@ -299,7 +311,7 @@ marche_status_t kv_cache_init(marche_kv_cache_t *cache, const marche_model_t *m,
 size_t marche_step_workspace_bytes(const marche_model_t *m, int32_t batch, int32_t a_total) {
   (void)batch;
   if (!m || a_total < 0) return 0;
-  const size_t es = elem_size(m->dtype);
+  const size_t es = elem_size(raw_enum(m->dtype));
   const size_t M = (size_t)a_total;
   return align256(M * sizeof(RowMap)) + 2 * align256(M * m->d_model * es) +
          align256(M * m->d_mlp * es);
@@ -320,7 +332,7 @@ marche_status_t marche::step_impl(const marche_model_t *m, const marche_layer_t 
   if (!cache || !cache->k || !cache->v) return fail(MARCHE_ERR_INVALID_ARG, "cache is NULL or unbound");
   if (cache->n_layers != m->n_layers || cache->n_heads != m->n_heads ||
       cache->n_tokens != m->n_tokens || cache->head_dim != m->head_dim ||
-      cache->dtype != m->dtype)
+      raw_enum(cache->dtype) != raw_enum(m->dtype))
     return fail(MARCHE_ERR_INVALID_ARG, "cache shape/dtype does not match the model");
   if (batch < 0 || batch > cache->batch)
     return fail(MARCHE_ERR_INVALID_ARG, "batch=%d outside [0, cache.batch=%d]", batch, cache->batch);
@@ -703,8 +715,8 @@ namespace {
 
 marche_status_t check_head(const marche_head_t *h) {
   if (!h) return fail(MARCHE_ERR_INVALID_ARG, "head is NULL");
-  if (h->dtype != MARCHE_F32 && h->dtype != MARCHE_BF16)
-    return fail(MARCHE_ERR_UNSUPPORTED, "head.dtype=%d is not F32 or BF16", h->dtype);
+  if (raw_enum(h->dtype) != MARCHE_F32 && raw_enum(h->dtype) != MARCHE_BF16)
+    return fail(MARCHE_ERR_UNSUPPORTED, "head.dtype=%d is not F32 or BF16", raw_enum(h->dtype));
   if (h->width < 256 || h->width % 256 != 0 || h->width > 4096)
     return fail(MARCHE_ERR_UNSUPPORTED, "head.width=%d (must be a multiple of 256, <= 4096)", h->width);
   if (h->d_cond < 256 || h->d_cond % 256 != 0 || h->d_cond > 4096)
