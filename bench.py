@@ -416,6 +416,156 @@ def e2e_main(args) -> int:
     return 0
 
 
+def single_block_main(args) -> int:
+    """The single-block fp32 case (one pre-LN block, D 768, 12 heads, N 320,
+    batch 1, 16 generating + 16 refresh tokens active): one cache-aware step
+    with the attention-mass scores, then the top-16 refresh selection over
+    the tokens outside A.  Latency per step (both calls), HIP events on the
+    launch stream, median of the timed repetitions; the fp64 oracle's same
+    step on this host's cores beside it."""
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_info
+
+    from paper_2506_12035_amd import binding, workload
+
+    cfg = workload.CONFIGS[1]
+    case = workload.single_block_case(cfg)
+    p = workload.layer_weights(cfg, 0)
+    N, D, H, dh, F = cfg.n_tokens, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_mlp
+    dev = "cuda"
+    model = binding.make_model(1, D, H, dh, F, N, binding.MARCHE_F32, cfg.ln_eps)
+    params = {k: torch.from_numpy(np.ascontiguousarray(v, np.float32)).to(dev) for k, v in p.items()}
+    layers = binding.make_layers([params])
+    k = torch.from_numpy(case.k_cache.reshape(-1)).to(dev)
+    v = torch.from_numpy(case.v_cache.reshape(-1)).to(dev)
+    cache = binding.kv_cache_init(model, 1, k, v, k.numel() * 4)
+    x0 = torch.from_numpy(case.x).to(dev)
+    x = x0.clone()
+    act = case.active[0].astype(np.int32)
+    a = len(act)
+    idx = torch.from_numpy(act).to(dev)
+    off = torch.tensor([0, a], dtype=torch.int32, device=dev)
+    gen = torch.tensor([case.n_gen], dtype=torch.int32, device=dev)
+    scores = torch.empty(1, H, N, device=dev)
+    wsb = binding.workspace_bytes(model, 1, a)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    out = torch.empty(case.k_top, dtype=torch.int32, device=dev)
+    ooff = torch.zeros(1, dtype=torch.int32, device=dev)
+    eoff = torch.tensor([0, a], dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        binding.marche_step(model, layers, cache, 0, 1, 1, x, idx, off, gen, a, a, case.n_gen,
+                            scores, 0, ws, wsb, stream=stream)
+        binding.select_refresh(scores, H, idx, eoff, 1, N, case.k_top, out, ooff, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    n = max(args.steps, 1)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    ev[0].record(stream)
+    for i in range(n):
+        step()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per = [ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(n)]
+    us = statistics.median(per)
+    # the step's kernels alone (library timing hooks), one pass
+    binding.profile_reset()
+    binding.profile_enable(True)
+    step()
+    torch.cuda.synchronize()
+    binding.profile_enable(False)
+    prof = binding.profile_collect()
+    kern_us = sum(e["ms"] for e in prof.values()) * 1e3
+    log(f"[bench] single block: {us:.1f} us per step (median of {n}), kernels {kern_us:.1f} us")
+
+    # fp64 oracle: the same step on this host
+    from oracle import block, select
+    p64 = {kk: np.asarray(vv, np.float64) for kk, vv in p.items()}
+    cpu = []
+    t_end = time.perf_counter() + args.cpu_budget_s
+    while not cpu or (time.perf_counter() < t_end and len(cpu) < 50):
+        t0 = time.perf_counter()
+        r = block.cache_aware_layer(p64, case.x[0], case.k_cache[0], case.v_cache[0], list(act),
+                                    list(act[:case.n_gen]), n_heads=H, eps=cfg.ln_eps, score=True)
+        select.select_topk(select.total_scores(r.scores), list(act), case.k_top)
+        cpu.append(time.perf_counter() - t0)
+    threads = sum(i.get("num_threads", 0) for i in threadpool_info() if i.get("user_api") == "blas")
+    weight_bytes = 4.0 * (3 * D * D + D * D + 2 * D * F)
+    res = {
+        "metric": "single-block cache-aware step + top-16 refresh latency (us)", "value": us,
+        "unit": "us", "higher_is_better": False, "n_gpus": 1, "steps": n, "warmup": args.warmup,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": cfg.name, "batch": 1, "n_tokens": N, "d_model": D, "n_heads": H,
+                   "active": a, "generating": case.n_gen, "top_k": case.k_top},
+        "kernels_us": {kk: vv["ms"] * 1e3 / vv["launches"] for kk, vv in prof.items()},
+        "kernel_sum_us": kern_us,
+        "weight_stream_bound_us": weight_bytes / (PEAK_HBM_GBS * 1e9) * 1e6,
+        "cpu_baseline": {"value": statistics.median(cpu) * 1e6, "unit": "us", "cores": threads,
+                         "kind": "oracle",
+                         "sample": f"fp64 oracle cache_aware_layer + select_topk, median of {len(cpu)}"},
+    }
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+def drift_main(args) -> int:
+    """A free-running generation of one image against the fp64 oracle (not a
+    parity gate): the GPU runs every step of the whole batch with its own
+    refresh sets; the oracle runs image 0's steps from the same seeded inputs
+    with its own.  Per step: the relative error of z (the last layer's rows
+    at the generating tokens) and how many of the oracle's refresh tokens the
+    GPU also chose."""
+    import numpy as np
+    import torch
+
+    from oracle import schedule as osched
+    from oracle import step as ostep
+    from paper_2506_12035_amd import driver, workload
+
+    cfg = workload.CONFIGS[args.config]
+    b = 0
+    weights = workload.all_weights(cfg)
+    eng = driver.Engine(cfg, weights=weights, micro_batches=args.micro_batches)
+    p64 = [{k: np.asarray(v, np.float64) for k, v in w.items()} for w in weights]
+    emb = workload.embeddings(cfg)
+    order = workload.orders(cfg)[b]
+    H, N, dh = cfg.n_heads, cfg.n_tokens, cfg.head_dim
+    kcs = [np.zeros((H, N, dh)) for _ in p64]
+    vcs = [np.zeros((H, N, dh)) for _ in p64]
+    rows = []
+    for t in range(cfg.n_steps):
+        eng.step(t)
+        torch.cuda.synchronize()
+        gen = osched.generating_tokens(order, cfg.n_buf, cfg.n_steps, t)
+        cache = osched.caching_tokens(order, cfg.n_buf, cfg.n_steps, t)
+        known = osched.known_before(order, cfg.n_buf, cfg.n_steps, t)
+        full = osched.is_full_step(t, cfg.full_every)
+        k = ostep.refresh_count("ratio", cfg.ratio_bp, N, len(gen), len(cache))
+        x_in = ostep.decoder_input(emb.cls[b], emb.value[b], emb.mask, emb.pos, known, cfg.n_buf)
+        res = ostep.marche_step(p64, x_in, kcs, vcs, gen, cache, n_heads=H, eps=cfg.ln_eps,
+                                sel_layer=cfg.sel_layer, full=full, k_refresh=k)
+        kcs, vcs = res.k_caches, res.v_caches
+        z_gpu = eng.x[b].cpu().numpy().astype(np.float64)[gen]
+        z_err = float(np.abs(z_gpu - res.z).max() / np.abs(res.z).max())
+        row = {"t": t, "full": full, "z_rel_err": z_err}
+        if not full:
+            r_gpu = set(int(v) for v in eng.refresh_lists(t)[b])
+            r_ora = set(res.refresh)
+            row["refresh_agree"] = len(r_gpu & r_ora) / max(len(r_ora), 1)
+        rows.append(row)
+        log(f"[drift] step {t:2d} {'full' if full else 'cache-aware'}: z rel err {z_err:.2e}"
+            + (f", refresh agreement {row['refresh_agree']:.3f}" if not full else ""))
+    agree = [r["refresh_agree"] for r in rows if "refresh_agree" in r]
+    print(json.dumps({"drift": rows, "workload": cfg.name, "image": b,
+                      "mean_refresh_agreement": statistics.mean(agree) if agree else None,
+                      "max_z_rel_err": max(r["z_rel_err"] for r in rows)}), flush=True)
+    return 0
+
+
 def ingest_main(args) -> int:
     from paper_2506_12035_amd import workload
 
@@ -474,6 +624,12 @@ def main() -> int:
                          "cache-aware decoder and the sampler (s/image), against full recompute "
                          "of the decoder with the same encoder and sampler")
     ap.add_argument("--e2e-config", default="mar-l-e2e", help="whole-model workload name")
+    ap.add_argument("--repeats", type=int, default=5,
+                    help="after the timed K steps, time the same K steps this many more times "
+                         "and report their median and spread beside the value (0: off)")
+    ap.add_argument("--drift", action="store_true",
+                    help="only run a free-running generation against the fp64 oracle for image "
+                         "0 (relative error of z and refresh-set agreement per step); not a gate")
     ap.add_argument("--ingest-counters", nargs=4, default=None,
                     metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="write profiles/traffic.json from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE "
@@ -505,6 +661,8 @@ def main() -> int:
         return appb_main(args)
     if args.e2e:
         return e2e_main(args)
+    if args.drift:
+        return drift_main(args)
     if args.calibrate_copy:
         n = args.calibrate_copy * (1 << 20) // 4
         src = torch.arange(n, dtype=torch.float32, device="cuda")
@@ -517,8 +675,7 @@ def main() -> int:
         return 0
     cfg = workload.CONFIGS[args.config]
     if args.config == 1:
-        print("the single-block case is a parity case, not a bench workload", file=sys.stderr)
-        return 2
+        return single_block_main(args)
     if args.ratio_bp is not None:
         cfg = cfg.with_(ratio_bp=args.ratio_bp)
     if args.full_every is not None:
@@ -550,6 +707,12 @@ def main() -> int:
     if ca_us:
         step_us["cache_aware"] = statistics.median(ca_us)
     log(f"[bench] {value:.2f} images/s, {wall / args.steps * 1e3:.3f} ms/step, {step_us}")
+    reps = []
+    for r_ in range(args.repeats):
+        # the same K steps again (the state of each step is rebuilt from its
+        # input; the work does not depend on the values)
+        rwall, _, _ = timed(eng, args.steps, first, T)
+        reps.append(B * args.steps / T / rwall)
 
     out = {
         "metric": METRIC, "value": value, "unit": "images/s", "n_gpus": 1,
@@ -566,6 +729,12 @@ def main() -> int:
                    "full_steps_in_schedule": sum(p.full for p in eng.plans)},
         "step_us": step_us,
     }
+    if reps:
+        out["repeats"] = {"n": len(reps), "median_images_per_s": statistics.median(reps),
+                          "min": min(reps), "max": max(reps),
+                          "note": "the same timed steps repeated after the value's timing"}
+        log(f"[bench] {len(reps)} repeats: median {statistics.median(reps):.2f} images/s "
+            f"({min(reps):.2f} - {max(reps):.2f})")
 
     if not args.no_full_recompute:
         eng.set_schedule(1, "ratio", 10000)

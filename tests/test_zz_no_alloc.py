@@ -30,9 +30,13 @@ class _State:
         self.layers = binding.make_layers(self.params)
         n_el = c.n_layers * B * c.n_heads * c.n_tokens * c.head_dim
         kv = rng.standard_normal((2, n_el), dtype=np.float32)
-        self.k = torch.from_numpy(kv[0]).to(torch.bfloat16).to(DEV)
-        self.v = torch.from_numpy(kv[1]).to(torch.bfloat16).to(DEV)
+        self.k = torch.empty(n_el, dtype=torch.bfloat16, device=DEV)
+        self.v = torch.empty(n_el, dtype=torch.bfloat16, device=DEV)
+        # bound without initial values the cache is zero-filled: the cached
+        # rows are written afterwards
         self.cache = binding.kv_cache_init(self.model, B, self.k, self.v, n_el * 2)
+        self.k.copy_(torch.from_numpy(kv[0]).to(torch.bfloat16))
+        self.v.copy_(torch.from_numpy(kv[1]).to(torch.bfloat16))
         self.x = torch.from_numpy(rng.standard_normal((B, c.n_tokens, c.d_model),
                                                       dtype=np.float32)).to(DEV)
         self.scores = torch.full((B, c.n_heads, c.n_tokens), float("nan"), device=DEV)
