@@ -113,16 +113,66 @@ def counter_rows(path: str) -> list:
     at the decoder-input kernel, launched once per step."""
     import csv
     rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Dispatch_Id"]))
+    out = []
+    for key, r in zip(dispatch_classes(rows), rows):
+        if key is not None:
+            out.append((key, float(r["Counter_Value"])))
+    return out
+
+
+# Classes that the library never times as cache-aware: the score pass runs at
+# the selection layer (every token active), the selection and the decoder
+# input outside the step; the row map has the same grid in both kinds of call.
+NOT_SPLIT = {"attn_scores", "select_topk", "decoder_input", "fill_zero", "row_map"}
+
+
+def dispatch_classes(rows: list) -> list:
+    """Timing class (split by layer kind) of each dispatch record, in order;
+    see counter_rows."""
     starts = [i for i, r in enumerate(rows) if "decoder_input_kernel" in r["Kernel_Name"]]
     step0_end = starts[1] if len(starts) > 1 else len(rows)
     full = {(counter_class(r["Kernel_Name"]), r["Grid_Size"]) for r in rows[:step0_end]}
     out = []
     for r in rows:
         c = counter_class(r["Kernel_Name"])
-        if c is None:
+        if c is None or c in NOT_SPLIT or (c, r["Grid_Size"]) in full:
+            out.append(c)
+        else:
+            out.append(c + "_ca")
+    return out
+
+
+def ingest_mfma(path: str, simds: int, xcds: int) -> dict:
+    """MFMA utilisation per timing class from a rocprofv3 --pmc run of
+    SQ_VALU_MFMA_BUSY_CYCLES, GRBM_GUI_ACTIVE and SQ_BUSY_CU_CYCLES over the
+    bench's first steps: per dispatch, MFMA-busy cycles summed over the SIMDs
+    / (GPU-active cycles x SIMDs), averaged over the class's dispatches (the
+    MfmaUtil metric of rocprofv3).  The CSV sums GRBM_GUI_ACTIVE over the
+    XCDs, each of which counts the whole dispatch, so it is divided by their
+    number (the metric takes the maximum instead)."""
+    import collections
+    import csv
+    per = collections.defaultdict(dict)
+    first = {}
+    for r in csv.DictReader(open(path)):
+        d = int(r["Dispatch_Id"])
+        per[d][r["Counter_Name"]] = float(r["Counter_Value"])
+        first.setdefault(d, r)
+    order = sorted(per)
+    keys = dispatch_classes([first[d] for d in order])
+    agg = collections.defaultdict(list)
+    for d, key in zip(order, keys):
+        c = per[d]
+        if key is None or not c.get("GRBM_GUI_ACTIVE"):
             continue
-        key = c if (c, r["Grid_Size"]) in full else c + "_ca"
-        out.append((key, float(r["Counter_Value"])))
+        active = c["GRBM_GUI_ACTIVE"] / xcds
+        agg[key].append((c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (active * simds),
+                         c.get("SQ_BUSY_CU_CYCLES", 0.0), active))
+    out = {}
+    for key, v in sorted(agg.items()):
+        out[key] = {"mfma_util": sum(u for u, _, _ in v) / len(v), "dispatches": len(v),
+                    "gpu_active_cycles": sum(g for _, _, g in v) / len(v),
+                    "source_sha": source_hash(key)}
     return out
 
 
@@ -566,6 +616,41 @@ def drift_main(args) -> int:
     return 0
 
 
+def trace_summary_main(args) -> int:
+    """Markdown summary of a rocprofv3 --kernel-trace run of the default bench
+    (kernel_trace.csv and the run's stderr+stdout with its JSON line): per
+    timing class, the trace's average duration over the dispatches of the
+    instrumented pass (the class's last `launches` dispatches, the pass being
+    the last kernels the bench launches) beside the live HIP-event average of
+    the same launches, and the whole trace's totals."""
+    import csv
+    import collections
+    trace_csv, log_path = args.trace_summary
+    rows = sorted(csv.DictReader(open(trace_csv)), key=lambda r: int(r["Dispatch_Id"]))
+    for r in rows:
+        r["Grid_Size"] = r["Grid_Size_X"]
+    keys = dispatch_classes(rows)
+    dur = collections.defaultdict(list)
+    for k, r in zip(keys, rows):
+        if k is not None:
+            dur[k].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    line = [ln for ln in open(log_path) if ln.startswith("{")][-1]
+    live = json.loads(line)
+    kern = live.get("kernels", {})
+    dom = live.get("roofline", {}).get("kernel")
+    out = ["| Class | Live launches | Live avg us | Trace avg us (same launches) | Trace dispatches | Trace total ms |",
+           "|---|---:|---:|---:|---:|---:|"]
+    for k, v in sorted(kern.items(), key=lambda kv: -kv[1]["total_ms"]):
+        d = dur.get(k, [])
+        n = v["launches"]
+        tail = d[-n:] if len(d) >= n else d
+        tavg = sum(tail) / len(tail) if tail else float("nan")
+        mark = " (dominant)" if k == dom else ""
+        out.append(f"| {k}{mark} | {n} | {v['avg_us']:.1f} | {tavg:.1f} | {len(d)} | {sum(d) / 1e3:.2f} |")
+    print("\n".join(out))
+    return 0
+
+
 def ingest_main(args) -> int:
     from paper_2506_12035_amd import workload
 
@@ -630,6 +715,13 @@ def main() -> int:
     ap.add_argument("--drift", action="store_true",
                     help="only run a free-running generation against the fp64 oracle for image "
                          "0 (relative error of z and refresh-set agreement per step); not a gate")
+    ap.add_argument("--trace-summary", nargs=2, default=None, metavar=("TRACE_CSV", "BENCH_LOG"),
+                    help="print a markdown table of a rocprofv3 --kernel-trace run of the bench "
+                         "against the live timing of the same launches; no GPU needed")
+    ap.add_argument("--ingest-mfma", default=None, metavar="MFMA_CSV",
+                    help="write profiles/mfma_util.json from a rocprofv3 --pmc run of "
+                         "SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_BUSY_CU_CYCLES over the "
+                         "first steps (--steps 1 --warmup 1); no GPU needed")
     ap.add_argument("--ingest-counters", nargs=4, default=None,
                     metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="write profiles/traffic.json from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE "
@@ -638,6 +730,23 @@ def main() -> int:
     args = ap.parse_args()
     if args.ingest_counters:
         return ingest_main(args)
+    if args.trace_summary:
+        return trace_summary_main(args)
+    if args.ingest_mfma:
+        from paper_2506_12035_amd import workload
+        import csv as _csv
+        agent = args.ingest_mfma.replace("counter_collection", "agent_info")
+        gpu = [r for r in _csv.DictReader(open(agent)) if r["Agent_Type"] == "GPU"][0]
+        simds, xcds = int(gpu["Simd_Count"]), int(gpu["Num_Xcc"])
+        rec = {"simds": simds, "xcds": xcds,
+               "classes": ingest_mfma(args.ingest_mfma, simds, xcds)}
+        path = os.path.join(ROOT, "profiles", "mfma_util.json")
+        allrec = json.load(open(path)) if os.path.exists(path) else {}
+        allrec[workload.CONFIGS[args.config].name] = rec
+        with open(path, "w") as f:
+            json.dump(allrec, f, indent=1, sort_keys=True)
+        print(json.dumps(rec, indent=1))
+        return 0
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
