@@ -286,6 +286,213 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(AttnArgs a, int chun
   }
 }
 
+// ------------------------------------------------------------ cache-aware kernel, head width 64
+//
+// Cache-aware layers at head width 64 with every key tile whole (N a multiple
+// of 64): one workgroup per (image, head, chunk of QB*32 active queries), one
+// wavefront per 32 queries over all keys.  Key tiles (64 keys of K and of V,
+// 16 KB) go global -> registers -> one of two LDS slots, row-major: no
+// transposition on the way.  The MFMA operand V^T (32 head dims x 16 keys per
+// lane group) comes from the transposing LDS read of gfx950 (ds_read_tr16_b64:
+// within 16 lanes, lane 4e + q names row e and four consecutive columns
+// 4q..4q+3 of a 4 x 16 block, and lane i receives column i of the four rows).
+// K and V tiles permute the 16-byte chunks of a row by an XOR with the
+// bit-reversed row-pair index, so a K fragment read (16 rows at one chunk)
+// and a V^T read (4 rows x 4 chunks per 32 lanes) each touch every bank group
+// once.  Only registers stage the next tile, so a workgroup needs 32 KB of
+// LDS and five fit on a compute unit: at MAR-L sizes every (image, head) of a
+// call is resident at once, each with one tile in flight.
+namespace strm {
+
+constexpr int kSlotBytes = 16384;  // 64 keys x 64 dims x 2 bytes, K then V
+
+// Chunk permutation of row r: the row-pair index (r >> 1) & 7, bit-reversed.
+__device__ __forceinline__ int swz(int r) {
+  const int x = (r >> 1) & 7;
+  return ((x & 1) << 2) | (x & 2) | (x >> 2);
+}
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// Transposing read of four consecutive keys for this lane's head dim (see above).
+__device__ __forceinline__ s16x4 read_tr(const unsigned char *p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (s16x4 __attribute__((address_space(3))) *)(
+          (__attribute__((address_space(3))) unsigned char *)(uintptr_t)p));
+}
+
+// One 64-key tile of the online softmax for this wavefront's 32 queries
+// (lane -> query lane & 31), in the log2 domain, as attn_tile does for the
+// transposed-V layouts: S^T = K Q^T, running max over the raw logits, the
+// scale folded into the exponent, O^T += V^T P^T.
+__device__ __forceinline__ void tile(const unsigned char *slot, const bf16x8 (&qf)[4],
+                                     f32x16 (&acc)[2], float &m_run, float &l_run, float sl2,
+                                     int lane) {
+  const unsigned char *kt = slot, *vt = slot + 8192;
+  f32x16 s[2];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    s[kb] = f32x16{};
+    const int row = kb * 32 + (lane & 31);
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      const int c = st * 2 + (lane >> 5);
+      const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(kt + row * 128 + ((c ^ swz(row)) << 4));
+      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[st], s[kb], 0, 0, 0);
+    }
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  const float m_new = fmaxf(m_run, mx * sl2);
+  const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+  float psum = 0.f;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], sl2, -m_new));
+      s[kb][r] = p;
+      psum += p;
+    }
+  l_run = l_run * alpha + psum;
+  m_run = m_new;
+  acc[0] *= alpha;
+  acc[1] *= alpha;
+
+  // V^T operand rows: lane group g = lane / 16 reads rows kbase + e (e = its
+  // source lane's (lane & 15) / 4) at head dims d0 + 4 (lane & 3) .. + 3
+  const int g = lane >> 4, e = (lane & 15) >> 2, q = lane & 3;
+  const int hf = lane >> 5;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      // P^T: lane half hf holds keys 16u + 4hf + 0..3 and 16u + 8 + 4hf + 0..3
+      // of the 32-key block in s[kb][8u .. 8u + 7]
+      bf16x8 pb;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) pb[j] = (bf16)s[kb][8 * u + j];
+#pragma unroll
+      for (int db = 0; db < 2; ++db) {
+        const int c = db * 4 + (g & 1) * 2 + (q >> 1);  // logical 16-byte chunk
+        s16x4 lo, hi;
+        {
+          const int row = kb * 32 + u * 16 + 4 * hf + e;
+          lo = read_tr(vt + row * 128 + ((c ^ swz(row)) << 4) + (q & 1) * 8);
+        }
+        {
+          const int row = kb * 32 + u * 16 + 8 + 4 * hf + e;
+          hi = read_tr(vt + row * 128 + ((c ^ swz(row)) << 4) + (q & 1) * 8);
+        }
+        const s16x4 v8[2] = {lo, hi};
+        const bf16x8 va = *reinterpret_cast<const bf16x8 *>(v8);
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, acc[db], 0, 0, 0);
+      }
+    }
+}
+
+}  // namespace strm
+
+// DEPTH register sets of the next tiles (1 or 2) per lane.
+template <int QB, int DEPTH>
+__global__ __launch_bounds__(QB * 64) void attn_reg_kernel(AttnArgs a, int chunks) {
+  using namespace strm;
+  constexpr int NT = QB * 64;
+  constexpr int CPL = 1024 / NT;  // 16-byte chunks per lane per tile (K and V)
+  static_assert(DEPTH == 1 || DEPTH == 2, "register sets in flight");
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * kSlotBytes];
+
+  const int id = xcd_remap(blockIdx.x, gridDim.x);
+  const int bh = id / chunks, chunk = id - bh * chunks;
+  const int b = bh / a.n_heads, h = bh - b * a.n_heads;
+  const int r0 = a.a_off ? a.a_off[b] : b * a.a_max;
+  const int na = a.a_off ? a.a_off[b + 1] - r0 : a.a_max;
+  const int q0 = chunk * QB * 32;
+  if (q0 >= na) return;  // uniform over the workgroup
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int N = a.n_tokens, D = a.d_model, nt = N / TK;
+  const bf16 *kg = static_cast<const bf16 *>(a.k_cache) + (size_t)bh * N * 64;
+  const bf16 *vg = static_cast<const bf16 *>(a.v_cache) + (size_t)bh * N * 64;
+
+  const int qi = q0 + wave * 32 + (lane & 31);
+  const bf16 *qrow = static_cast<const bf16 *>(a.q) + (size_t)(r0 + min(qi, na - 1)) * D + h * 64;
+  bf16x8 qf[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    qf[s] = *reinterpret_cast<const bf16x8 *>(qrow + s * 16 + (lane >> 5) * 8);
+
+  // Chunk j of a tile (j = i * NT + tid): matrix j / 512 (K, V), row (j % 512)
+  // / 8, logical chunk j % 8; coalesced in global memory, permuted in LDS.
+  // Every load is unconditional (a tile index past the last repeats the last
+  // tile, which the L2 still holds), so the waits the compiler places count
+  // exactly the loads issued after the ones a store needs.
+  u32x4 rt[DEPTH][CPL];
+  auto gload = [&](u32x4 (&r)[CPL], int t) {
+    const size_t off = (size_t)min(t, nt - 1) * TK * 64;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      const int j = i * NT + tid;
+      r[i] = *reinterpret_cast<const u32x4 *>((j < 512 ? kg : vg) + off + (j & 511) * 8);
+    }
+  };
+  auto sstore = [&](const u32x4 (&r)[CPL], int buf) {
+    unsigned char *slot = smem + buf * kSlotBytes;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      const int j = i * NT + tid;
+      const int row = (j & 511) >> 3, c = j & 7;
+      *reinterpret_cast<u32x4 *>(slot + (j >> 9) * 8192 + row * 128 + ((c ^ swz(row)) << 4)) = r[i];
+    }
+  };
+
+  const float sl2 = 1.4426950408889634f / 8.0f;  // log2(e) / sqrt(64)
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x16 acc[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+  for (int d = 0; d < DEPTH; ++d) gload(rt[d], d);
+  sstore(rt[0], 0);
+  __syncthreads();
+  // Tile t is in LDS slot t & 1 and its register set t % DEPTH is free again:
+  // it takes tile t + DEPTH while tile t computes; tile t + 1 then goes from
+  // its register set into the other slot.
+  // The scheduling barriers keep the stores of the next tile (and the waits
+  // for its loads) behind the whole tile step, which would otherwise start
+  // them, and wait, in the middle of it.
+  auto step = [&](int t, u32x4 (&r_free)[CPL], const u32x4 (&r_next)[CPL]) {
+    gload(r_free, t + DEPTH);
+    __builtin_amdgcn_sched_barrier(0);
+    tile(smem + (t & 1) * kSlotBytes, qf, acc, m_run, l_run, sl2, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    sstore(r_next, (t + 1) & 1);
+    __syncthreads();
+  };
+  int t = 0;
+  for (; t + DEPTH <= nt; t += DEPTH) {
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) step(t + d, rt[d], rt[(d + 1) % DEPTH]);
+  }
+  if (DEPTH == 2 && t < nt) step(t, rt[0], rt[1 % DEPTH]);
+
+  const float inv = 1.0f / (l_run + __shfl_xor(l_run, 32, 64));
+  if (qi < na) {
+    bf16 *orow = static_cast<bf16 *>(a.o) + (size_t)(r0 + qi) * D + h * 64;
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        const int dh0 = db * 32 + gq * 8 + (lane >> 5) * 4;
+        bf16x4 pk = {(bf16)(acc[db][4 * gq + 0] * inv), (bf16)(acc[db][4 * gq + 1] * inv),
+                     (bf16)(acc[db][4 * gq + 2] * inv), (bf16)(acc[db][4 * gq + 3] * inv)};
+        *reinterpret_cast<bf16x4 *>(orow + dh0) = pk;
+      }
+  }
+}
+
 // Every query of an image in one workgroup and every key resident in LDS
 // (layers where all N <= NTL * 64 tokens are active): one workgroup per
 // (image, head); wavefront w owns the NQB 32-query blocks w, w + NW, ...  All
@@ -455,8 +662,27 @@ static hipError_t run_attn_mfma(const AttnArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// The register-staged kernel of head width 64 for one key segment of whole
+// tiles (at least three).
+bool attn_streams(int32_t head_dim, int32_t n_tokens, bool two_segments) {
+  return head_dim == 64 && !two_segments && n_tokens % TK == 0 && n_tokens >= 3 * TK;
+}
+
+constexpr int REG_DEPTH = 1;
+template <int QB>
+static hipError_t run_attn_reg(const AttnArgs &a, hipStream_t s) {
+  const int chunks = (a.a_max + QB * 32 - 1) / (QB * 32);
+  attn_reg_kernel<QB, REG_DEPTH><<<a.batch * a.n_heads * chunks, QB * 64, 0, s>>>(a, chunks);
+  return hipGetLastError();
+}
+
 template <int DH, bool SEG2>
 static hipError_t attn_bf16_nw(const AttnArgs &a, hipStream_t s) {
+  if (attn_streams(DH, a.n_tokens, SEG2)) {
+    if (a.a_max <= 32) return run_attn_reg<1>(a, s);
+    if (a.a_max <= 64) return run_attn_reg<2>(a, s);
+    return run_attn_reg<4>(a, s);
+  }
   if (a.a_max <= 32) return run_attn_mfma<DH, 1, SEG2>(a, s);
   if (a.a_max <= 64) return run_attn_mfma<DH, 2, SEG2>(a, s);
   return run_attn_mfma<DH, 4, SEG2>(a, s);
