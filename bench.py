@@ -27,6 +27,7 @@ import hashlib
 import json
 import os
 import statistics
+import re
 import sys
 import time
 
@@ -90,7 +91,14 @@ def counter_class(name: str):
             if key in name:
                 return f"gemm_{cls}_{tile}"
     if "attn_resident_kernel" in name:
-        return "attention_res"
+        # the last template argument: the score pass of the selection layer
+        scores = re.search(r"attn_resident_kernel<[^>]*, true>", name) is not None or \
+            "ELb1EEEv" in name
+        return "attention_res_scores" if scores else "attention_res"
+    if "attn_reg_kernel" in name:
+        for qb, q in (("4", "q128"), ("2", "q64"), ("1", "q32")):
+            if f"attn_reg_kernelILi{qb}E" in name or f"attn_reg_kernel<{qb}," in name:
+                return f"attention_{q}"
     if "attn_mfma_kernel" in name:
         for nw, q in (("4", "q128"), ("2", "q64"), ("1", "q32")):
             if f"ELi{nw}ELb" in name or f"ELi{nw}EEEv" in name or f", {nw}, " in name:
@@ -123,7 +131,8 @@ def counter_rows(path: str) -> list:
 # Classes that the library never times as cache-aware: the score pass runs at
 # the selection layer (every token active), the selection and the decoder
 # input outside the step; the row map has the same grid in both kinds of call.
-NOT_SPLIT = {"attn_scores", "select_topk", "decoder_input", "fill_zero", "row_map"}
+NOT_SPLIT = {"attn_scores", "attention_res_scores", "select_topk", "decoder_input", "fill_zero",
+             "row_map"}
 
 
 def dispatch_classes(rows: list) -> list:

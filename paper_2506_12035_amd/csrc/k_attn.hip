@@ -502,7 +502,17 @@ __global__ __launch_bounds__(QB * 64) void attn_reg_kernel(AttnArgs a, int chunk
 // no further loads or barriers.  With SWZ (head width 64) the tiles take
 // 80 KB, so two workgroups share a CU and one's loads overlap the other's
 // arithmetic.
-template <int DH, int NW, int NTL, int NQB, bool SWZ>
+//
+// SCORES (the selection layer, Section 4.2): the kernel also writes the
+// attention mass each key receives from the image's generating rows (its
+// first n_gen[b] active rows), a.scores[b][h][j] = sum over those rows i of
+// softmax_j(q_i . k_j / sqrt(d_h)), from the K tiles it holds.  Each
+// wavefront keeps the final row maximum and normaliser of its generating
+// rows; once every wavefront is done with the V tiles, those go to LDS in
+// their place, and the wavefronts split the key tiles: for each key, S = Q
+// K^T over the generating rows (one lane per key), the probabilities with
+// the final statistics, summed over the rows in a fixed order.
+template <int DH, int NW, int NTL, int NQB, bool SWZ, bool SCORES = false>
 __global__ __launch_bounds__(NW * 64) void attn_resident_kernel(AttnArgs a) {
   constexpr int NT = NW * 64;
   constexpr int ODB = (DH + 31) / 32;
@@ -605,10 +615,18 @@ __global__ __launch_bounds__(NW * 64) void attn_resident_kernel(AttnArgs a) {
   __syncthreads();
 
   const float sl2 = 1.4426950408889634f / sqrtf((float)DH);
+  const int n_gen = SCORES ? a.n_gen[b] : 0;
+  // final statistics of this wavefront's blocks (generating rows only)
+  float st_m[NQB], st_inv[NQB];
+#pragma unroll
+  for (int qb = 0; qb < NQB; ++qb) {
+    st_m[qb] = INFINITY;
+    st_inv[qb] = 0.f;
+  }
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb) {
     const int wq0 = (qb * NW + wave) * 32;
-    if (wq0 >= na) break;  // uniform over the wavefront; no barrier follows
+    if (wq0 >= na) break;  // uniform over the wavefront; no barrier inside the loop
     const int qi = wq0 + (lane & 31);
     const bf16x8 (&qf)[QS] = qall[qb];
     float m_run = -INFINITY, l_run = 0.f;
@@ -623,6 +641,10 @@ __global__ __launch_bounds__(NW * 64) void attn_resident_kernel(AttnArgs a) {
 
     const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
     const float inv = 1.0f / l_tot;
+    if (SCORES && qi < n_gen) {
+      st_m[qb] = m_run;
+      st_inv[qb] = inv;
+    }
     if (qi < na) {
       bf16 *orow = static_cast<bf16 *>(a.o) + (size_t)(r0 + qi) * D + h * DH;
 #pragma unroll
@@ -638,6 +660,66 @@ __global__ __launch_bounds__(NW * 64) void attn_resident_kernel(AttnArgs a) {
         }
     }
   }
+  if constexpr (SCORES) {
+    // statistics of generating row i at st_mx[i], st_iv[i], in the V tiles'
+    // place; rows at or past n_gen read maximum +inf and normaliser 0, so
+    // their probabilities are exactly 0
+    const int gb_n = (n_gen + 31) / 32;  // blocks with generating rows
+    float *st_mx = reinterpret_cast<float *>(&Vt[0][0]);
+    float *st_iv = st_mx + NQB * NW * 32;
+    static_assert(2 * NQB * NW * 32 * 4 <= (int)sizeof(Vt), "statistics fit the V tiles");
+    __syncthreads();  // every wavefront is done with the V tiles
+#pragma unroll
+    for (int qb = 0; qb < NQB; ++qb) {
+      const int row = (qb * NW + wave) * 32 + (lane & 31);
+      if (lane < 32 && row < gb_n * 32) {
+        st_mx[row] = st_m[qb];
+        st_iv[row] = st_inv[qb];
+      }
+    }
+    __syncthreads();
+    const int hf = lane >> 5;
+    for (int t = wave; t < ntiles; t += NW) {
+      float sc[2] = {0.f, 0.f};  // keys t*64 + kb*32 + (lane & 31), this lane's half of the rows
+      for (int gb = 0; gb < gb_n; ++gb) {
+        const int qi = gb * 32 + (lane & 31);
+        const bf16 *qrow =
+            static_cast<const bf16 *>(a.q) + (size_t)(r0 + min(qi, na - 1)) * D + h * DH;
+        bf16x8 qf[QS];
+#pragma unroll
+        for (int st = 0; st < QS; ++st)
+          qf[st] = *reinterpret_cast<const bf16x8 *>(qrow + st * 16 + hf * 8);
+        // rows of register r: gb*32 + 8 (r / 4) + 4 hf + r % 4
+        f32x4 mx[4], iv[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          mx[g] = *reinterpret_cast<const f32x4 *>(st_mx + gb * 32 + 8 * g + 4 * hf);
+          iv[g] = *reinterpret_cast<const f32x4 *>(st_iv + gb * 32 + 8 * g + 4 * hf);
+        }
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          f32x16 s = f32x16{};
+#pragma unroll
+          for (int st = 0; st < QS; ++st) {
+            const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(
+                &Ks[t][k_off<DH, SWZ>(kb * 32 + (lane & 31), st * 16 + hf * 8)]);
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[st], ka, s, 0, 0, 0);
+          }
+          float part = 0.f;
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            part += __builtin_amdgcn_exp2f(fmaf(s[r], sl2, -mx[r >> 2][r & 3])) * iv[r >> 2][r & 3];
+          sc[kb] += part;
+        }
+      }
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const float tot = sc[kb] + __shfl_xor(sc[kb], 32, 64);
+        const int key = t * TK + kb * 32 + (lane & 31);
+        if (lane < 32 && key < N) a.scores[(size_t)bh * N + key] = tot;
+      }
+    }
+  }
 }
 
 constexpr int RES_NTL = 5;    // keys resident: 320
@@ -648,6 +730,10 @@ constexpr int RES_QMAX = 320; // queries per workgroup
 // of them and all keys within one workgroup's reach, one key segment.
 bool attn_resident(int32_t a_max, int32_t n_tokens, bool two_segments) {
   return !two_segments && a_max > 64 && a_max <= RES_QMAX && n_tokens <= RES_NTL * TK;
+}
+
+bool attn_fuses_scores(int32_t a_max, int32_t n_tokens) {
+  return attn_resident(a_max, n_tokens, false);
 }
 
 template <int DH, int NW, bool SEG2>
@@ -692,10 +778,14 @@ template <int DH>
 static hipError_t attn_bf16_dispatch(const AttnArgs &a, hipStream_t s) {
   if (a.k2) return attn_bf16_nw<DH, true>(a, s);
   if (attn_resident(a.a_max, a.n_tokens, a.k2 != nullptr)) {
-    if constexpr (DH == 64)  // 80 KB of swizzled tiles: two workgroups per CU
-      attn_resident_kernel<DH, 4, RES_NTL, 3, true><<<a.batch * a.n_heads, 4 * 64, 0, s>>>(a);
-    else
-      attn_resident_kernel<DH, 10, RES_NTL, 1, false><<<a.batch * a.n_heads, 10 * 64, 0, s>>>(a);
+    const int grid = a.batch * a.n_heads;
+    if constexpr (DH == 64) {  // 80 KB of swizzled tiles: two workgroups per CU
+      if (a.scores) attn_resident_kernel<DH, 4, RES_NTL, 3, true, true><<<grid, 4 * 64, 0, s>>>(a);
+      else attn_resident_kernel<DH, 4, RES_NTL, 3, true><<<grid, 4 * 64, 0, s>>>(a);
+    } else {
+      if (a.scores) attn_resident_kernel<DH, 10, RES_NTL, 1, false, true><<<grid, 10 * 64, 0, s>>>(a);
+      else attn_resident_kernel<DH, 10, RES_NTL, 1, false><<<grid, 10 * 64, 0, s>>>(a);
+    }
     return hipGetLastError();
   }
   return attn_bf16_nw<DH, false>(a, s);

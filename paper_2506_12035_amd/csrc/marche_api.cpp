@@ -116,6 +116,7 @@ enum KClass {
   K_HEAD_GATE_MOD, K_HEAD_OUT_STEP, K_GEMM_QKV_S, K_GEMM_O_S, K_GEMM_FC1_S, K_GEMM_FC2_S,
   K_GEMM_EMBED_S, K_GEMM_HEAD_S, K_GEMM_HEAD_SILU_S, K_TRANSPOSE, K_GEMM_QKV_M, K_GEMM_O_M,
   K_GEMM_FC1_M, K_GEMM_FC2_M, K_GEMM_EMBED_M, K_GEMM_HEAD_M, K_GEMM_HEAD_SILU_M,
+  K_ATTN_RES_SC,
   K_NCLASS
 };
 const char *const kClassNames[K_NCLASS] = {
@@ -131,7 +132,7 @@ const char *const kClassNames[K_NCLASS] = {
     "gemm_qkv_t64x128",  "gemm_o_t64x128", "gemm_fc1_t64x128",  "gemm_fc2_t64x128",
     "gemm_embed_t64x128", "gemm_head_t64x128", "gemm_head_silu_t64x128", "transpose",
     "gemm_qkv_t128",     "gemm_o_t128",    "gemm_fc1_t128",     "gemm_fc2_t128",
-    "gemm_embed_t128",   "gemm_head_t128", "gemm_head_silu_t128"};
+    "gemm_embed_t128",   "gemm_head_t128", "gemm_head_silu_t128", "attention_res_scores"};
 static_assert(sizeof(kClassNames) / sizeof(kClassNames[0]) == K_NCLASS, "one name per class");
 
 // Launches inside marche_step in layers where not every token of every image
@@ -434,11 +435,24 @@ marche_status_t marche::step_impl(const marche_model_t *m, const marche_layer_t 
            launch_gemm_qkv(dt, buf0, L.w_qkv, static_cast<const float *>(L.b_qkv), M, 3 * D, D,
                            map, qo, stream));
     AttnArgs aa{buf1, kc, vc, buf0, a_off, map, batch, H, N, dh, D, M, a_max};
+    // At the selection layer the resident attention kernel also writes the
+    // score pass (Section 4.2) from the K tiles it holds; other sizes run the
+    // score pass as a kernel of its own after the attention.
+    const bool sel = want_scores && l == score_layer;
+    const bool fused = sel && dt == DType::BF16 && attn_fuses_scores(a_max, N);
+    if (fused) {
+      aa.n_gen = n_gen;
+      aa.scores = scores;
+    }
     // Algorithmic traffic: every cached K/V element of the batch read once,
-    // plus the queries read and the outputs written.
-    LAUNCH(attn_class(dt, a_max, N) + ko, 4.0 * M * N * D, es * (2.0 * batch * N * D + 2.0 * M * D),
+    // plus the queries read and the outputs written (and the scores).
+    LAUNCH((fused ? K_ATTN_RES_SC : attn_class(dt, a_max, N)) + ko,
+           4.0 * M * N * D + (fused ? 2.0 * batch * gen_max * N * D : 0.0),
+           es * (2.0 * batch * N * D + 2.0 * M * D) + (fused ? 4.0 * batch * H * N : 0.0),
            launch_attention(dt, aa, stream));
-    if (want_scores && l == score_layer) {
+    aa.n_gen = nullptr;
+    aa.scores = nullptr;
+    if (sel && !fused) {
       LAUNCH(K_ATTN_SCORES + ko, 2.0 * batch * gen_max * N * D,
              es * (double)batch * N * D + 4.0 * batch * H * N,
              launch_attn_scores(dt, aa, n_gen, gen_max, scores, stream));

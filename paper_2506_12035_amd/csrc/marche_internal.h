@@ -140,11 +140,19 @@ struct AttnArgs {
   const void *k2 = nullptr;
   const void *v2 = nullptr;
   int32_t n2 = 0;
+  // Optional attention mass of the generating rows (the first n_gen[b] rows
+  // of image b), scores[b][h][j], written by the same kernel where
+  // attn_fuses_scores() holds (one key segment).
+  const int32_t *n_gen = nullptr;
+  float *scores = nullptr;
 };
 hipError_t launch_attention(DType dt, const AttnArgs &a, hipStream_t s);
 // Whether bf16 attention with these sizes runs the resident-K/V kernel (one
 // workgroup per (image, head)).
 bool attn_resident(int32_t a_max, int32_t n_tokens, bool two_segments);
+// Whether bf16 attention with these sizes can write the score pass itself
+// (the resident kernel: every key of a head in LDS).
+bool attn_fuses_scores(int32_t a_max, int32_t n_tokens);
 // dst[b][h] = [a[b][h] (na rows) ; c[b][h] (nc rows)], rows of dh elements, for
 // K and V: the concatenation of the active and cached segments.
 hipError_t launch_concat_kv(DType dt, void *k_dst, void *v_dst, const void *k_a, const void *v_a,
