@@ -2,6 +2,8 @@
 // 64-lane wavefronts).
 #pragma once
 
+#include <hip/hip_ext.h>
+
 #include "marche_internal.h"
 
 namespace marche {
@@ -65,6 +67,22 @@ __device__ __forceinline__ float to_f32(T v) { return (float)v; }
 __device__ __forceinline__ int xcd_remap(int wg, int n_wg) {
   if (n_wg % 8 != 0) return wg;
   return (wg % 8) * (n_wg / 8) + wg / 8;
+}
+
+// Launch of a kernel of this library: when a timed call is in progress on
+// this thread (kernel_events()), its events go with the dispatch of the
+// call's first kernel.
+template <typename... KArgs, typename... Args>
+inline void launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block, uint32_t lds,
+                          hipStream_t s, Args... args) {
+  KernelEvents *ev = kernel_events();
+  if (ev && !ev->used) {
+    ev->used = true;
+    hipExtLaunchKernelGGL(kernel, grid, block, lds, s, ev->start, ev->stop, 0,
+                          static_cast<KArgs>(args)...);
+  } else {
+    kernel<<<grid, block, lds, s>>>(static_cast<KArgs>(args)...);
+  }
 }
 
 }  // namespace marche

@@ -742,9 +742,9 @@ static hipError_t run_attn_mfma(const AttnArgs &a, hipStream_t s) {
   const int grid = a.batch * a.n_heads * chunks;
   const bool aligned = a.n_tokens % TK == 0 && (!SEG2 || a.n2 % TK == 0);
   if (aligned)
-    attn_mfma_kernel<DH, NW, SEG2, true><<<grid, NW * 64, 0, s>>>(a, chunks);
+    launch_kernel(attn_mfma_kernel<DH, NW, SEG2, true>, grid, NW * 64, 0, s, a, chunks);
   else
-    attn_mfma_kernel<DH, NW, SEG2, false><<<grid, NW * 64, 0, s>>>(a, chunks);
+    launch_kernel(attn_mfma_kernel<DH, NW, SEG2, false>, grid, NW * 64, 0, s, a, chunks);
   return hipGetLastError();
 }
 
@@ -758,7 +758,8 @@ constexpr int REG_DEPTH = 1;
 template <int QB>
 static hipError_t run_attn_reg(const AttnArgs &a, hipStream_t s) {
   const int chunks = (a.a_max + QB * 32 - 1) / (QB * 32);
-  attn_reg_kernel<QB, REG_DEPTH><<<a.batch * a.n_heads * chunks, QB * 64, 0, s>>>(a, chunks);
+  launch_kernel(attn_reg_kernel<QB, REG_DEPTH>, a.batch * a.n_heads * chunks, QB * 64, 0, s,
+                a, chunks);
   return hipGetLastError();
 }
 
@@ -780,11 +781,16 @@ static hipError_t attn_bf16_dispatch(const AttnArgs &a, hipStream_t s) {
   if (attn_resident(a.a_max, a.n_tokens, a.k2 != nullptr)) {
     const int grid = a.batch * a.n_heads;
     if constexpr (DH == 64) {  // 80 KB of swizzled tiles: two workgroups per CU
-      if (a.scores) attn_resident_kernel<DH, 4, RES_NTL, 3, true, true><<<grid, 4 * 64, 0, s>>>(a);
-      else attn_resident_kernel<DH, 4, RES_NTL, 3, true><<<grid, 4 * 64, 0, s>>>(a);
+      if (a.scores)
+        launch_kernel(attn_resident_kernel<DH, 4, RES_NTL, 3, true, true>, grid, 4 * 64, 0, s, a);
+      else
+        launch_kernel(attn_resident_kernel<DH, 4, RES_NTL, 3, true>, grid, 4 * 64, 0, s, a);
     } else {
-      if (a.scores) attn_resident_kernel<DH, 10, RES_NTL, 1, false, true><<<grid, 10 * 64, 0, s>>>(a);
-      else attn_resident_kernel<DH, 10, RES_NTL, 1, false><<<grid, 10 * 64, 0, s>>>(a);
+      if (a.scores)
+        launch_kernel(attn_resident_kernel<DH, 10, RES_NTL, 1, false, true>, grid, 10 * 64, 0, s,
+                      a);
+      else
+        launch_kernel(attn_resident_kernel<DH, 10, RES_NTL, 1, false>, grid, 10 * 64, 0, s, a);
     }
     return hipGetLastError();
   }
@@ -841,8 +847,7 @@ hipError_t launch_concat_kv(DType dt, void *k_dst, void *v_dst, const void *k_a,
   const int per = (na + nc) * cpr;
   if (bh == 0 || per == 0) return hipSuccess;
   const dim3 grid((per + 256 * CONCAT_CPT - 1) / (256 * CONCAT_CPT), bh);
-  concat_kv_kernel<<<grid, 256, 0, s>>>(
-      static_cast<u32x4 *>(k_dst), static_cast<u32x4 *>(v_dst), static_cast<const u32x4 *>(k_a),
+  launch_kernel(concat_kv_kernel, grid, 256, 0, s, static_cast<u32x4 *>(k_dst), static_cast<u32x4 *>(v_dst), static_cast<const u32x4 *>(k_a),
       static_cast<const u32x4 *>(v_a), static_cast<const u32x4 *>(k_c),
       static_cast<const u32x4 *>(v_c), na * cpr, nc * cpr);
   return hipGetLastError();
@@ -898,7 +903,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
 template <int DH>
 static hipError_t attn_f32_dispatch(const AttnArgs &a, hipStream_t s) {
   const size_t lds = (size_t)(DH + a.n_tokens) * sizeof(float);
-  attn_f32_kernel<DH><<<a.a_total * a.n_heads, 64, lds, s>>>(a);
+  launch_kernel(attn_f32_kernel<DH>, a.a_total * a.n_heads, 64, lds, s, a);
   return hipGetLastError();
 }
 
@@ -1039,7 +1044,8 @@ static hipError_t scores_dispatch(const AttnArgs &a, const int32_t *n_gen, float
   int gq = 12288 / a.n_tokens;
   gq = gq < 1 ? 1 : (gq > 8 ? 8 : gq);
   const size_t lds = (size_t)(gq * DH + gq * a.n_tokens + 4) * sizeof(float);
-  attn_scores_kernel<T, DH><<<a.batch * a.n_heads, SC_THREADS, lds, s>>>(a, n_gen, scores, gq);
+  launch_kernel(attn_scores_kernel<T, DH>, a.batch * a.n_heads, SC_THREADS, lds, s,
+                a, n_gen, scores, gq);
   return hipGetLastError();
 }
 

@@ -21,7 +21,7 @@ __global__ void row_map_kernel(RowMap *map, const int32_t *a_idx, const int32_t 
 
 hipError_t launch_row_map(RowMap *map, const int32_t *a_idx, const int32_t *a_off, int32_t batch,
                           int32_t n_tokens, hipStream_t s) {
-  row_map_kernel<<<batch, 256, 0, s>>>(map, a_idx, a_off, n_tokens);
+  launch_kernel(row_map_kernel, batch, 256, 0, s, map, a_idx, a_off, n_tokens);
   return hipGetLastError();
 }
 
@@ -74,8 +74,8 @@ __global__ __launch_bounds__(256) void check_active_kernel(
 hipError_t launch_check_active(const int32_t *a_idx, const int32_t *a_off, const int32_t *n_gen,
                                int32_t batch, int32_t n_tokens, int32_t a_total, int32_t a_max,
                                int32_t gen_max, int32_t *report, hipStream_t s) {
-  clear_word_kernel<<<1, 64, 0, s>>>(report);
-  check_active_kernel<<<batch, 256, 0, s>>>(a_idx, a_off, n_gen, batch, n_tokens, a_total, a_max,
+  launch_kernel(clear_word_kernel, 1, 64, 0, s, report);
+  launch_kernel(check_active_kernel, batch, 256, 0, s, a_idx, a_off, n_gen, batch, n_tokens, a_total, a_max,
                                             gen_max, report);
   return hipGetLastError();
 }
@@ -137,14 +137,14 @@ static hipError_t gather_ln_dispatch(OutT *out, const float *x, const RowMap *ma
                                      const float *b, int rows, int d, float eps, hipStream_t s) {
   const int grid = (rows + 3) / 4;
   switch (d / 256) {
-    case 1: gather_ln_kernel<OutT, 1><<<grid, 256, 0, s>>>(out, x, map, g, b, rows, eps); break;
-    case 2: gather_ln_kernel<OutT, 2><<<grid, 256, 0, s>>>(out, x, map, g, b, rows, eps); break;
-    case 3: gather_ln_kernel<OutT, 3><<<grid, 256, 0, s>>>(out, x, map, g, b, rows, eps); break;
-    case 4: gather_ln_kernel<OutT, 4><<<grid, 256, 0, s>>>(out, x, map, g, b, rows, eps); break;
-    case 5: gather_ln_kernel<OutT, 5><<<grid, 256, 0, s>>>(out, x, map, g, b, rows, eps); break;
-    case 6: gather_ln_kernel<OutT, 6><<<grid, 256, 0, s>>>(out, x, map, g, b, rows, eps); break;
-    case 7: gather_ln_kernel<OutT, 7><<<grid, 256, 0, s>>>(out, x, map, g, b, rows, eps); break;
-    case 8: gather_ln_kernel<OutT, 8><<<grid, 256, 0, s>>>(out, x, map, g, b, rows, eps); break;
+    case 1: launch_kernel(gather_ln_kernel<OutT, 1>, grid, 256, 0, s, out, x, map, g, b, rows, eps); break;
+    case 2: launch_kernel(gather_ln_kernel<OutT, 2>, grid, 256, 0, s, out, x, map, g, b, rows, eps); break;
+    case 3: launch_kernel(gather_ln_kernel<OutT, 3>, grid, 256, 0, s, out, x, map, g, b, rows, eps); break;
+    case 4: launch_kernel(gather_ln_kernel<OutT, 4>, grid, 256, 0, s, out, x, map, g, b, rows, eps); break;
+    case 5: launch_kernel(gather_ln_kernel<OutT, 5>, grid, 256, 0, s, out, x, map, g, b, rows, eps); break;
+    case 6: launch_kernel(gather_ln_kernel<OutT, 6>, grid, 256, 0, s, out, x, map, g, b, rows, eps); break;
+    case 7: launch_kernel(gather_ln_kernel<OutT, 7>, grid, 256, 0, s, out, x, map, g, b, rows, eps); break;
+    case 8: launch_kernel(gather_ln_kernel<OutT, 8>, grid, 256, 0, s, out, x, map, g, b, rows, eps); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -189,7 +189,7 @@ hipError_t launch_decoder_input(float *x, const float *cls, const float *value, 
                                 int32_t n_tokens, int32_t n_buf, int32_t d_model, int32_t n_known,
                                 hipStream_t s) {
   if (batch == 0) return hipSuccess;
-  decoder_input_kernel<<<batch * n_tokens, 256, 0, s>>>(x, cls, value, mask, pos, rank, n_tokens,
+  launch_kernel(decoder_input_kernel, batch * n_tokens, 256, 0, s, x, cls, value, mask, pos, rank, n_tokens,
                                                         n_buf, d_model / 4, n_known);
   return hipGetLastError();
 }
@@ -210,7 +210,7 @@ hipError_t launch_fill_zero(void *dst, size_t bytes, hipStream_t s) {
   size_t grid = (n16 + 255) / 256;
   if (grid > 8192) grid = 8192;
   if (grid == 0) grid = 1;
-  fill_zero_kernel<<<(unsigned)grid, 256, 0, s>>>(static_cast<uint4 *>(dst), n16, tail,
+  launch_kernel(fill_zero_kernel, (unsigned)grid, 256, 0, s, static_cast<uint4 *>(dst), n16, tail,
                                                   bytes - n16 * 16);
   return hipGetLastError();
 }

@@ -1069,22 +1069,25 @@ static hipError_t run_bf16(const void *a, const void *w, int m, int n, int k, co
   const bf16 *A = static_cast<const bf16 *>(a), *W = static_cast<const bf16 *>(w);
   switch (gemm_tile_kind(DType::BF16, m, n, k)) {
     case GEMM_TILE_256:
-      gemm_bf16_big_kernel<Epi><<<((m + 255) / 256) * (n / 256), 256, 0, s>>>(A, W, m, n, k, epi);
+      launch_kernel(gemm_bf16_big_kernel<Epi>, ((m + 255) / 256) * (n / 256), 256, 0, s,
+                    A, W, m, n, k, epi);
       break;
     case GEMM_TILE_64x128:
-      gemm_bf16_small_kernel<Epi>
-          <<<((m + small::kBM - 1) / small::kBM) * (n / small::kBN), 256, 0, s>>>(A, W, m, n, k, epi);
+      launch_kernel(gemm_bf16_small_kernel<Epi>,
+                    ((m + small::kBM - 1) / small::kBM) * (n / small::kBN), 256, 0, s, A, W, m, n,
+                    k, epi);
       break;
     case GEMM_TILE_128:
-      gemm_bf16_mid_kernel<Epi, 4>
-          <<<((m + mid::kBM - 1) / mid::kBM) * (n / mid::kBN), 256, 0, s>>>(A, W, m, n, k, epi);
+      launch_kernel(gemm_bf16_mid_kernel<Epi, 4>,
+                    ((m + mid::kBM - 1) / mid::kBM) * (n / mid::kBN), 256, 0, s, A, W, m, n, k,
+                    epi);
       break;
     default: {
       const int tiles = ((m + pair::kBM - 1) / pair::kBM) * (n / pair::kBN);
       if (tiles <= device_cu_count() && k >= 2048)
-        gemm_bf16_pair_kernel<Epi, 6><<<tiles, 256, 0, s>>>(A, W, m, n, k, epi);
+        launch_kernel(gemm_bf16_pair_kernel<Epi, 6>, tiles, 256, 0, s, A, W, m, n, k, epi);
       else
-        gemm_bf16_pair_kernel<Epi, 3><<<tiles, 256, 0, s>>>(A, W, m, n, k, epi);
+        launch_kernel(gemm_bf16_pair_kernel<Epi, 3>, tiles, 256, 0, s, A, W, m, n, k, epi);
     }
   }
   return hipGetLastError();
@@ -1143,7 +1146,7 @@ static hipError_t run_f32(const void *a, const void *w, int m, int n, int k, con
   if (m == 0) return hipSuccess;
   if (n % 64 != 0 || k % 16 != 0) return hipErrorInvalidValue;
   const int grid = ((m + 63) / 64) * (n / 64);
-  gemm_f32_kernel<Epi><<<grid, 256, 0, s>>>(static_cast<const float *>(a),
+  launch_kernel(gemm_f32_kernel<Epi>, grid, 256, 0, s, static_cast<const float *>(a),
                                             static_cast<const float *>(w), m, n, k, epi);
   return hipGetLastError();
 }

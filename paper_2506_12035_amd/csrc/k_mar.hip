@@ -377,7 +377,7 @@ static void encoder_input_dispatch(int grid, hipStream_t s, float *x, const floa
                                    const float *tok, const float *w_z, const float *b_z,
                                    const float *pe, const int32_t *known, int rows, int n_enc,
                                    int n_buf, int n_img, int n_known, int c) {
-#define E_(CM) encoder_input_kernel<NV, CM><<<grid, 256, 0, s>>>(x, cls, tok, w_z, b_z, pe, known, \
+#define E_(CM) launch_kernel(encoder_input_kernel<NV, CM>, grid, 256, 0, s, x, cls, tok, w_z, b_z, pe, known, \
                                                                 rows, n_enc, n_buf, n_img, n_known, c)
   if (c <= 4) E_(4);
   else if (c <= 8) E_(8);
@@ -410,7 +410,7 @@ hipError_t launch_mask_fill(float *x, const float *mask, const float *pe, const 
   if (d_model % 256 != 0) return hipErrorInvalidValue;
   const int grid = (rows + 3) / 4;
 #define L_(NV)                                                                          \
-  mask_fill_kernel<NV><<<grid, 256, 0, s>>>(x, mask, pe, rank, rows, n_tokens, n_buf, n_img, \
+  launch_kernel(mask_fill_kernel<NV>, grid, 256, 0, s, x, mask, pe, rank, rows, n_tokens, n_buf, n_img, \
                                             n_known)
   MARCHE_NV_SWITCH(d_model / 256, L_)
 #undef L_
@@ -426,13 +426,13 @@ hipError_t launch_ln_rows(DType dt, void *out, const float *x, const int32_t *ro
   const int grid = (rows + 3) / 4;
   if (dt == DType::F32) {
 #define L_(NV)                                                                                  \
-  ln_rows_kernel<float, NV><<<grid, 256, 0, s>>>(static_cast<float *>(out), x, rows_idx, g, b, add, \
+  launch_kernel(ln_rows_kernel<float, NV>, grid, 256, 0, s, static_cast<float *>(out), x, rows_idx, g, b, add, \
                                                  rows, n_tokens, n_buf, eps)
     MARCHE_NV_SWITCH(d_model / 256, L_)
 #undef L_
   } else {
 #define L_(NV)                                                                                \
-  ln_rows_kernel<bf16, NV><<<grid, 256, 0, s>>>(static_cast<bf16 *>(out), x, rows_idx, g, b, add, \
+  launch_kernel(ln_rows_kernel<bf16, NV>, grid, 256, 0, s, static_cast<bf16 *>(out), x, rows_idx, g, b, add, \
                                                 rows, n_tokens, n_buf, eps)
     MARCHE_NV_SWITCH(d_model / 256, L_)
 #undef L_
@@ -445,9 +445,11 @@ hipError_t launch_time_sinus(DType dt, void *out, int32_t n_steps, int32_t freq,
   if (n == 0) return hipSuccess;
   const int grid = (n + 255) / 256;
   if (dt == DType::F32)
-    time_sinus_kernel<float><<<grid, 256, 0, s>>>(static_cast<float *>(out), n_steps, freq);
+    launch_kernel(time_sinus_kernel<float>, grid, 256, 0, s,
+                  static_cast<float *>(out), n_steps, freq);
   else
-    time_sinus_kernel<bf16><<<grid, 256, 0, s>>>(static_cast<bf16 *>(out), n_steps, freq);
+    launch_kernel(time_sinus_kernel<bf16>, grid, 256, 0, s,
+                  static_cast<bf16 *>(out), n_steps, freq);
   return hipGetLastError();
 }
 
@@ -458,9 +460,11 @@ hipError_t launch_silu_cond(DType dt, void *sc, const float *cond, const float *
   if (width % 4 != 0) return hipErrorInvalidValue;
   const int grid = (n4 + 255) / 256;
   if (dt == DType::F32)
-    silu_cond_kernel<float><<<grid, 256, 0, s>>>(static_cast<float *>(sc), cond, temb, rows, width);
+    launch_kernel(silu_cond_kernel<float>, grid, 256, 0, s,
+                  static_cast<float *>(sc), cond, temb, rows, width);
   else
-    silu_cond_kernel<bf16><<<grid, 256, 0, s>>>(static_cast<bf16 *>(sc), cond, temb, rows, width);
+    launch_kernel(silu_cond_kernel<bf16>, grid, 256, 0, s,
+                  static_cast<bf16 *>(sc), cond, temb, rows, width);
   return hipGetLastError();
 }
 
@@ -468,7 +472,7 @@ template <typename T, int NV>
 static void head_in_mod_dispatch(int grid, hipStream_t s, T *a, float *h, const float *x,
                                  const float *w_in_t, const float *b_in, const T *mod, int mod_ld,
                                  int rows, int c, float eps) {
-#define E_(CM) head_in_mod_kernel<T, NV, CM><<<grid, 256, 0, s>>>(a, h, x, w_in_t, b_in, mod, mod_ld, \
+#define E_(CM) launch_kernel(head_in_mod_kernel<T, NV, CM>, grid, 256, 0, s, a, h, x, w_in_t, b_in, mod, mod_ld, \
                                                                  rows, c, eps)
   if (c <= 4) E_(4);
   else if (c <= 8) E_(8);
@@ -482,7 +486,7 @@ hipError_t launch_transpose_f32(float *w_t, const float *w, int32_t rows, int32_
                                 hipStream_t s) {
   const int n = rows * cols;
   if (n == 0) return hipSuccess;
-  transpose_f32_kernel<<<(n + 255) / 256, 256, 0, s>>>(w_t, w, rows, cols);
+  launch_kernel(transpose_f32_kernel, (n + 255) / 256, 256, 0, s, w_t, w, rows, cols);
   return hipGetLastError();
 }
 
@@ -517,14 +521,14 @@ hipError_t launch_head_gate_mod(DType dt, void *a, float *h, const float *t, con
   const int grid = (rows + 3) / 4;
   if (dt == DType::F32) {
 #define L_(NV)                                                                              \
-  head_gate_mod_kernel<float, NV><<<grid, 256, 0, s>>>(static_cast<float *>(a), h, t,          \
+  launch_kernel(head_gate_mod_kernel<float, NV>, grid, 256, 0, s, static_cast<float *>(a), h, t,          \
                                                        static_cast<const float *>(mod), mod_ld, \
                                                        gate_off, shift_off, scale_off, rows, eps)
     MARCHE_NV_SWITCH(width / 256, L_)
 #undef L_
   } else {
 #define L_(NV)                                                                            \
-  head_gate_mod_kernel<bf16, NV><<<grid, 256, 0, s>>>(static_cast<bf16 *>(a), h, t,          \
+  launch_kernel(head_gate_mod_kernel<bf16, NV>, grid, 256, 0, s, static_cast<bf16 *>(a), h, t,          \
                                                       static_cast<const bf16 *>(mod), mod_ld, \
                                                       gate_off, shift_off, scale_off, rows, eps)
     MARCHE_NV_SWITCH(width / 256, L_)
@@ -539,7 +543,7 @@ static void head_out_step_dispatch(int grid, hipStream_t s, float *x_next, float
                                    const float *x_cur, const float *noise, const int32_t *out_rows,
                                    int rows, int W, int c, const HeadStep &st) {
 #define E_(CM)                                                                                 \
-  head_out_step_kernel<T, CM><<<grid, 256, 0, s>>>(x_next, tok_out, a, w_out, b_out, x_cur, noise, \
+  launch_kernel(head_out_step_kernel<T, CM>, grid, 256, 0, s, x_next, tok_out, a, w_out, b_out, x_cur, noise, \
                                                    out_rows, rows, W, c, st.sra, st.srm1, st.c1,   \
                                                    st.c2, st.sigma)
   if (c <= 4) E_(4);

@@ -114,13 +114,13 @@ hipError_t launch_select_topk(const float *scores, int32_t n_parts, const int32_
   if (batch == 0 || k == 0) return hipSuccess;
   if (n_tokens > SEL_MAX_N) return hipErrorInvalidValue;
   if (n_tokens <= 512)
-    select_topk_kernel<8><<<batch, SEL_THREADS, 0, s>>>(scores, n_parts, excl_idx, excl_off,
+    launch_kernel(select_topk_kernel<8>, batch, SEL_THREADS, 0, s, scores, n_parts, excl_idx, excl_off,
                                                         n_tokens, k, out_idx, out_off, lowest);
   else if (n_tokens <= 2048)
-    select_topk_kernel<32><<<batch, SEL_THREADS, 0, s>>>(scores, n_parts, excl_idx, excl_off,
+    launch_kernel(select_topk_kernel<32>, batch, SEL_THREADS, 0, s, scores, n_parts, excl_idx, excl_off,
                                                          n_tokens, k, out_idx, out_off, lowest);
   else
-    select_topk_kernel<64><<<batch, SEL_THREADS, 0, s>>>(scores, n_parts, excl_idx, excl_off,
+    launch_kernel(select_topk_kernel<64>, batch, SEL_THREADS, 0, s, scores, n_parts, excl_idx, excl_off,
                                                          n_tokens, k, out_idx, out_off, lowest);
   return hipGetLastError();
 }

@@ -197,6 +197,7 @@ struct Totals {
 
 std::mutex g_mu;
 bool g_prof = false;
+thread_local KernelEvents *t_kernel_events = nullptr;
 std::vector<Pending> g_pending;
 std::vector<hipEvent_t> g_pool;
 Totals g_tot[K_NTIMED];
@@ -212,37 +213,51 @@ hipEvent_t pool_get() {
   return e;
 }
 
-// Brackets one kernel launch with events when profiling is on.
+// Times one launch call when profiling is on: its first kernel's dispatch
+// carries the two events (launch_kernel), so they hold that kernel's own
+// start and end.  A call that launches no kernel records nothing.
 struct ProfScope {
   int cls;
-  hipStream_t s;
   double flops, bytes;
-  hipEvent_t e0 = nullptr;
+  KernelEvents ev;
   bool on = false;
-  ProfScope(int c, hipStream_t st, double f, double b) : cls(c), s(st), flops(f), bytes(b) {
+  ProfScope(int c, double f, double b) : cls(c), flops(f), bytes(b) {
     std::lock_guard<std::mutex> lk(g_mu);
     if (!g_prof) return;
-    e0 = pool_get();
-    if (e0 && hipEventRecord(e0, s) == hipSuccess) on = true;
+    ev.start = pool_get();
+    ev.stop = pool_get();
+    if (!ev.start || !ev.stop) return;
+    on = true;
+    kernel_events() = &ev;
   }
   void done() {
     if (!on) return;
+    kernel_events() = nullptr;
     std::lock_guard<std::mutex> lk(g_mu);
-    hipEvent_t e1 = pool_get();
-    if (e1 && hipEventRecord(e1, s) == hipSuccess) g_pending.push_back({cls, e0, e1, flops, bytes});
+    if (ev.used) {
+      g_pending.push_back({cls, ev.start, ev.stop, flops, bytes});
+    } else {
+      g_pool.push_back(ev.start);
+      g_pool.push_back(ev.stop);
+    }
     on = false;
+  }
+  ~ProfScope() {
+    if (on) kernel_events() = nullptr;
   }
 };
 
 #define LAUNCH(cls, flops, bytes, call)                        \
   do {                                                         \
-    ProfScope ps_(cls, stream, (double)(flops), (double)(bytes)); \
+    ProfScope ps_(cls, (double)(flops), (double)(bytes));      \
     hipError_t e_ = (call);                                    \
     ps_.done();                                                \
     if (e_ != hipSuccess) return fail_hip(e_, #call);          \
   } while (0)
 
 }  // namespace
+
+marche::KernelEvents *&marche::kernel_events() { return t_kernel_events; }
 
 marche_status_t marche::set_error(marche_status_t s, const char *fmt, ...) {
   char buf[512];

@@ -23,6 +23,18 @@ struct RowMap {
   int32_t pad;
 };
 
+// Kernel timing of the library's profiling mode (marche_profile_*): while a
+// timed call runs on a thread, the first kernel it launches through
+// launch_kernel() (device_common.h) carries the call's two events on its
+// dispatch (hipExtLaunchKernel), so they hold the kernel's own start and end,
+// not the stream's dispatch gap before it.
+struct KernelEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+  bool used = false;
+};
+// This thread's slot: the timed call in progress, or nullptr.
+KernelEvents *&kernel_events();
+
 // Element type of the packed activations, weights and KV cache.
 enum class DType { F32 = 0, BF16 = 1 };
 
