@@ -26,8 +26,8 @@ import argparse
 import hashlib
 import json
 import os
-import statistics
 import re
+import statistics
 import sys
 import time
 
@@ -96,7 +96,7 @@ def counter_class(name: str):
             "ELb1EEEv" in name
         return "attention_res_scores" if scores else "attention_res"
     if "attn_reg_kernel" in name:
-        for qb, q in (("4", "q128"), ("2", "q64"), ("1", "q32")):
+        for qb, q in (("8", "q256"), ("4", "q128"), ("2", "q64"), ("1", "q32")):
             if f"attn_reg_kernelILi{qb}E" in name or f"attn_reg_kernel<{qb}," in name:
                 return f"attention_{q}"
     if "attn_mfma_kernel" in name:
@@ -224,7 +224,10 @@ def kernel_rates(prof: dict, dtype: str) -> dict:
     for name, e in prof.items():
         avg_s = e["ms"] * 1e-3 / e["launches"]
         base = name[:-3] if name.endswith("_ca") else name   # cache-aware layers' classes
-        if base in HBM_BOUND or e["flops"] == 0:
+        # attention of a cache-aware layer: about |A| flop per byte of K/V, far
+        # below the ridge point (312), so HBM-bound whatever its query chunk
+        ca_attention = name.endswith("_ca") and base.startswith("attention_q")
+        if base in HBM_BOUND or e["flops"] == 0 or ca_attention:
             ach = e["bytes"] / e["launches"] / avg_s / 1e9
             out[name] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": ach / PEAK_HBM_GBS}

@@ -398,7 +398,16 @@ __device__ __forceinline__ void tile(const unsigned char *slot, const bf16x8 (&q
 }  // namespace strm
 
 // DEPTH register sets of the next tiles (1 or 2) per lane.
-template <int QB, int DEPTH>
+//
+// SCORES (the selection layer, Section 4.2): the workgroup of query chunk 0,
+// which holds the image's generating rows (its first n_gen[b] <= 16 QB rows),
+// then writes the attention mass each key receives from them,
+// a.scores[b][h][j].  Its wavefronts put the final row maximum and
+// normaliser of those rows in LDS and stream the K tiles once more; wavefront
+// w takes key block w % 2 of each tile for generating block w / 2: S = Q K^T
+// (one lane per key), the probabilities with the final statistics, summed
+// over the block's rows; the blocks' sums are added in block order.
+template <int QB, int DEPTH, bool SCORES = false>
 __global__ __launch_bounds__(QB * 64) void attn_reg_kernel(AttnArgs a, int chunks) {
   using namespace strm;
   constexpr int NT = QB * 64;
@@ -490,6 +499,90 @@ __global__ __launch_bounds__(QB * 64) void attn_reg_kernel(AttnArgs a, int chunk
                      (bf16)(acc[db][4 * gq + 2] * inv), (bf16)(acc[db][4 * gq + 3] * inv)};
         *reinterpret_cast<bf16x4 *>(orow + dh0) = pk;
       }
+  }
+  if constexpr (SCORES) {
+    if (chunk != 0) return;  // uniform over the workgroup
+    constexpr int CPK = 512 / NT;  // K chunks per lane per tile
+    const int n_gen = a.n_gen[b];
+    const int gb_n = (n_gen + 31) / 32;
+    // LDS: K tiles in the K halves of the two slots; the blocks' per-key sums
+    // in slot 0's V half; the statistics in slot 1's V half
+    float *part = reinterpret_cast<float *>(smem + 8192);
+    float *st_mx = reinterpret_cast<float *>(smem + kSlotBytes + 8192);
+    float *st_iv = st_mx + QB * 32;
+    // (the main loop ended on a barrier: no wavefront reads the slots again)
+    if (lane < 32) {
+      const int row = wave * 32 + lane;            // query qi of this lane
+      st_mx[row] = qi < n_gen ? m_run : INFINITY;  // rows past n_gen: probability 0
+      st_iv[row] = qi < n_gen ? inv : 0.f;
+    }
+    const int kb = wave & 1, gb = wave >> 1, hf = lane >> 5;
+    const bool active = gb < gb_n;
+    bf16x8 qg[4];
+    {
+      const int row = r0 + min(gb * 32 + (lane & 31), na - 1);
+      const bf16 *qr = static_cast<const bf16 *>(a.q) + (size_t)row * D + h * 64;
+#pragma unroll
+      for (int s2 = 0; s2 < 4; ++s2)
+        qg[s2] = *reinterpret_cast<const bf16x8 *>(qr + s2 * 16 + hf * 8);
+    }
+    u32x4 rk[CPK];
+    auto kload = [&](int tk) {
+      const size_t off = (size_t)min(tk, nt - 1) * TK * 64;
+#pragma unroll
+      for (int i = 0; i < CPK; ++i)
+        rk[i] = *reinterpret_cast<const u32x4 *>(kg + off + (i * NT + tid) * 8);
+    };
+    auto kstore = [&](int buf) {
+      unsigned char *slot = smem + buf * kSlotBytes;
+#pragma unroll
+      for (int i = 0; i < CPK; ++i) {
+        const int j = i * NT + tid, row = j >> 3, c = j & 7;
+        *reinterpret_cast<u32x4 *>(slot + row * 128 + ((c ^ swz(row)) << 4)) = rk[i];
+      }
+    };
+    __syncthreads();  // the statistics are in LDS
+    f32x4 mx[4], iv[4];  // rows gb*32 + 8 g + 4 hf + 0..3 of the accumulator
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int r = min(gb, QB - 1) * 32 + 8 * g + 4 * hf;
+      mx[g] = *reinterpret_cast<const f32x4 *>(st_mx + r);
+      iv[g] = *reinterpret_cast<const f32x4 *>(st_iv + r);
+    }
+    kload(0);
+    kstore(0);
+    __syncthreads();
+    for (int tk = 0; tk < nt; ++tk) {
+      kload(tk + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (active) {
+        const unsigned char *kt = smem + (tk & 1) * kSlotBytes;
+        const int row = kb * 32 + (lane & 31);
+        f32x16 sc = f32x16{};
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+          const int c = st * 2 + hf;
+          const bf16x8 ka =
+              *reinterpret_cast<const bf16x8 *>(kt + row * 128 + ((c ^ swz(row)) << 4));
+          sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qg[st], ka, sc, 0, 0, 0);
+        }
+        float p = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          p += __builtin_amdgcn_exp2f(fmaf(sc[r], sl2, -mx[r >> 2][r & 3])) * iv[r >> 2][r & 3];
+        p += __shfl_xor(p, 32, 64);
+        if (lane < 32) part[gb * 64 + kb * 32 + lane] = p;
+      }
+      __syncthreads();
+      if (wave == 0) {
+        float tot = 0.f;
+        for (int g2 = 0; g2 < gb_n; ++g2) tot += part[g2 * 64 + lane];
+        a.scores[(size_t)bh * N + tk * TK + lane] = tot;
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      kstore((tk + 1) & 1);
+      __syncthreads();
+    }
   }
 }
 
@@ -728,12 +821,20 @@ constexpr int RES_QMAX = 320; // queries per workgroup
 // Host choice of the resident kernel: more than 64 active queries per image
 // (where the streaming kernel needs several workgroups per (image, head)), all
 // of them and all keys within one workgroup's reach, one key segment.
+// Query blocks per workgroup of the streaming kernel for a_max rows.
+static int reg_qb(int32_t a_max) {
+  return a_max <= 32 ? 1 : a_max <= 64 ? 2 : a_max <= 128 ? 4 : 8;
+}
+
 bool attn_resident(int32_t a_max, int32_t n_tokens, bool two_segments) {
   return !two_segments && a_max > 64 && a_max <= RES_QMAX && n_tokens <= RES_NTL * TK;
 }
 
-bool attn_fuses_scores(int32_t a_max, int32_t n_tokens) {
-  return attn_resident(a_max, n_tokens, false);
+bool attn_fuses_scores(int32_t a_max, int32_t n_tokens, int32_t head_dim, int32_t gen_max) {
+  if (attn_resident(a_max, n_tokens, false)) return true;
+  // streaming kernel: the generating rows within query chunk 0, and one
+  // (key block, generating block) pair per wavefront
+  return attn_streams(head_dim, n_tokens, false) && 2 * ((gen_max + 31) / 32) <= reg_qb(a_max);
 }
 
 template <int DH, int NW, bool SEG2>
@@ -758,17 +859,22 @@ constexpr int REG_DEPTH = 1;
 template <int QB>
 static hipError_t run_attn_reg(const AttnArgs &a, hipStream_t s) {
   const int chunks = (a.a_max + QB * 32 - 1) / (QB * 32);
-  launch_kernel(attn_reg_kernel<QB, REG_DEPTH>, a.batch * a.n_heads * chunks, QB * 64, 0, s,
-                a, chunks);
+  const int grid = a.batch * a.n_heads * chunks;
+  if (a.scores)
+    launch_kernel(attn_reg_kernel<QB, REG_DEPTH, true>, grid, QB * 64, 0, s, a, chunks);
+  else
+    launch_kernel(attn_reg_kernel<QB, REG_DEPTH>, grid, QB * 64, 0, s, a, chunks);
   return hipGetLastError();
 }
+
 
 template <int DH, bool SEG2>
 static hipError_t attn_bf16_nw(const AttnArgs &a, hipStream_t s) {
   if (attn_streams(DH, a.n_tokens, SEG2)) {
     if (a.a_max <= 32) return run_attn_reg<1>(a, s);
     if (a.a_max <= 64) return run_attn_reg<2>(a, s);
-    return run_attn_reg<4>(a, s);
+    if (a.a_max <= 128) return run_attn_reg<4>(a, s);
+    return run_attn_reg<8>(a, s);  // one pass over K/V per 256 queries
   }
   if (a.a_max <= 32) return run_attn_mfma<DH, 1, SEG2>(a, s);
   if (a.a_max <= 64) return run_attn_mfma<DH, 2, SEG2>(a, s);

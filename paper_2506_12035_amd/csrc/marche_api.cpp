@@ -116,7 +116,7 @@ enum KClass {
   K_HEAD_GATE_MOD, K_HEAD_OUT_STEP, K_GEMM_QKV_S, K_GEMM_O_S, K_GEMM_FC1_S, K_GEMM_FC2_S,
   K_GEMM_EMBED_S, K_GEMM_HEAD_S, K_GEMM_HEAD_SILU_S, K_TRANSPOSE, K_GEMM_QKV_M, K_GEMM_O_M,
   K_GEMM_FC1_M, K_GEMM_FC2_M, K_GEMM_EMBED_M, K_GEMM_HEAD_M, K_GEMM_HEAD_SILU_M,
-  K_ATTN_RES_SC,
+  K_ATTN_RES_SC, K_ATTN_W8, K_ATTN_SC,
   K_NCLASS
 };
 const char *const kClassNames[K_NCLASS] = {
@@ -132,7 +132,8 @@ const char *const kClassNames[K_NCLASS] = {
     "gemm_qkv_t64x128",  "gemm_o_t64x128", "gemm_fc1_t64x128",  "gemm_fc2_t64x128",
     "gemm_embed_t64x128", "gemm_head_t64x128", "gemm_head_silu_t64x128", "transpose",
     "gemm_qkv_t128",     "gemm_o_t128",    "gemm_fc1_t128",     "gemm_fc2_t128",
-    "gemm_embed_t128",   "gemm_head_t128", "gemm_head_silu_t128", "attention_res_scores"};
+    "gemm_embed_t128",   "gemm_head_t128", "gemm_head_silu_t128", "attention_res_scores", "attention_q256",
+    "attention_scores"};
 static_assert(sizeof(kClassNames) / sizeof(kClassNames[0]) == K_NCLASS, "one name per class");
 
 // Launches inside marche_step in layers where not every token of every image
@@ -180,8 +181,9 @@ int gemm_class(int base, DType dt, int32_t m, int32_t n, int32_t k) {
   }
 }
 
-int attn_class(DType dt, int a_max, int n_tokens) {
+int attn_class(DType dt, int a_max, int n_tokens, int head_dim) {
   if (dt == DType::BF16 && attn_resident(a_max, n_tokens, false)) return K_ATTN_RES;
+  if (a_max > 128 && dt == DType::BF16 && attn_streams(head_dim, n_tokens, false)) return K_ATTN_W8;
   return a_max <= 32 ? K_ATTN_W1 : (a_max <= 64 ? K_ATTN_W2 : K_ATTN_W4);
 }
 
@@ -454,14 +456,15 @@ marche_status_t marche::step_impl(const marche_model_t *m, const marche_layer_t 
     // score pass (Section 4.2) from the K tiles it holds; other sizes run the
     // score pass as a kernel of its own after the attention.
     const bool sel = want_scores && l == score_layer;
-    const bool fused = sel && dt == DType::BF16 && attn_fuses_scores(a_max, N);
+    const bool fused = sel && dt == DType::BF16 && attn_fuses_scores(a_max, N, dh, gen_max);
     if (fused) {
       aa.n_gen = n_gen;
       aa.scores = scores;
     }
     // Algorithmic traffic: every cached K/V element of the batch read once,
     // plus the queries read and the outputs written (and the scores).
-    LAUNCH((fused ? K_ATTN_RES_SC : attn_class(dt, a_max, N)) + ko,
+    const int acls = attn_class(dt, a_max, N, dh);
+    LAUNCH((fused ? (acls == K_ATTN_RES ? K_ATTN_RES_SC : K_ATTN_SC) : acls) + ko,
            4.0 * M * N * D + (fused ? 2.0 * batch * gen_max * N * D : 0.0),
            es * (2.0 * batch * N * D + 2.0 * M * D) + (fused ? 4.0 * batch * H * N : 0.0),
            launch_attention(dt, aa, stream));
@@ -607,7 +610,7 @@ marche_status_t marche_attention_segments(const void *q, void *o, int32_t n_quer
       aa.n2 = n_c;
     }
     const int cls = (n_a > 0 && n_c > 0) ? K_ATTN2_W1 + cls_w
-                                         : attn_class(DType::BF16, n_query, aa.n_tokens);
+                                         : attn_class(DType::BF16, n_query, aa.n_tokens, head_dim);
     LAUNCH(cls, flops, attn_bytes, launch_attention(DType::BF16, aa, stream));
     return MARCHE_OK;
   }
@@ -627,7 +630,7 @@ marche_status_t marche_attention_segments(const void *q, void *o, int32_t n_quer
   aa.k_cache = kcat;
   aa.v_cache = vcat;
   aa.n_tokens = nt;
-  LAUNCH(attn_class(DType::BF16, n_query, nt), flops, attn_bytes,
+  LAUNCH(attn_class(DType::BF16, n_query, nt, head_dim), flops, attn_bytes,
          launch_attention(DType::BF16, aa, stream));
   return MARCHE_OK;
 }

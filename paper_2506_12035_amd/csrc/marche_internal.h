@@ -162,9 +162,13 @@ hipError_t launch_attention(DType dt, const AttnArgs &a, hipStream_t s);
 // Whether bf16 attention with these sizes runs the resident-K/V kernel (one
 // workgroup per (image, head)).
 bool attn_resident(int32_t a_max, int32_t n_tokens, bool two_segments);
-// Whether bf16 attention with these sizes can write the score pass itself
-// (the resident kernel: every key of a head in LDS).
-bool attn_fuses_scores(int32_t a_max, int32_t n_tokens);
+// Whether bf16 attention with these sizes runs the register-staged streaming
+// kernel (head width 64, one key segment of whole tiles).
+bool attn_streams(int32_t head_dim, int32_t n_tokens, bool two_segments);
+// Whether bf16 attention with these sizes can write the score pass itself:
+// the resident kernel (every key of a head in LDS), or the streaming kernel
+// when the generating rows fit its first query chunk.
+bool attn_fuses_scores(int32_t a_max, int32_t n_tokens, int32_t head_dim, int32_t gen_max);
 // dst[b][h] = [a[b][h] (na rows) ; c[b][h] (nc rows)], rows of dh elements, for
 // K and V: the concatenation of the active and cached segments.
 hipError_t launch_concat_kv(DType dt, void *k_dst, void *v_dst, const void *k_a, const void *v_a,
