@@ -24,6 +24,8 @@
 // key tiles of the first segment, then of the second, in one online-softmax
 // pass -- Appendix A's merge without concatenation, as the stand-alone
 // two-segment attention of Appendix B's comparison.
+#include <type_traits>
+
 #include "device_common.h"
 
 namespace marche {
@@ -397,8 +399,6 @@ __device__ __forceinline__ void tile(const unsigned char *slot, const bf16x8 (&q
 
 }  // namespace strm
 
-// DEPTH register sets of the next tiles (1 or 2) per lane.
-//
 // SCORES (the selection layer, Section 4.2): the workgroup of query chunk 0,
 // which holds the image's generating rows (its first n_gen[b] <= 16 QB rows),
 // then writes the attention mass each key receives from them,
@@ -407,12 +407,11 @@ __device__ __forceinline__ void tile(const unsigned char *slot, const bf16x8 (&q
 // w takes key block w % 2 of each tile for generating block w / 2: S = Q K^T
 // (one lane per key), the probabilities with the final statistics, summed
 // over the block's rows; the blocks' sums are added in block order.
-template <int QB, int DEPTH, bool SCORES = false>
+template <int QB, bool SCORES = false>
 __global__ __launch_bounds__(QB * 64) void attn_reg_kernel(AttnArgs a, int chunks) {
   using namespace strm;
   constexpr int NT = QB * 64;
   constexpr int CPL = 1024 / NT;  // 16-byte chunks per lane per tile (K and V)
-  static_assert(DEPTH == 1 || DEPTH == 2, "register sets in flight");
   __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * kSlotBytes];
 
   const int id = xcd_remap(blockIdx.x, gridDim.x);
@@ -440,7 +439,7 @@ __global__ __launch_bounds__(QB * 64) void attn_reg_kernel(AttnArgs a, int chunk
   // Every load is unconditional (a tile index past the last repeats the last
   // tile, which the L2 still holds), so the waits the compiler places count
   // exactly the loads issued after the ones a store needs.
-  u32x4 rt[DEPTH][CPL];
+  u32x4 rt[CPL];
   auto gload = [&](u32x4 (&r)[CPL], int t) {
     const size_t off = (size_t)min(t, nt - 1) * TK * 64;
 #pragma unroll
@@ -462,30 +461,31 @@ __global__ __launch_bounds__(QB * 64) void attn_reg_kernel(AttnArgs a, int chunk
   const float sl2 = 1.4426950408889634f / 8.0f;  // log2(e) / sqrt(64)
   float m_run = -INFINITY, l_run = 0.f;
   f32x16 acc[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-  for (int d = 0; d < DEPTH; ++d) gload(rt[d], d);
-  sstore(rt[0], 0);
+  gload(rt, 0);
+  sstore(rt, 0);
   __syncthreads();
-  // Tile t is in LDS slot t & 1 and its register set t % DEPTH is free again:
-  // it takes tile t + DEPTH while tile t computes; tile t + 1 then goes from
-  // its register set into the other slot.
-  // The scheduling barriers keep the stores of the next tile (and the waits
-  // for its loads) behind the whole tile step, which would otherwise start
-  // them, and wait, in the middle of it.
-  auto step = [&](int t, u32x4 (&r_free)[CPL], const u32x4 (&r_next)[CPL]) {
-    gload(r_free, t + DEPTH);
+  // Tile t is in LDS slot t & 1 and the registers are free again: they take
+  // tile t + 1 while tile t computes, then it goes into the other slot.  The
+  // loop is unrolled by two so that each step's slot is a constant (its LDS
+  // offsets fold into the reads' immediates).  The scheduling barriers keep
+  // the stores of the next tile (and the waits for its loads) behind the
+  // whole tile step, which would otherwise start them, and wait, in the
+  // middle of it.
+  auto step = [&](int t, auto slot) {
+    constexpr int SL = decltype(slot)::value;
+    gload(rt, t + 1);
     __builtin_amdgcn_sched_barrier(0);
-    tile(smem + (t & 1) * kSlotBytes, qf, acc, m_run, l_run, sl2, lane);
+    tile(smem + SL * kSlotBytes, qf, acc, m_run, l_run, sl2, lane);
     __builtin_amdgcn_sched_barrier(0);
-    sstore(r_next, (t + 1) & 1);
+    sstore(rt, SL ^ 1);
     __syncthreads();
   };
   int t = 0;
-  for (; t + DEPTH <= nt; t += DEPTH) {
-#pragma unroll
-    for (int d = 0; d < DEPTH; ++d) step(t + d, rt[d], rt[(d + 1) % DEPTH]);
+  for (; t + 2 <= nt; t += 2) {
+    step(t, std::integral_constant<int, 0>{});
+    step(t + 1, std::integral_constant<int, 1>{});
   }
-  if (DEPTH == 2 && t < nt) step(t, rt[0], rt[1 % DEPTH]);
+  if (t < nt) step(t, std::integral_constant<int, 0>{});
 
   const float inv = 1.0f / (l_run + __shfl_xor(l_run, 32, 64));
   if (qi < na) {
@@ -855,15 +855,14 @@ bool attn_streams(int32_t head_dim, int32_t n_tokens, bool two_segments) {
   return head_dim == 64 && !two_segments && n_tokens % TK == 0 && n_tokens >= 3 * TK;
 }
 
-constexpr int REG_DEPTH = 1;
 template <int QB>
 static hipError_t run_attn_reg(const AttnArgs &a, hipStream_t s) {
   const int chunks = (a.a_max + QB * 32 - 1) / (QB * 32);
   const int grid = a.batch * a.n_heads * chunks;
   if (a.scores)
-    launch_kernel(attn_reg_kernel<QB, REG_DEPTH, true>, grid, QB * 64, 0, s, a, chunks);
+    launch_kernel(attn_reg_kernel<QB, true>, grid, QB * 64, 0, s, a, chunks);
   else
-    launch_kernel(attn_reg_kernel<QB, REG_DEPTH>, grid, QB * 64, 0, s, a, chunks);
+    launch_kernel(attn_reg_kernel<QB>, grid, QB * 64, 0, s, a, chunks);
   return hipGetLastError();
 }
 
