@@ -245,6 +245,22 @@ def test_select_refresh_lowest_first():
     assert 11 not in sel[2]
 
 
+def test_select_refresh_long_sequence_many_heads():
+    # 20 heads (two batches of sixteen loads), 3000 tokens (two tokens per
+    # thread), and an image with more exclusions than the workgroup has threads
+    rng = np.random.default_rng(31)
+    N, H, B = 3000, 20, 3
+    s = rng.standard_normal((B, H, N)).astype(np.float32)
+    s[1, :, 100:200] = 0.75          # a block of ties
+    excl = [rng.choice(N, 1500, replace=False), rng.choice(N, 10, replace=False), np.arange(0)]
+    k = 120
+    for lowest in (False, True):
+        sel = _select_gpu(s, excl, k, lowest=lowest)
+        for b in range(B):
+            assert list(sel[b]) == select.select_topk(_fp32_head_sum(s[b]), excl[b], k,
+                                                      lowest=lowest)
+
+
 def test_bf16_layer_cache_aware_range_size():
     """A cache-aware MAR-L layer on a 64-image range (34-44 active rows per
     image, about 2500 in all): the size at which the output projection and fc2
