@@ -9,9 +9,10 @@
 //   - adds into the float32 residual stream row     (output projection, fc2)
 //   - applies exact GELU and stores the hidden row  (fc1)
 //
-// bf16 path (v_mfma_f32_32x32x16_bf16, fp32 accumulators): a 256x256 tile on
-// four wavefronts (one workgroup per CU) for shapes that fill the chip in
-// whole waves, else a 128x256 tile of which two workgroups share a CU.  Both
+// bf16 path (v_mfma_f32_32x32x16_bf16, fp32 accumulators): a 256x256 tile
+// (one workgroup per CU; four wavefronts for K >= 2048, eight below) for
+// shapes that fill the chip in whole waves, else a 128x256 tile of which two
+// workgroups share a CU, or 128x128 / 64x128 tiles for narrow products.  All
 // load operands straight from global memory into XOR-swizzled LDS stages and
 // write back through LDS in row-major order.
 //
@@ -523,6 +524,167 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_big_kernel(const bf16 *A, co
   write_back_staged<4, 4, 16>(acc, epi, m0 + wm * 128, n0 + wn * 128, M, lane,
                            reinterpret_cast<float *>(smem) + wave * 32 * kWbStride,
                            reinterpret_cast<const typename Epi::Row *>(side + 1024) + wm * 128, b);
+}
+
+// ------------------------------------------------------------------ 256x256 tile, eight wavefronts
+//
+// The 256x256x64 tile of gemm_bf16_big_kernel (same LDS stages, swizzle,
+// direct-to-LDS loads and stage schedule) on eight wavefronts of 128x64 (8
+// accumulator blocks, 128 accumulation registers each), two per SIMD: while
+// one wavefront of a SIMD waits on a fragment read, a barrier or its
+// write-back's LDS round trip, the other can issue MFMAs.  Per k16 step a
+// wavefront reads 6 fragments for 8 MFMAs (4 activation and 2 weight
+// fragments), 1.5 times the LDS reads per MFMA of the 128x128 wavefront tile.
+namespace big8 {
+
+struct Frag {
+  bf16x8 x[4];  // activation rows (MFMA B operand)
+  bf16x8 w[2];  // weight rows (MFMA A operand)
+};
+
+// Fragment r of k16 step s, in the order the MFMAs need them: x0 w0 x1 x2 x3 w1.
+__device__ __forceinline__ void read_frag(Frag &f, int r, const unsigned char *sa,
+                                          const unsigned char *sw, int s, int wm, int wn,
+                                          int lane) {
+  const int kc = s * 2 + (lane >> 5);
+  if (r == 1 || r == 5) {
+    const int idx = r == 1 ? 0 : 1;
+    const int row = wn * 64 + idx * 32 + (lane & 31);
+    f.w[idx] = *reinterpret_cast<const bf16x8 *>(sw + row * 128 + big::swz(row, kc) * 16);
+  } else {
+    const int idx = r == 0 ? 0 : r - 1;
+    const int row = wm * 128 + idx * 32 + (lane & 31);
+    f.x[idx] = *reinterpret_cast<const bf16x8 *>(sa + row * 128 + big::swz(row, kc) * 16);
+  }
+}
+
+__device__ __forceinline__ void mfma(f32x16 (&acc)[2][4], const Frag &f, int q) {
+  const int j = q >> 2, i = q & 3;
+  acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.w[j], f.x[i], acc[j][i], 0, 0, 0);
+}
+
+}  // namespace big8
+
+template <class Epi>
+__global__ __launch_bounds__(512, 1) void gemm_bf16_big8_kernel(const bf16 *A, const bf16 *W,
+                                                                int M, int N, int K, Epi epi) {
+  using namespace big;
+  // LDS as in gemm_bf16_big_kernel; the write-back stages 8 x 32 rows of 68
+  // floats in [0, 70 KB)
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[kSmem];
+  static_assert(1024 + 256 * sizeof(typename Epi::Row) <= kStage, "row records fit one stage");
+  static_assert(8 * 32 * 68 * 4 <= kWBase, "staged write-back fits the activation stages");
+  const int tiles_m = (M + 255) / 256, tiles_n = N / 256;
+  int tm, tn;
+  tile_coords(xcd_remap(blockIdx.x, gridDim.x), tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * 256, n0 = tn * 256;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 2, wn = wave & 3;
+  const int q0 = wave * 4;  // this wavefront's load instructions q0 .. q0 + 3 of each operand
+  const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void *)smem;
+  f32x16 acc[2][4];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[j][i] = f32x16{};
+  const int nk = K / 64;
+  auto load_a = [&](int sa, int kt, int p) {
+    load_lds(lds0 + sa * kStage, q0 + p, A, M, K, m0, kt * 64, lane);
+  };
+  auto load_w = [&](int kt, int p) {
+    load_lds(lds0 + kWBase + (kt & 1) * kStage, q0 + p, W, N, K, n0, kt * 64, lane);
+  };
+
+  const typename Epi::Row rec = epi.row(min(m0 + (tid & 255), M - 1));
+  const f32x4 bias = tid < 64 ? epi.bias4(n0 + tid * 4) : f32x4{};
+  // k-tiles 0 and 1 of both operands, then wait for k-tile 0 only
+#pragma unroll
+  for (int p = 0; p < 4; ++p) load_a(0, 0, p);
+#pragma unroll
+  for (int p = 0; p < 4; ++p) load_w(0, p);
+  if (nk > 1) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) load_a(1, 1, p);
+#pragma unroll
+    for (int p = 0; p < 4; ++p) load_w(1, p);
+    barrier_vm<8>();
+  } else {
+    barrier();
+  }
+  big8::Frag fa, fb;
+#pragma unroll
+  for (int r = 0; r < 6; ++r) big8::read_frag(fa, r, smem, smem + kWBase, 0, wm, wn, lane);
+
+  int sa0 = 0, sa1 = 1, sa2 = 2;
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    const unsigned char *ac = smem + sa0 * kStage, *wc = smem + kWBase + (kt & 1) * kStage;
+    const unsigned char *an = smem + sa1 * kStage, *wnx = smem + kWBase + ((kt + 1) & 1) * kStage;
+    const bool a2 = kt + 2 < nk;
+    // k16 steps 0..2: the fragments of the next step, then two loads: the
+    // second half of the weight rows of k-tile kt+1 (step 0; k-tile 1 was
+    // loaded whole in the prologue), the activation rows of k-tile kt+2 into
+    // the stage k-tile kt-1 left (steps 1 and 2)
+#pragma unroll
+    for (int st = 0; st < 3; ++st) {
+      big8::Frag &fc = (st & 1) ? fb : fa;
+      big8::Frag &fn = (st & 1) ? fa : fb;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        big8::mfma(acc, fc, q);
+        if (q < 6) big8::read_frag(fn, q, ac, wc, st + 1, wm, wn, lane);
+        else if (st == 0 && kt > 0) load_w(kt + 1, 2 + (q - 6));
+        else if (st > 0 && a2) load_a(sa2, kt + 2, (st - 1) * 2 + (q - 6));
+        pin();
+      }
+    }
+    // k16 step 3: barrier (k-tile kt+1 complete -- only the activation loads
+    // of k-tile kt+2 may still be in flight -- and every wavefront done with
+    // k-tile kt), the first fragments of k-tile kt+1, the first half of the
+    // weight rows of k-tile kt+2 into the weight stage of k-tile kt
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      big8::mfma(acc, fb, q);
+      pin();
+    }
+    if (a2) barrier_vm<4>();
+    else barrier();
+    pin();
+#pragma unroll
+    for (int q = 2; q < 8; ++q) {
+      big8::mfma(acc, fb, q);
+      big8::read_frag(fa, q - 2, an, wnx, 0, wm, wn, lane);
+      if (q >= 6 && a2) load_w(kt + 2, q - 6);
+      pin();
+    }
+    const int t = sa0;
+    sa0 = sa1;
+    sa1 = sa2;
+    sa2 = t;
+  }
+  {  // last k-tile: no loads in flight
+    const unsigned char *ac = smem + sa0 * kStage, *wc = smem + kWBase + ((nk - 1) & 1) * kStage;
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      big8::Frag &fc = (st & 1) ? fb : fa;
+      big8::Frag &fn = (st & 1) ? fa : fb;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        big8::mfma(acc, fc, q);
+        if (st < 3 && q < 6) big8::read_frag(fn, q, ac, wc, st + 1, wm, wn, lane);
+        pin();
+      }
+    }
+  }
+  unsigned char *side = smem + kWBase + (nk & 1) * kStage;
+  if (tid < 64) *reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(side) + tid * 4) = bias;
+  if (tid < 256) reinterpret_cast<typename Epi::Row *>(side + 1024)[tid] = rec;
+  barrier();
+  const f32x4 b = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(side) +
+                                                    wn * 64 + (lane & 15) * 4);
+  write_back_staged<2, 4, 4>(acc, epi, m0 + wm * 128, n0 + wn * 64, M, lane,
+                             reinterpret_cast<float *>(smem) + wave * 32 * 68,
+                             reinterpret_cast<const typename Epi::Row *>(side + 1024) + wm * 128, b);
 }
 
 // ------------------------------------------------------------------ 128x256 tile, two per CU
@@ -1069,8 +1231,15 @@ static hipError_t run_bf16(const void *a, const void *w, int m, int n, int k, co
   const bf16 *A = static_cast<const bf16 *>(a), *W = static_cast<const bf16 *>(w);
   switch (gemm_tile_kind(DType::BF16, m, n, k)) {
     case GEMM_TILE_256:
-      launch_kernel(gemm_bf16_big_kernel<Epi>, ((m + 255) / 256) * (n / 256), 256, 0, s,
-                    A, W, m, n, k, epi);
+      // eight wavefronts where the write-back is a large share of a tile
+      // (K < 2048: fc1, QKV, the output projection), four where the main
+      // loop dominates and the fewer LDS reads per MFMA win (fc2)
+      if (k < 2048)
+        launch_kernel(gemm_bf16_big8_kernel<Epi>, ((m + 255) / 256) * (n / 256), 512, 0, s, A, W,
+                      m, n, k, epi);
+      else
+        launch_kernel(gemm_bf16_big_kernel<Epi>, ((m + 255) / 256) * (n / 256), 256, 0, s, A, W,
+                      m, n, k, epi);
       break;
     case GEMM_TILE_64x128:
       launch_kernel(gemm_bf16_small_kernel<Epi>,
