@@ -83,6 +83,7 @@ def counter_class(name: str):
     """Timing class of a kernel symbol as rocprofv3 prints it (mangled or not),
     before the split into full and cache-aware layers."""
     tile = ("t256" if ("gemm_bf16_big_kernel" in name or "gemm_bf16_big8_kernel" in name) else
+            "t320" if "gemm_bf16_t320_kernel" in name else
             "t64x128" if "gemm_bf16_small_kernel" in name else
             "t128" if "gemm_bf16_mid_kernel" in name else "t128x256")
     if "gemm_bf16" in name:

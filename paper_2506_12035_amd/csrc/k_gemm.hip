@@ -10,7 +10,8 @@
 //   - applies exact GELU and stores the hidden row  (fc1)
 //
 // bf16 path (v_mfma_f32_32x32x16_bf16, fp32 accumulators): a 256x256 tile
-// (one workgroup per CU; four wavefronts for K >= 2048, eight below) for
+// (one workgroup per CU; four wavefronts for K >= 2048, eight below) or a
+// 320x256 tile (whole 320-token images per tile row, eight wavefronts) for
 // shapes that fill the chip in whole waves, else a 128x256 tile of which two
 // workgroups share a CU, or 128x128 / 64x128 tiles for narrow products.  All
 // load operands straight from global memory into XOR-swizzled LDS stages and
@@ -687,6 +688,196 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_big8_kernel(const bf16 *A, c
                              reinterpret_cast<const typename Epi::Row *>(side + 1024) + wm * 128, b);
 }
 
+// ------------------------------------------------------------------ 320x256 tile, eight wavefronts
+//
+// A 320x256x64 workgroup tile for products over whole images of 320 tokens:
+// one tile row is one image, so a range of b images has b tile rows and a
+// product with N = 1024 runs b * 4 tiles -- exactly one wave of 256 compute
+// units for a 64-image range, where 256x256 tiles make 320 (1.25 waves) --
+// and N = 3072 / 4096 three / four whole waves.  Eight wavefronts of 160x64
+// (2 x 5 accumulator blocks, 160 accumulation registers each; two wavefronts
+// share a SIMD), the 256x256 tile's 128-byte swizzled rows and direct-to-LDS
+// loads, two 40 KB activation stages and two 32 KB weight stages (144 KB).
+// Each k-tile's loads go out right after the barrier that frees their stage,
+// one k-tile ahead of use.  Per k16 step a wavefront reads 7 fragments for 10
+// MFMAs (5 activation, 2 weight).  Accumulation is the same chain of k16
+// steps in ascending order as every other tile, so results are bitwise
+// those of the 256x256 tile.
+namespace t320 {
+
+constexpr int kBM = 320;
+constexpr int kAStage = kBM * 128;      // 40 KB: 320 rows x 64 k
+constexpr int kWStage = 256 * 128;      // 32 KB
+constexpr int kWBase = 2 * kAStage;     // weight stages start at 80 KB
+constexpr int kSmem = kWBase + 2 * kWStage;  // 144 KB
+constexpr int kALoads = kBM / 8 / 8;    // 1 KB load instructions per wavefront per k-tile: 5
+constexpr int kWLoads = 256 / 8 / 8;    // 4
+constexpr int kLoads = kALoads + kWLoads;
+constexpr int kWbStride = 68;           // floats per staged row (64 + 4)
+static_assert(8 * 32 * kWbStride * 4 <= kWBase, "staged write-back fits the activation stages");
+
+// One set of fragments, refilled as the MFMAs of a k16 step release them.
+struct Frag {
+  bf16x8 x[5];  // activation rows (MFMA B operand)
+  bf16x8 w[2];  // weight rows (MFMA A operand)
+};
+
+// Fragment r (0..4: activation row block r; 5, 6: weight row block r - 5) of
+// k16 step s from a stage pair.
+__device__ __forceinline__ void read_frag(Frag &f, int r, const unsigned char *sa,
+                                          const unsigned char *sw, int s, int wm, int wn,
+                                          int lane) {
+  const int kc = s * 2 + (lane >> 5);
+  if (r >= 5) {
+    const int row = wn * 64 + (r - 5) * 32 + (lane & 31);
+    f.w[r - 5] = *reinterpret_cast<const bf16x8 *>(sw + row * 128 + big::swz(row, kc) * 16);
+  } else {
+    const int row = wm * 160 + r * 32 + (lane & 31);
+    f.x[r] = *reinterpret_cast<const bf16x8 *>(sa + row * 128 + big::swz(row, kc) * 16);
+  }
+}
+
+// MFMA q of a k16 step: column block q / 5, row block q % 5.
+__device__ __forceinline__ void mfma(f32x16 (&acc)[2][5], const Frag &f, int q) {
+  const int j = q / 5, i = q % 5;
+  acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.w[j], f.x[i], acc[j][i], 0, 0, 0);
+}
+
+// 1 KB of an operand into LDS at `lds` (wave-uniform): the scalar base is the
+// operand at the k-tile's first column, `off` the lane's byte offset from it
+// (32-bit: the host keeps every operand below 2^31 elements).
+__device__ __forceinline__ void load_lds(unsigned lds, const bf16 *base, uint32_t off) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(off), "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds))
+               : "memory", "m0");
+}
+
+}  // namespace t320
+
+template <class Epi>
+__global__ __launch_bounds__(512, 1) void gemm_bf16_t320_kernel(const bf16 *A, const bf16 *W,
+                                                                 int M, int N, int K, Epi epi) {
+  using namespace t320;
+  // activation stages at [0, 80K), weight stages at [80K, 144K); after the
+  // main loop the write-back stages rows in [0, 68K) and keeps the tile's
+  // biases and row records in the weight stage the last k-tile left free
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[kSmem];
+  static_assert(1024 + kBM * sizeof(typename Epi::Row) <= kWStage, "row records fit one stage");
+  const int tiles_m = (M + kBM - 1) / kBM, tiles_n = N / 256;
+  int tm, tn;
+  tile_coords(xcd_remap(blockIdx.x, gridDim.x), tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * kBM, n0 = tn * 256;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 2, wn = wave & 3;
+  const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void *)smem;
+  f32x16 acc[2][5];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int i = 0; i < 5; ++i) acc[j][i] = f32x16{};
+  const int nk = K / 64;
+  // This wavefront's load p of every k-tile: p < 5 moves activation rows
+  // 8 q .. 8 q + 7 (q = 5 wave + p of the tile's 40 blocks), p >= 5 weight
+  // rows (q = 4 wave + p - 5 of 32); lane l writes row 8 q + l / 8 at
+  // physical chunk l % 8, which holds logical chunk swz(row, l % 8).
+  // Activation rows past M repeat row M - 1 (their results are never stored).
+  uint32_t off[kLoads];
+#pragma unroll
+  for (int p = 0; p < kLoads; ++p) {
+    const bool is_a = p < kALoads;
+    const int q = is_a ? wave * kALoads + p : wave * kWLoads + (p - kALoads);
+    const int r = q * 8 + (lane >> 3);
+    const int row = is_a ? min(m0 + r, M - 1) : n0 + r;
+    off[p] = (uint32_t)(row * K + big::swz(r, lane & 7) * 8) * 2u;
+  }
+  auto load = [&](int kt, int p) {
+    const int s = kt & 1;
+    if (p < kALoads)
+      load_lds(lds0 + s * kAStage + (wave * kALoads + p) * 1024, A + kt * 64, off[p]);
+    else
+      load_lds(lds0 + kWBase + s * kWStage + (wave * kWLoads + p - kALoads) * 1024, W + kt * 64,
+               off[p]);
+  };
+
+  const typename Epi::Row rec = epi.row(min(m0 + min(tid, kBM - 1), M - 1));
+  const f32x4 bias = tid < 64 ? epi.bias4(n0 + tid * 4) : f32x4{};
+  // k-tiles 0 and 1, then wait for k-tile 0 only
+#pragma unroll
+  for (int p = 0; p < kLoads; ++p) load(0, p);
+  if (nk > 1) {
+#pragma unroll
+    for (int p = 0; p < kLoads; ++p) load(1, p);
+    big::barrier_vm<kLoads>();
+  } else {
+    big::barrier();
+  }
+  // Per k16 step: MFMA q uses weight block q / 5 and activation block q % 5.
+  // The step's own x4 and w1 are read beside MFMAs 0 and 1 (their previous
+  // values are last used by MFMA 9 of the step before); beside MFMAs 5..9
+  // the next step's w0, x0, x1, x2, x3 replace the ones MFMAs 4..8 used last.
+  Frag f;
+  read_frag(f, 5, smem, smem + kWBase, 0, wm, wn, lane);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) read_frag(f, r, smem, smem + kWBase, 0, wm, wn, lane);
+  constexpr int kNext[5] = {5, 0, 1, 2, 3};  // fragment read beside MFMA 5 + i
+
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    const int c = kt & 1, n = c ^ 1;
+    const unsigned char *ac = smem + c * kAStage, *wc = smem + kWBase + c * kWStage;
+    const unsigned char *an = smem + n * kAStage, *wnx = smem + kWBase + n * kWStage;
+    const bool more = kt + 2 < nk;  // k-tile kt+2 exists
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+#pragma unroll
+      for (int q = 0; q < 10; ++q) {
+        t320::mfma(acc, f, q);
+        if (q == 0) read_frag(f, 4, ac, wc, st, wm, wn, lane);
+        if (q == 1) read_frag(f, 6, ac, wc, st, wm, wn, lane);
+        // loads 5..8 of k-tile kt+1 (loads 0..4 went out in the step 3 of
+        // k-tile kt-1; k-tile 1 was loaded whole in the prologue)
+        if (kt > 0 && st == 0 && q >= 2 && q <= 4) load(kt + 1, kALoads + q - 2);
+        if (kt > 0 && st == 1 && q == 2) load(kt + 1, kLoads - 1);
+        // step 3: barrier (k-tile kt+1 landed, every wavefront done with
+        // k-tile kt), then the next k-tile's first fragments and loads 0..4
+        // of k-tile kt+2 into the stages k-tile kt leaves
+        if (st == 3 && q == 4) big::barrier();
+        if (q >= 5) {
+          if (st < 3) read_frag(f, kNext[q - 5], ac, wc, st + 1, wm, wn, lane);
+          else read_frag(f, kNext[q - 5], an, wnx, 0, wm, wn, lane);
+          if (st == 3 && more) load(kt + 2, q - 5);
+        }
+        big::pin();
+      }
+    }
+  }
+  {  // last k-tile: no loads in flight
+    const int c = (nk - 1) & 1;
+    const unsigned char *ac = smem + c * kAStage, *wc = smem + kWBase + c * kWStage;
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+#pragma unroll
+      for (int q = 0; q < 10; ++q) {
+        t320::mfma(acc, f, q);
+        if (q == 0) read_frag(f, 4, ac, wc, st, wm, wn, lane);
+        if (q == 1) read_frag(f, 6, ac, wc, st, wm, wn, lane);
+        if (st < 3 && q >= 5) read_frag(f, kNext[q - 5], ac, wc, st + 1, wm, wn, lane);
+        big::pin();
+      }
+    }
+  }
+  unsigned char *side = smem + kWBase + (nk & 1) * kWStage;
+  if (tid < 64) *reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(side) + tid * 4) = bias;
+  if (tid < kBM) reinterpret_cast<typename Epi::Row *>(side + 1024)[tid] = rec;
+  big::barrier();
+  const f32x4 b = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(side) +
+                                                    wn * 64 + (lane & 15) * 4);
+  write_back_staged<2, 5, 4>(acc, epi, m0 + wm * 160, n0 + wn * 64, M, lane,
+                             reinterpret_cast<float *>(smem) + wave * 32 * kWbStride,
+                             reinterpret_cast<const typename Epi::Row *>(side + 1024) + wm * 160, b);
+}
+
 // ------------------------------------------------------------------ 128x256 tile, two per CU
 //
 // A 128x256x32 workgroup tile on four wavefronts of 64x128 (8 accumulators,
@@ -1209,7 +1400,15 @@ int gemm_tile_kind(DType dt, int32_t m, int32_t n, int32_t k) {
   const long tiles = (long)((m + 255) / 256) * (n / 256);
   const long waves = (tiles + cus - 1) / cus;
   const double fill = (double)tiles / (double)(waves * cus);
-  if (fill >= 0.45) return GEMM_TILE_256;
+  if (fill >= 0.45) {
+    // the 320x256 tile where its whole waves take less time than the
+    // 256x256 tile's, counting a wave as its tile area (whole 320-token
+    // images at N = 1024 / 3072: 1 wave against 1.25, 3 against 3.75)
+    const long tiles320 = (long)((m + t320::kBM - 1) / t320::kBM) * (n / 256);
+    const long waves320 = (tiles320 + cus - 1) / cus;
+    if (waves320 * t320::kBM < waves * 256) return GEMM_TILE_320;
+    return GEMM_TILE_256;
+  }
   if (k % small::kBK == 0 && (long)((m + 127) / 128) * (n / 256) * 2 < cus) {
     // narrow products that 128x128 tiles still spread over half the compute
     // units or more take them (the cache-aware output projection and fc2 of
@@ -1240,6 +1439,10 @@ static hipError_t run_bf16(const void *a, const void *w, int m, int n, int k, co
       else
         launch_kernel(gemm_bf16_big_kernel<Epi>, ((m + 255) / 256) * (n / 256), 256, 0, s, A, W,
                       m, n, k, epi);
+      break;
+    case GEMM_TILE_320:
+      launch_kernel(gemm_bf16_t320_kernel<Epi>, ((m + t320::kBM - 1) / t320::kBM) * (n / 256), 512,
+                    0, s, A, W, m, n, k, epi);
       break;
     case GEMM_TILE_64x128:
       launch_kernel(gemm_bf16_small_kernel<Epi>,

@@ -116,7 +116,8 @@ enum KClass {
   K_HEAD_GATE_MOD, K_HEAD_OUT_STEP, K_GEMM_QKV_S, K_GEMM_O_S, K_GEMM_FC1_S, K_GEMM_FC2_S,
   K_GEMM_EMBED_S, K_GEMM_HEAD_S, K_GEMM_HEAD_SILU_S, K_TRANSPOSE, K_GEMM_QKV_M, K_GEMM_O_M,
   K_GEMM_FC1_M, K_GEMM_FC2_M, K_GEMM_EMBED_M, K_GEMM_HEAD_M, K_GEMM_HEAD_SILU_M,
-  K_ATTN_RES_SC, K_ATTN_W8, K_ATTN_SC,
+  K_ATTN_RES_SC, K_ATTN_W8, K_ATTN_SC, K_GEMM_QKV_I, K_GEMM_O_I, K_GEMM_FC1_I, K_GEMM_FC2_I,
+  K_GEMM_EMBED_I, K_GEMM_HEAD_I, K_GEMM_HEAD_SILU_I,
   K_NCLASS
 };
 const char *const kClassNames[K_NCLASS] = {
@@ -133,7 +134,8 @@ const char *const kClassNames[K_NCLASS] = {
     "gemm_embed_t64x128", "gemm_head_t64x128", "gemm_head_silu_t64x128", "transpose",
     "gemm_qkv_t128",     "gemm_o_t128",    "gemm_fc1_t128",     "gemm_fc2_t128",
     "gemm_embed_t128",   "gemm_head_t128", "gemm_head_silu_t128", "attention_res_scores", "attention_q256",
-    "attention_scores"};
+    "attention_scores",  "gemm_qkv_t320",  "gemm_o_t320",      "gemm_fc1_t320",
+    "gemm_fc2_t320",     "gemm_embed_t320", "gemm_head_t320",  "gemm_head_silu_t320"};
 static_assert(sizeof(kClassNames) / sizeof(kClassNames[0]) == K_NCLASS, "one name per class");
 
 // Launches inside marche_step in layers where not every token of every image
@@ -158,6 +160,17 @@ const char *class_name(int i) {
 int gemm_class(int base, DType dt, int32_t m, int32_t n, int32_t k) {
   const int kind = gemm_tile_kind(dt, m, n, k);
   if (kind == GEMM_TILE_256) return base + 1;
+  if (kind == GEMM_TILE_320) {
+    switch (base) {
+      case K_GEMM_QKV: return K_GEMM_QKV_I;
+      case K_GEMM_O: return K_GEMM_O_I;
+      case K_GEMM_FC1: return K_GEMM_FC1_I;
+      case K_GEMM_FC2: return K_GEMM_FC2_I;
+      case K_GEMM_EMBED: return K_GEMM_EMBED_I;
+      case K_GEMM_HEAD: return K_GEMM_HEAD_I;
+      default: return K_GEMM_HEAD_SILU_I;
+    }
+  }
   if (kind == GEMM_TILE_128) {
     switch (base) {
       case K_GEMM_QKV: return K_GEMM_QKV_M;

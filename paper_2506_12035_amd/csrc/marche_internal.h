@@ -131,9 +131,12 @@ hipError_t launch_gemm_embed(DType dt, const void *a, const void *w, const float
                              int32_t n_enc, int32_t n_buf, int32_t n_known, int32_t n_tokens,
                              hipStream_t s);
 // bf16 GEMM workgroup tile for an M x N x K product: 128x256 (two workgroups
-// per CU), 256x256 (one per CU), 128x128 (narrow products on a few thousand
-// rows) or 64x128 (small products).
-enum GemmTile { GEMM_TILE_128x256 = 0, GEMM_TILE_256 = 1, GEMM_TILE_64x128 = 2, GEMM_TILE_128 = 3 };
+// per CU), 256x256 or 320x256 (one per CU), 128x128 (narrow products on a few
+// thousand rows) or 64x128 (small products).
+enum GemmTile {
+  GEMM_TILE_128x256 = 0, GEMM_TILE_256 = 1, GEMM_TILE_64x128 = 2, GEMM_TILE_128 = 3,
+  GEMM_TILE_320 = 4
+};
 int gemm_tile_kind(DType dt, int32_t m, int32_t n, int32_t k);
 // Compute units of the current device (queried once per device, then cached).
 int device_cu_count();
