@@ -751,7 +751,11 @@ marche_status_t marche_encoder_to_decoder(float *x_dec, const float *x_enc, cons
            launch_gemm_embed(dt, workspace, w_de, b_de, M, D, D, x_dec, pe_dec, known, n_enc, n_buf,
                              n_known, n_tokens, stream));
   }
-  LAUNCH(K_MASK_FILL, 0, 4.0 * D * (2.0 * batch * (n_img - n_known) + 1) + 4.0 * batch * n_img,
+  // algorithmic bytes: the masked rows written, each image position's
+  // positional row and the mask token read once (every image reads the same
+  // rows), the ranks
+  LAUNCH(K_MASK_FILL, 0,
+         4.0 * D * ((double)batch * (n_img - n_known) + n_img + 1) + 4.0 * batch * n_img,
          launch_mask_fill(x_dec, mask, pe_dec, rank, batch, n_tokens, n_buf, n_known, D, stream));
   return MARCHE_OK;
 }
