@@ -154,3 +154,29 @@ def test_no_generating_ablation_against_hand_composed_layers():
         assert not np.allclose(with_g.k_caches[l][:, gen], kcs[l][:, gen])
     # the rows both variants recompute see different keys at G, so they differ too
     assert not np.allclose(res.x_out[cache], with_g.x_out[cache])
+
+
+def test_decoder_input_row_kinds_and_positional_add():
+    """The decoder input's rows (Eq. 2's stand-in): each buffer position holds
+    the class row, each known image token its own value row (value_emb is
+    indexed by image position j - n_buf), every other position the shared mask
+    row, and the positional row adds on top of each.  Distinct random rows make
+    a wrong branch, a value row taken at j instead of j - n_buf, or a dropped
+    positional term fail."""
+    rng = np.random.default_rng(11)
+    n_buf, n_img, d = 3, 9, 5
+    cls = rng.standard_normal(d)
+    value = rng.standard_normal((n_img, d))
+    mask = rng.standard_normal(d)
+    known = [n_buf + 1, n_buf + 4, n_buf + 8]
+    zero = np.zeros((n_buf + n_img, d))
+    x0 = step.decoder_input(cls, value, mask, zero, known, n_buf)
+    for j in range(n_buf + n_img):
+        want = cls if j < n_buf else value[j - n_buf] if j in known else mask
+        np.testing.assert_array_equal(x0[j], want)
+    pos = rng.standard_normal((n_buf + n_img, d))
+    np.testing.assert_allclose(step.decoder_input(cls, value, mask, pos, known, n_buf), x0 + pos,
+                               rtol=0, atol=1e-15)
+    # the order in which known tokens are listed does not matter
+    np.testing.assert_array_equal(step.decoder_input(cls, value, mask, pos, known[::-1], n_buf),
+                                  step.decoder_input(cls, value, mask, pos, known, n_buf))
