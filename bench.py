@@ -61,8 +61,31 @@ def source_hash(kernel: str) -> str:
         fam = "select"
     else:
         fam = "elementwise"
-    with open(os.path.join(ROOT, KERNEL_SOURCES[fam]), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    with open(os.path.join(ROOT, KERNEL_SOURCES[fam])) as f:
+        return hashlib.sha256(code_only(f.read()).encode()).hexdigest()[:16]
+
+
+def code_only(src: str) -> str:
+    """A source file's code with its comments and blank space removed, so
+    that a change to the comments leaves the hash of the kernels unchanged."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        if src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+        elif src[i] == '"':  # string literal: copied whole
+            j = i + 1
+            while j < n and src[j] != '"':
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        else:
+            out.append(src[i])
+            i += 1
+    return " ".join("".join(out).split())
 
 
 def traffic_for(kernel: str, workload: str):

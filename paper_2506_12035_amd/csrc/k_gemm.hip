@@ -1376,24 +1376,26 @@ __global__ __launch_bounds__(256) void gemm_bf16_small_kernel(const bf16 *A, con
                              rows_lds + wm * 32, bias);
 }
 
-// Tile choice.  The 256x256 tile (one workgroup per CU) when its tiles fill
+// Tile choice.  A large tile (one workgroup per CU) when 256x256 tiles fill
 // at least 45% of their last wave over the compute units: a partly filled
 // last wave runs at a higher clock under the chip's power limit, and beside
 // another image range's kernels when the step runs as ranges on streams
 // (which is why the bound is this low: with a single range, such a wave
-// leaves the rest of the chip idle).
+// leaves the rest of the chip idle).  Of the two large tiles, the 320x256
+// one when its waves cover fewer rows than the 256x256 tile's.
 // Otherwise the 128x256 tile, two workgroups per CU, whose write-backs
 // overlap the other workgroup's main loop and whose finer steps fill the chip
-// better; and when even 128x256 tiles would occupy fewer than half the
-// compute units, the 64x128 tile (K a multiple of 128).  Measured at MAR-L
-// sizes, per 64-image range: every full-layer GEMM takes the 256x256 tile
-// (the output projection alone runs slower on it, 80 vs 75 us, but the
-// overlapped step is faster), and so do the cache-aware fc1 and QKV when a
-// range has more than 2304 active rows (10 tiles of rows); below that they
-// take the 128x256 tile; the cache-aware output projection and fc2 the 64x128
-// one, as do the sampler's per-block GEMMs (a few hundred rows).  Under sustained load the 128x256 tile runs
-// at a lower clock (more operand traffic per flop), which is why it does not
-// replace the large tile outright.
+// better; the 128x128 tile for narrow products it would spread too thinly;
+// and when even 128x256 tiles would occupy fewer than half the compute units,
+// the 64x128 tile (K a multiple of 128).  At MAR-L sizes, per 64-image range:
+// the full-layer QKV, output projection and fc2 take the 320x256 tile (3, 1
+// and 1 whole waves), fc1 the 256x256 tile (5 waves, a tie in rows that
+// measured faster on 256x256); the cache-aware fc1 and QKV take the 256x256
+// tile when a range has more than 2304 active rows (10 tiles of rows), else
+// the 128x256 tile; the cache-aware output projection and fc2 the 128x128
+// tile; the sampler's per-block GEMMs (a few hundred rows) the 64x128 tile.
+// Under sustained load the 128x256 tile runs at a lower clock (more operand
+// traffic per flop), which is why it does not replace the large tiles.
 int gemm_tile_kind(DType dt, int32_t m, int32_t n, int32_t k) {
   if (dt != DType::BF16 || m <= 0) return GEMM_TILE_128x256;
   const long cus = device_cu_count();

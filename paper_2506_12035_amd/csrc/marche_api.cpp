@@ -103,10 +103,11 @@ marche_status_t check_model(const marche_model_t *m) {
 // ------------------------------------------------------------------ profiling
 
 // One class per kernel symbol.  The attention kernel is instantiated per
-// query-chunk width (1, 2 or 4 wavefronts of 32 queries), chosen from the
-// largest active set of the call; each bf16 GEMM has a 128x256 and a 256x256
-// (class + 1) tile instantiation, chosen from its shape (fp32 GEMMs are timed
-// under the first).
+// query-chunk width (1, 2, 4 or 8 wavefronts of 32 queries), chosen from the
+// largest active set of the call; each bf16 GEMM has a 128x256, a 256x256
+// (class + 1), a 64x128 (_S), a 128x128 (_M) and a 320x256 (_I) tile
+// instantiation, chosen from its shape (fp32 GEMMs are timed under the
+// first).
 enum KClass {
   K_ROW_MAP, K_GATHER_LN, K_GEMM_QKV, K_GEMM_QKV_L, K_ATTN_W1, K_ATTN_W2, K_ATTN_W4,
   K_ATTN_SCORES, K_GEMM_O, K_GEMM_O_L, K_GEMM_FC1, K_GEMM_FC1_L, K_GEMM_FC2, K_GEMM_FC2_L,

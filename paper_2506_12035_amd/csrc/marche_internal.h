@@ -116,8 +116,6 @@ hipError_t launch_gemm_resid(DType dt, const void *a, const void *w, const float
                              hipStream_t s);
 hipError_t launch_gemm_gelu(DType dt, const void *a, const void *w, const float *bias, int32_t m,
                             int32_t n, int32_t k, void *h, hipStream_t s);
-// Whether a bf16 GEMM of this shape runs on the 256x256 tile (else 128x128);
-// each tile is its own kernel symbol.
 // Sampler GEMMs: out[r][c] = act(C + bias) as out_dt (row-major, ld = n), act
 // SiLU or the identity; a float32 GEMM writes float32 only.
 hipError_t launch_gemm_plain(DType dt, const void *a, const void *w, const float *bias, int32_t m,
