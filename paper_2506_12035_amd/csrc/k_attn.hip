@@ -471,11 +471,15 @@ __global__ __launch_bounds__(QB * 64) void attn_reg_kernel(AttnArgs a, int chunk
   // the stores of the next tile (and the waits for its loads) behind the
   // whole tile step, which would otherwise start them, and wait, in the
   // middle of it.
+  // A wavefront whose 32 queries all lie past the active set (the last query
+  // chunk of a long sequence) keeps loading, storing and meeting the
+  // barriers but skips the tile step, leaving its SIMD to the others.
+  const bool live = q0 + wave * 32 < na;  // uniform over the wavefront
   auto step = [&](int t, auto slot) {
     constexpr int SL = decltype(slot)::value;
     gload(rt, t + 1);
     __builtin_amdgcn_sched_barrier(0);
-    tile(smem + SL * kSlotBytes, qf, acc, m_run, l_run, sl2, lane);
+    if (live) tile(smem + SL * kSlotBytes, qf, acc, m_run, l_run, sl2, lane);
     __builtin_amdgcn_sched_barrier(0);
     sstore(rt, SL ^ 1);
     __syncthreads();
