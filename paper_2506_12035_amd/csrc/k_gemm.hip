@@ -767,8 +767,8 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_t320_kernel(const bf16 *A, c
   const int tiles_m = (M + kBM - 1) / kBM, tiles_n = N / 256;
   int tm, tn;
   // groups of 4 tile rows: an XCD's 32 concurrent tiles cover 4 rows x 8
-  // columns, so a row's activation panel serves two rounds of QKV's 12
-  // columns from the L2 (QKV 117 -> 114.5 us per range against groups of 8)
+  // columns (QKV 117 -> 114.5 us per range against groups of 8, with about
+  // the same L2 fetch bytes)
   tile_coords<4>(xcd_remap(blockIdx.x, gridDim.x), tiles_m, tiles_n, tm, tn);
   const int m0 = tm * kBM, n0 = tn * 256;
   const int tid = threadIdx.x, lane = tid & 63;
