@@ -698,8 +698,9 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_big8_kernel(const bf16 *A, c
 // (2 x 5 accumulator blocks, 160 accumulation registers each; two wavefronts
 // share a SIMD), the 256x256 tile's 128-byte swizzled rows and direct-to-LDS
 // loads, two 40 KB activation stages and two 32 KB weight stages (144 KB).
-// Each k-tile's loads go out right after the barrier that frees their stage,
-// one k-tile ahead of use.  Per k16 step a wavefront reads 7 fragments for 10
+// A k-tile's activation rows go out right after the barrier that frees their
+// stage, one k-tile ahead of use; its weight rows, which the L2 serves, beside
+// the first MFMAs of the next k-tile.  Per k16 step a wavefront reads 7 fragments for 10
 // MFMAs (5 activation, 2 weight).  Accumulation is the same chain of k16
 // steps in ascending order as every other tile, so results are bitwise
 // those of the 256x256 tile.
