@@ -1386,15 +1386,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_small_kernel(const bf16 *A, con
 // another image range's kernels when the step runs as ranges on streams
 // (which is why the bound is this low: with a single range, such a wave
 // leaves the rest of the chip idle).  Of the two large tiles, the 320x256
-// one when its waves cover fewer rows than the 256x256 tile's.
+// one when its waves cover no more rows than the 256x256 tile's.
 // Otherwise the 128x256 tile, two workgroups per CU, whose write-backs
 // overlap the other workgroup's main loop and whose finer steps fill the chip
 // better; the 128x128 tile for narrow products it would spread too thinly;
 // and when even 128x256 tiles would occupy fewer than half the compute units,
 // the 64x128 tile (K a multiple of 128).  At MAR-L sizes, per 64-image range:
-// the full-layer QKV, output projection and fc2 take the 320x256 tile (3, 1
-// and 1 whole waves), fc1 the 256x256 tile (5 waves, a tie in rows that
-// measured faster on 256x256); the cache-aware fc1 and QKV take the 256x256
+// every full-layer product takes the 320x256 tile (QKV 3, output projection
+// and fc2 1, fc1 4 whole waves); the cache-aware fc1 and QKV take the 256x256
 // tile when a range has more than 2304 active rows (10 tiles of rows), else
 // the 128x256 tile; the cache-aware output projection and fc2 the 128x128
 // tile; the sampler's per-block GEMMs (a few hundred rows) the 64x128 tile.
@@ -1407,12 +1406,13 @@ int gemm_tile_kind(DType dt, int32_t m, int32_t n, int32_t k) {
   const long waves = (tiles + cus - 1) / cus;
   const double fill = (double)tiles / (double)(waves * cus);
   if (fill >= 0.45) {
-    // the 320x256 tile where its whole waves take less time than the
+    // the 320x256 tile where its whole waves take no more time than the
     // 256x256 tile's, counting a wave as its tile area (whole 320-token
-    // images at N = 1024 / 3072: 1 wave against 1.25, 3 against 3.75)
+    // images at N = 1024 / 3072 / 4096: 1 wave against 1.25, 3 against
+    // 3.75, 4 against 5 -- the tie, fc1, measured 176.8 against 180.8 us)
     const long tiles320 = (long)((m + t320::kBM - 1) / t320::kBM) * (n / 256);
     const long waves320 = (tiles320 + cus - 1) / cus;
-    if (waves320 * t320::kBM < waves * 256) return GEMM_TILE_320;
+    if (waves320 * t320::kBM <= waves * 256) return GEMM_TILE_320;
     return GEMM_TILE_256;
   }
   if (k % small::kBK == 0 && (long)((m + 127) / 128) * (n / 256) * 2 < cus) {
